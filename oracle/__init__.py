@@ -1,0 +1,16 @@
+"""CPU oracle for the ReDASH garbled scaling gadget.
+
+TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import, call, link or execute anything
+under ``oracle/``.  The product path (``paper_2506_14489_amd``) must never
+touch it and fails loudly when its HIP library is missing.
+
+* ``rns``       -- value-level residue arithmetic (plain Python integers)
+* ``oracle``    -- ctypes wrapper of ``gc_oracle.c`` (plain C: AES-128 from
+                   FIPS-197, label hash, PRG, garble, encode, eval, decode)
+
+Parity unpinned by the paper: the exact label bits (hash construction, label
+length, PRG, tweaks, packing).  Those are pinned by FIPS-197 (AES), by the
+label invariants and decode results the tests check, and by the independent
+HIP implementation.
+"""
