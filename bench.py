@@ -1,0 +1,191 @@
+"""Benchmark: garbled scaling gadgets evaluated per second on one MI355X.
+
+A step is one call of redash_eval_scale over the whole workload (the online
+phase of the gadget; garbling and encoding happen before the timed region,
+decoding after it).  Default workload: the batched conv map, 16x64x56x56 =
+3,211,264 gadgets over the first 12 primes, scaled by 37.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "garbled scaling gadgets evaluated/sec (1 GPU) + % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+# int32 vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one lane-op per lane per clock)
+ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, x, sample: int, target_s: float):
+    """The CPU oracle's evaluation, single-threaded, on the first `sample`
+    gadgets of the workload (garbled by the oracle, untimed), repeated until
+    about target_s seconds have been timed."""
+    from oracle import oracle as O
+
+    op = O.make_params(list(w.moduli), list(w.scale_idx), sample, w.seed)
+    t0 = time.time()
+    offs, zin, zout, tab = O.garble(op, 0, sample)
+    X = O.encode(op, x[:sample], zin, offs)
+    log(f"cpu baseline: oracle garbled {sample} gadgets in {time.time() - t0:.1f} s")
+    reps, elapsed = 0, 0.0
+    while elapsed < target_s:
+        t1 = time.perf_counter()
+        Y = O.evaluate(op, 0, sample, X, tab)
+        elapsed += time.perf_counter() - t1
+        reps += 1
+    y, bad = O.decode(op, Y, zout, offs)
+    assert bad.sum() == 0 and np.array_equal(y, np.floor_divide(x[:sample], w.s))
+    return {
+        "value": round(sample * reps / elapsed, 1),
+        "unit": "gadgets/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"oracle eval of the first {sample} gadgets of the {w.name} workload "
+                  f"(oracle-garbled tables), {reps} passes, {elapsed:.1f} s timed; plain C, one thread; "
+                  f"host has {len(os.sched_getaffinity(0))} cores available",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="batched")
+    ap.add_argument("--cpu-sample", type=int, default=1024)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true", help="skip the decode check after timing")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(gadgets are independent: a multi-GPU run would shard them, see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2506_14489_amd import binding as B
+    from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import workloads as WL
+
+    w = WL.by_name(args.workload)
+    n = w.n
+    log(f"workload {w.name}: {n} gadgets, moduli {w.moduli}, s = {w.s}, seed {w.seed}")
+    t0 = time.time()
+    x = WL.make_inputs(w)
+    log(f"inputs ready in {time.time() - t0:.1f} s")
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    params = B.make_params(w.moduli, w.scale_idx, n, w.seed)
+    buf = B.Buffers(params, dev)
+    stream = torch.cuda.current_stream()
+    t0 = time.time()
+    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, stream)
+    xd = torch.from_numpy(x).to(dev)
+    B.redash_encode(params, xd, buf.in_zero, buf.offsets, buf.in_labels, stream)
+    torch.cuda.synchronize()
+    log(f"garbled and encoded on the GPU in {time.time() - t0:.1f} s "
+        f"({buf.sizes['table_words'] * 4 / 1e9:.1f} GB of tables)")
+
+    for _ in range(args.warmup):
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, stream)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / args.steps
+    log(f"eval: {ms_step:.3f} ms per call (events), wall {wall * 1e3 / args.steps:.3f} ms per call")
+
+    check = "skipped"
+    if not args.no_check:
+        B.redash_decode(params, buf.out_labels, buf.out_zero, buf.offsets, buf.y, buf.bad, stream)
+        torch.cuda.synchronize()
+        ok = int(buf.bad.item()) == 0 and np.array_equal(buf.y.cpu().numpy()[:n], np.floor_divide(x, w.s))
+        if not ok:
+            log("decode check FAILED")
+            sys.exit(1)
+        check = f"decode = floor(x/s) with every label valid, all {n} gadgets"
+        log(check)
+
+    gadgets_per_s = n / (ms_step / 1e3)
+    bytes_g = cost.bytes_per_gadget(w.moduli, w.scale_idx)
+    ops_g = cost.ops_per_gadget(w.moduli, w.scale_idx)
+    aes_g = cost.aes_blocks_per_gadget(w.moduli, w.scale_idx)
+    achieved_tops = ops_g * n / (ms_step / 1e3) / 1e12
+    achieved_gbs = bytes_g * n / (ms_step / 1e3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(gadgets_per_s, 1),
+        "unit": "gadgets/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: {n} gadgets" + (f" ({'x'.join(map(str, w.out_shape[1:] if w.out_shape[0] == 1 else w.out_shape))} map)" if w.out_shape else ""),
+            "moduli": list(w.moduli),
+            "scale": w.s,
+            "seed": w.seed,
+            "gates_per_gadget": len(cost.gates(w.moduli, w.scale_idx)),
+            "aes_blocks_per_gadget": aes_g,
+        },
+        "roofline": {
+            "bound": "alu",
+            "achieved": round(achieved_tops, 3),
+            "peak": round(ALU_PEAK_TOPS, 2),
+            "unit": "TOP/s",
+            "frac": round(achieved_tops / ALU_PEAK_TOPS, 4),
+            "traffic": None,
+            "kernel": "k_eval",
+            "ops_per_gadget": ops_g,
+        },
+        "hbm": {
+            "achieved": round(achieved_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
+            "bytes_per_gadget": round(bytes_g, 1),
+        },
+        "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
+        "check": check,
+    }
+    del buf
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,199 @@
+/*
+ * redash.h -- C ABI of the MI355X (gfx950) library for the ReDASH garbled
+ * scaling gadget (Maurer, Sander, Eisenbarth: "ReDASH", arXiv 2506.14489).
+ *
+ * The gadget maps an RNS-encoded activation, held as one arithmetic-garbled
+ * wire label per base modulus, to floor(x / s) where s is one base modulus or
+ * a product of base moduli.  It is ShiftUp by P/2, a division step per factor
+ * of s (Sec. 3.2), the generalized base extension (Sec. 3.3, Eq. rns_to_mrs)
+ * and ShiftDown by P/(2s) (Sec. 3.4).  Every step that is not free label
+ * arithmetic (Sec. 2.3) is a projection gate: hash the digit label, select a
+ * ciphertext row by the label's colour, decrypt.
+ *
+ * Roles (Sec. 2.1): the garbler garbles offline (redash_garble_scale), hands
+ * the evaluator its input labels (redash_encode stands in for the oblivious
+ * transfer) and decodes the returned labels (redash_decode).  The evaluator
+ * runs redash_eval_scale online; that call is the hot path.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named d_* are DEVICE pointers on the current HIP device.  The
+ *    caller allocates and owns every buffer, sized from redash_plan(); the
+ *    library never allocates or frees device memory and keeps no state
+ *    between calls beyond read-only constants.
+ *  - Calls are asynchronous on `stream` (0 = the null stream); they return
+ *    after the launches are queued.  Buffers must stay valid until the stream
+ *    reaches the work.  Calls that write the same buffers must be ordered by
+ *    the caller.
+ *  - Return codes: REDASH_OK (0) or a negative REDASH_E* value; nothing is
+ *    launched when a call returns an error.  Device kernels never trap.
+ *  - Label encoding ("PK32"): a label over Z_m has lambda_m residues, lambda_m
+ *    the least integer with m^lambda_m >= 2^128 (128-bit security, Sec. 2.3
+ *    leaves the length open).  With b_m = bit length of (m-1) and
+ *    g_m = floor(32 / b_m), residue r sits in 32-bit word r / g_m at bit
+ *    b_m * (r % g_m); unused bits are zero.  W_m = ceil(lambda_m / g_m) words.
+ *  - LabelTensor layout (structure of arrays): for base modulus i in base
+ *    order, a block of W_{m_i} * n words; word w of gadget a is at
+ *    block_i + w * n + a.  label_words = n * sum_i W_{m_i}.
+ *  - Offsets (the garbler's global offsets R_m, Sec. 2.3: l_v = l_0 + v R):
+ *    one PK32 label per modulus in base order, offset_words = sum_i W_{m_i}.
+ *  - Garbled tables: one block per projection gate in gate order; gate g with
+ *    input modulus q and output modulus m holds n * (q-1) * W_m words (row
+ *    reduction, Sec. 2.3: the colour-0 row is implicit).  The row of colour
+ *    c in 1..q-1 of gadget a starts at word (a * (q-1) + c - 1) * W_m of the
+ *    gate block.
+ *  - Gate order (the same for every gadget): Phase A (division, Sec. 3.2):
+ *    for each scaling modulus S[a] in ascending order, one gate onto every
+ *    later scaling modulus and then onto every remaining modulus R.  Phase B
+ *    (base extension, Sec. 3.3): for each remaining modulus R[b] in ascending
+ *    order, one gate onto every later remaining modulus and then onto every
+ *    scaling modulus.  gates = k(k-1)/2 + t(k-t).
+ *  - Hash of a projection gate (the paper fixes none): fixed-key AES-128 in
+ *    Matyas-Meyer-Oseas form with the key 00 01 .. 0f, applied to the linear
+ *    orthomorphism sigma(x) = ((x_hi ^ x_lo) << 64) | x_hi of the XOR-fold
+ *    of the input label's PK32 words, tweaked with
+ *    T_j = gadget_id * 2^96 + 4 tau + j, tau = a * gates + g, and
+ *    gadget_id = seed mod 2^32; two blocks (one when m = 2) give a 256-bit
+ *    (128-bit) fraction whose first lambda_m base-m digits are the pad.
+ */
+#ifndef REDASH_H
+#define REDASH_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REDASH_OK 0
+#define REDASH_E_PARAM (-1) /* invalid parameters (see redash_params)             */
+#define REDASH_E_NULL (-2)  /* a required pointer is NULL                          */
+#define REDASH_E_HIP (-3)   /* a HIP launch or runtime call failed                 */
+#define REDASH_E_LABEL (-4) /* reported by callers that read d_bad_count > 0       */
+
+#define REDASH_MAX_K 15
+
+/*
+ * One gadget call: n independent gadget instances with the same base and
+ * scaling factor.
+ *   k           number of base moduli, 2..15.
+ *   moduli      the RNS base (Sec. 2.2): primes, strictly ascending, 2..255,
+ *               with P = prod(moduli) < 2^63.
+ *   t           number of scaling moduli, 1..k-1.
+ *   scale_idx   indices into moduli of the scaling moduli S, strictly
+ *               ascending; s = prod of those moduli (Sec. 3.4: s may be one
+ *               base modulus or a product of several).  P/(2s) must be an
+ *               integer (P even and 2 not in S), because ShiftUp and
+ *               ShiftDown add the constants P/2 and P/(2s) (Sec. 3.4).
+ *   n           number of gadget instances held in the buffers (may be 0).
+ *   seed        garbler seed: keys the garbling PRG; gadget_id = seed mod 2^32.
+ *   a0          global index of the first gadget held in the buffers.  The
+ *               hash tweaks and the PRG are addressed by a0 + local index, so
+ *               any slice of a larger call can be garbled or evaluated alone.
+ * The struct is passed by pointer; unused array entries are ignored.
+ */
+typedef struct {
+    uint32_t k;
+    uint32_t moduli[16];
+    uint32_t t;
+    uint32_t scale_idx[16];
+    uint64_t n;
+    uint64_t seed;
+    uint64_t a0;
+} redash_params;
+
+/* Buffer sizes in 32-bit words for a given redash_params. */
+typedef struct {
+    uint64_t label_words;  /* one LabelTensor (inputs, outputs, zero-labels) */
+    uint64_t table_words;  /* all garbled tables of the n gadgets            */
+    uint32_t offset_words; /* the k offsets R_m                              */
+    uint32_t gates;        /* projection gates per gadget                    */
+} redash_sizes;
+
+/*
+ * Host only, no device work.  Validates `p` and reports the buffer sizes.
+ * Returns REDASH_E_NULL if p or out is NULL, REDASH_E_PARAM if p is invalid.
+ */
+int redash_plan(const redash_params *p, redash_sizes *out);
+
+/*
+ * Garbler, offline phase (Sec. 2.1; Sec. 2.3 projection gates with row
+ * reduction; Sec. 3.4 free ShiftUp/ShiftDown applied to zero-labels).
+ * Writes:
+ *   d_offsets   offset_words: R_m for every modulus (R_m[0] != 0, so the k
+ *               colours of a wire are distinct).
+ *   d_in_zero   label_words: input zero-labels Z of gadgets a0..a0+n-1.
+ *   d_out_zero  label_words: output zero-labels (value 0 after ShiftDown).
+ *   d_tables    table_words: every garbled row (may be NULL when n = 0).
+ * Deterministic in (moduli, scale set, seed, global gadget index).
+ */
+int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero,
+                        uint32_t *d_out_zero, uint32_t *d_tables, hipStream_t stream);
+
+/*
+ * Stand-in for the oblivious transfer of input labels (Sec. 2.1):
+ * X_{a,i} = Z_{a,i} + ((x_a mod P) mod m_i) * R_{m_i}, residue-wise mod m_i.
+ *   d_x         n signed activations (int64), any value (reduced mod P; the
+ *               result is floor(x/s) for x in [-P/2, P/2), Sec. 3.2/3.4).
+ *   d_in_zero   label_words, from redash_garble_scale.
+ *   d_offsets   offset_words, from redash_garble_scale.
+ *   d_in_labels label_words, written.
+ */
+int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_in_zero,
+                  const uint32_t *d_offsets, uint32_t *d_in_labels, hipStream_t stream);
+
+/*
+ * Evaluator, online phase: THE HOT PATH.  Runs the scaling gadget of
+ * Sec. 3.4 on n LabelTensors: per projection gate, colour c = residue 0 of
+ * the digit label, pad = hash (see conventions), E = row[c] + pad (row 0 is
+ * zero), then the free operation of the gate -- Phase A and the recursion of
+ * Phase B: L_dst <- q^{-1} (L_dst - E) mod m (Sec. 3.2 display equation,
+ * Eq. rns_to_mrs); Phase B onto the scaling moduli: Acc_dst <- Acc_dst +
+ * w * E with the mixed-radix weight w = prod of the earlier remaining moduli
+ * (the missing residue of Sec. 3.3 written as the mixed-radix value of the
+ * digits).
+ *   d_in_labels  label_words (read only).
+ *   d_tables     table_words from redash_garble_scale with the same params.
+ *   d_out_labels label_words, written; may not alias d_in_labels.
+ * Output labels carry floor(x/s) under the garbler's output zero-labels.
+ */
+int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
+                      uint32_t *d_out_labels, hipStream_t stream);
+
+/*
+ * Garbler decodes the returned labels (Sec. 2.1): v_i = (Y_i[0] - O_i[0]) *
+ * R_i[0]^{-1} mod m_i, y = CRT(v) in the signed range [-P/2, P/2)
+ * (Sec. 2.4).  A gadget whose label differs from O_i + v_i R_i in any residue
+ * is counted as bad (its d_y entry is still written).
+ *   d_out_labels, d_out_zero  label_words; d_offsets offset_words.
+ *   d_y          n int64, written.
+ *   d_bad_count  one uint64, overwritten with the number of bad gadgets.
+ * Callers that want an error on bad labels read d_bad_count after the stream
+ * completes and report REDASH_E_LABEL when it is nonzero.
+ */
+int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,
+                  const uint32_t *d_offsets, int64_t *d_y, uint64_t *d_bad_count, hipStream_t stream);
+
+/*
+ * The projection-gate hash alone (Sec. 2.3; construction in the conventions
+ * above), for tests and for measuring the AES throughput of the device.
+ *   q, m        input and output modulus (2..255, prime).
+ *   count       number of labels.
+ *   d_labels    W_q * count words, SoA: word w of label a at w * count + a.
+ *   gadget_id   tweak high word.
+ *   d_tau       count uint64 tweaks.
+ *   d_out       W_m * count words, SoA, written.
+ */
+int redash_hash_labels(uint32_t q, uint32_t m, uint64_t count, const uint32_t *d_labels,
+                       uint32_t gadget_id, const uint64_t *d_tau, uint32_t *d_out, hipStream_t stream);
+
+/* Static text for a return code. */
+const char *redash_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REDASH_H */

@@ -1,0 +1,76 @@
+"""Work model of one scaling-gadget instance, used to report throughput
+against hardware roofs.
+
+Per gadget (structure of the gate list in include/redash.h):
+  * algorithmic HBM bytes: the k input labels and k output labels (packed
+    words) plus, per projection gate q -> m, one W_m-word row, read with
+    probability (q-1)/q because the colour-0 row is implicit (row reduction);
+  * AES-128 blocks: two per gate, one when the output modulus is 2;
+  * algorithmic 32-bit integer operations of the table formulation:
+      - per AES block: 10 rounds x 16 (byte extract + table read + XOR)
+        + 4 initial key XORs = 484, plus 12 XORs for tweak and feed-forward;
+      - per gate: W_q + 1 for folding the input label and sigma;
+      - per output word (m > 2): 8 limb multiply-adds of 4 operations each;
+      - per output residue (m > 2): 14 (digit split 3, row add 3, free
+        operation 5, field extract and insert 3); per word for m = 2: 3.
+"""
+
+from __future__ import annotations
+
+AES_OPS_PER_BLOCK = 484 + 12
+LIMB_OPS_PER_WORD = 8 * 4
+OPS_PER_RESIDUE = 14
+
+
+def lam(m: int) -> int:
+    """Residues per label: least lambda with m^lambda >= 2^128."""
+    v, lam_ = 1, 0
+    while v < (1 << 128):
+        v *= m
+        lam_ += 1
+    return lam_
+
+
+def words(m: int) -> int:
+    b = (m - 1).bit_length()
+    g = 32 // b
+    return -(-lam(m) // g)
+
+
+def gates(moduli, scale_idx):
+    """(q, m) per gate in gate order."""
+    S = sorted(scale_idx)
+    R = [i for i in range(len(moduli)) if i not in S]
+    out = []
+    for a, si in enumerate(S):
+        for dst in S[a + 1:] + R:
+            out.append((moduli[si], moduli[dst]))
+    for b, ri in enumerate(R):
+        for dst in R[b + 1:] + S:
+            out.append((moduli[ri], moduli[dst]))
+    return out
+
+
+def bytes_per_gadget(moduli, scale_idx) -> float:
+    labels = 2 * sum(4 * words(m) for m in moduli)
+    rows = sum((q - 1) / q * 4 * words(m) for (q, m) in gates(moduli, scale_idx))
+    return labels + rows
+
+
+def aes_blocks_per_gadget(moduli, scale_idx) -> int:
+    return sum(1 if m == 2 else 2 for (_q, m) in gates(moduli, scale_idx))
+
+
+def ops_per_gadget(moduli, scale_idx) -> int:
+    total = 0
+    for (q, m) in gates(moduli, scale_idx):
+        total += (1 if m == 2 else 2) * AES_OPS_PER_BLOCK + words(q) + 1
+        if m == 2:
+            total += 3 * words(m)
+        else:
+            total += LIMB_OPS_PER_WORD * words(m) + OPS_PER_RESIDUE * lam(m)
+    return total
+
+
+def table_bytes_per_gadget(moduli, scale_idx) -> int:
+    return sum((q - 1) * 4 * words(m) for (q, m) in gates(moduli, scale_idx))

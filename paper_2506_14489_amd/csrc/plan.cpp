@@ -1,0 +1,197 @@
+// Host-side plan: validation, label sizes, gate list, per-modulus constants.
+#include "plan.hpp"
+
+#include <string.h>
+
+namespace redash {
+
+namespace {
+
+bool is_prime(uint32_t v) {
+    if (v < 2) return false;
+    for (uint32_t d = 2; d * d <= v; ++d)
+        if (v % d == 0) return false;
+    return true;
+}
+
+uint32_t bit_length(uint32_t v) {
+    uint32_t b = 0;
+    while (v) {
+        ++b;
+        v >>= 1;
+    }
+    return b;
+}
+
+uint32_t ipow(uint32_t m, uint32_t e) {
+    uint64_t r = 1;
+    for (uint32_t i = 0; i < e; ++i) r *= m;
+    return static_cast<uint32_t>(r);
+}
+
+// Division constants for floor(x / m), x a 32-bit value below x_bound.
+void division_constants(uint32_t m, uint64_t x_bound, ModConst *mc) {
+    if (m == 2) {  // a plain shift; umulhi(x, 2^31) >> 0 = x >> 1
+        mc->divM = 0x80000000u;
+        mc->divS = 0;
+        mc->div_fix = 0;
+        return;
+    }
+    // Round-up magic: s = floor(log2 m), M = ceil(2^(32+s) / m) < 2^32 for m
+    // not a power of two.  The error of x M / 2^(32+s) over x / m is
+    // x (m M - 2^(32+s)) / (m 2^(32+s)); it keeps the floor exact whenever it
+    // stays below 1/m, i.e. x (m M - 2^(32+s)) < 2^(32+s).
+    uint32_t s = bit_length(m) - 1;
+    unsigned __int128 two = static_cast<unsigned __int128>(1) << (32 + s);
+    unsigned __int128 M = (two + m - 1) / m;
+    unsigned __int128 err = M * m - two;
+    if (M < (static_cast<unsigned __int128>(1) << 32) && static_cast<unsigned __int128>(x_bound) * err < two) {
+        mc->divM = static_cast<uint32_t>(M);
+        mc->divS = s;
+        mc->div_fix = 0;
+        return;
+    }
+    // General 32-bit case: l = ceil(log2 m), M' = floor(2^32 (2^l - m) / m) + 1,
+    // q = (t + ((x - t) >> 1)) >> (l - 1) with t = umulhi(x, M').
+    uint32_t l = bit_length(m - 1);
+    unsigned __int128 Mp = ((static_cast<unsigned __int128>(1) << 32) *
+                            ((static_cast<unsigned __int128>(1) << l) - m)) / m + 1;
+    mc->divM = static_cast<uint32_t>(Mp);
+    mc->divS = l - 1;
+    mc->div_fix = 1;
+}
+
+}  // namespace
+
+uint32_t inverse_mod(uint32_t a, uint32_t m) {
+    a %= m;
+    for (uint32_t x = 1; x < m; ++x)
+        if ((a * x) % m == 1) return x;
+    return 0;
+}
+
+uint32_t label_lambda(uint32_t m) {
+    // least lambda with m^lambda >= 2^128, by exact integer comparison
+    const unsigned __int128 limit = ~static_cast<unsigned __int128>(0);  // 2^128 - 1
+    unsigned __int128 p = 1;
+    uint32_t lam = 0;
+    while (p <= limit / m) {  // p * m <= 2^128 - 1, i.e. still below 2^128
+        p *= m;
+        ++lam;
+    }
+    return lam + 1;  // the next power reaches at least 2^128
+}
+
+uint32_t label_words(uint32_t m) {
+    uint32_t g = 32u / bit_length(m - 1);
+    return (label_lambda(m) + g - 1) / g;
+}
+
+void fill_mod_const(uint32_t m, ModConst *mc) {
+    memset(mc, 0, sizeof *mc);
+    mc->m = m;
+    mc->lam = label_lambda(m);
+    mc->b = bit_length(m - 1);
+    mc->g = 32u / mc->b;
+    mc->W = (mc->lam + mc->g - 1) / mc->g;
+    mc->glast = mc->lam - (mc->W - 1) * mc->g;
+    mc->mask = (mc->b == 32) ? 0xffffffffu : ((1u << mc->b) - 1u);
+    if (m > 2) {
+        mc->pw_g = ipow(m, mc->g);
+        mc->pw_last = ipow(m, mc->glast);
+    }
+    uint64_t bound = (m > 2) ? static_cast<uint64_t>(mc->pw_g) : (1ull << 32);
+    // Products c * d of two residues (< m^2) are reduced with the same
+    // constants, so the bound covers them as well.
+    uint64_t sq = static_cast<uint64_t>(m) * m;
+    if (sq > bound) bound = sq;
+    division_constants(m, bound, mc);
+}
+
+int build_plan(const redash_params *p, Plan *pl) {
+    if (!p || !pl) return REDASH_E_NULL;
+    memset(pl, 0, sizeof *pl);
+    if (p->k < 2 || p->k > static_cast<uint32_t>(kMaxK)) return REDASH_E_PARAM;
+    if (p->t < 1 || p->t > p->k - 1) return REDASH_E_PARAM;
+    unsigned __int128 P = 1;
+    for (uint32_t i = 0; i < p->k; ++i) {
+        uint32_t m = p->moduli[i];
+        if (m < 2 || m > 255 || !is_prime(m)) return REDASH_E_PARAM;
+        if (i > 0 && m <= p->moduli[i - 1]) return REDASH_E_PARAM;  // ascending, hence pairwise coprime
+        P *= m;
+    }
+    if (P >= (static_cast<unsigned __int128>(1) << 63)) return REDASH_E_PARAM;
+    uint64_t s = 1;
+    uint32_t is_scale = 0;
+    for (uint32_t a = 0; a < p->t; ++a) {
+        uint32_t si = p->scale_idx[a];
+        if (si >= p->k) return REDASH_E_PARAM;
+        if (a > 0 && si <= p->scale_idx[a - 1]) return REDASH_E_PARAM;
+        is_scale |= 1u << si;
+        s *= p->moduli[si];
+        pl->S[a] = si;
+    }
+    const uint64_t P64 = static_cast<uint64_t>(P);
+    // ShiftDown adds P/(2s): it must be an integer (P even, 2 not in S).
+    if (P64 % (2 * s) != 0) return REDASH_E_PARAM;
+
+    pl->k = p->k;
+    pl->t = p->t;
+    pl->u = p->k - p->t;
+    pl->n = p->n;
+    pl->a0 = p->a0;
+    pl->seed = p->seed;
+    pl->gid = static_cast<uint32_t>(p->seed);
+    pl->P = P64;
+    pl->s = s;
+    pl->is_scale_mask = is_scale;
+    uint32_t u = 0, woff = 0;
+    for (uint32_t i = 0; i < p->k; ++i) {
+        if (!(is_scale & (1u << i))) pl->R[u++] = i;
+        ModConst &mc = pl->mod[i];
+        fill_mod_const(p->moduli[i], &mc);
+        mc.woff = woff;
+        woff += mc.W;
+        mc.up = static_cast<uint32_t>((P64 / 2) % mc.m);
+        mc.down = static_cast<uint32_t>((P64 / (2 * s)) % mc.m);
+    }
+    pl->total_words = woff;
+
+    auto pack = [](uint32_t src, uint32_t dst, uint32_t kind, uint32_t phase, uint32_t coeff) {
+        return src | (dst << 4) | (kind << 8) | (phase << 9) | (coeff << 16);
+    };
+    uint32_t G = 0;
+    // Phase A (Sec. 3.2, once per scaling modulus): digit S[a] onto the later
+    // scaling moduli, then onto every remaining modulus; L <- q^{-1}(L - E).
+    for (uint32_t a = 0; a < pl->t; ++a) {
+        uint32_t src = pl->S[a], q = p->moduli[src];
+        for (uint32_t b = a + 1; b < pl->t; ++b) {
+            uint32_t dst = pl->S[b];
+            pl->gate[G++] = pack(src, dst, 0, 0, inverse_mod(q, p->moduli[dst]));
+        }
+        for (uint32_t b = 0; b < pl->u; ++b) {
+            uint32_t dst = pl->R[b];
+            pl->gate[G++] = pack(src, dst, 0, 0, inverse_mod(q, p->moduli[dst]));
+        }
+    }
+    // Phase B (Sec. 3.3): mixed-radix conversion over R.  Digit R[b] onto the
+    // later remaining moduli (the recursion of Eq. rns_to_mrs), then onto
+    // every scaling modulus with its mixed-radix weight prod_{b'<b} R[b'].
+    for (uint32_t b = 0; b < pl->u; ++b) {
+        uint32_t src = pl->R[b], q = p->moduli[src];
+        for (uint32_t c = b + 1; c < pl->u; ++c) {
+            uint32_t dst = pl->R[c];
+            pl->gate[G++] = pack(src, dst, 0, 1, inverse_mod(q, p->moduli[dst]));
+        }
+        for (uint32_t a = 0; a < pl->t; ++a) {
+            uint32_t dst = pl->S[a], md = p->moduli[dst];
+            uint32_t w = 1 % md;
+            for (uint32_t c = 0; c < b; ++c) w = (w * (p->moduli[pl->R[c]] % md)) % md;
+            pl->gate[G++] = pack(src, dst, 1, 1, w);
+        }
+    }
+    pl->G = G;
+    return REDASH_OK;
+}
+
+}  // namespace redash

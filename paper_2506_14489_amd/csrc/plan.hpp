@@ -1,0 +1,73 @@
+// Host-side plan of one scaling-gadget call: parameter validation, label
+// sizes, the gate list and every per-modulus constant the kernels need.
+// The plan is passed to the kernels by value as their argument block, so it
+// holds no pointers and stays well under the kernel-argument limit.
+#pragma once
+
+#include <stdint.h>
+
+#include "../../include/redash.h"
+
+namespace redash {
+
+constexpr int kMaxK = REDASH_MAX_K;
+// gates = k(k-1)/2 + t(k-t) <= 105 + 56 for k = 15.
+constexpr int kMaxGates = 168;
+
+// Per base modulus.
+struct ModConst {
+    uint32_t m;        // the modulus
+    uint32_t lam;      // residues per label: least lambda with m^lambda >= 2^128
+    uint32_t b;        // bits per packed residue: bit length of m - 1
+    uint32_t g;        // residues per 32-bit word: floor(32 / b)
+    uint32_t W;        // words per label: ceil(lam / g)
+    uint32_t glast;    // residues in the last word: lam - (W - 1) g
+    uint32_t woff;     // word offset of this modulus in a gadget's k labels
+    uint32_t mask;     // (1 << b) - 1
+    uint32_t pw_g;     // m^g      (digits of one full word per 32-bit multiply)
+    uint32_t pw_last;  // m^glast
+    // floor(x / m) for 32-bit x: if div_fix == 0, umulhi(x, divM) >> divS is
+    // exact for every x < m^g (checked when the plan is built); otherwise
+    // the round-up method with a fix-up step:
+    //   t = umulhi(x, divM); floor(x/m) = (t + ((x - t) >> 1)) >> divS.
+    uint32_t divM, divS, div_fix;
+    uint32_t up;       // (P/2) mod m      (ShiftUp)
+    uint32_t down;     // (P/(2s)) mod m   (ShiftDown)
+};
+
+// Gate descriptor packed in one word:
+//   bits 0-3 src modulus index, 4-7 dst modulus index, 8 kind (0 sub, 1 acc),
+//   9 phase (0 A, 1 B), 16-23 coefficient.
+constexpr uint32_t gate_src(uint32_t d) { return d & 15u; }
+constexpr uint32_t gate_dst(uint32_t d) { return (d >> 4) & 15u; }
+constexpr uint32_t gate_kind(uint32_t d) { return (d >> 8) & 1u; }
+constexpr uint32_t gate_phase(uint32_t d) { return (d >> 9) & 1u; }
+constexpr uint32_t gate_coeff(uint32_t d) { return (d >> 16) & 255u; }
+
+struct Plan {
+    uint32_t k, t, u, G;
+    uint32_t total_words;      // sum of W over the base (words per gadget per LabelTensor)
+    uint32_t S[kMaxK];         // scaling modulus indices, ascending
+    uint32_t R[kMaxK];         // remaining modulus indices, ascending
+    uint32_t is_scale_mask;    // bit i set when modulus i is a scaling modulus
+    uint32_t gid;              // gadget_id = seed mod 2^32
+    uint64_t n, a0, seed;
+    uint64_t P, s;
+    ModConst mod[kMaxK];
+    uint32_t gate[kMaxGates];
+};
+
+// Builds and validates the plan.  Returns REDASH_OK, REDASH_E_NULL or
+// REDASH_E_PARAM.
+int build_plan(const redash_params *p, Plan *out);
+
+// Residues per label and words per label for a modulus (2..255).
+uint32_t label_lambda(uint32_t m);
+uint32_t label_words(uint32_t m);
+
+// Fills one ModConst for modulus m (everything except woff, up, down).
+void fill_mod_const(uint32_t m, ModConst *mc);
+
+uint32_t inverse_mod(uint32_t a, uint32_t m);
+
+}  // namespace redash

@@ -1,0 +1,625 @@
+// Kernels and C ABI of the ReDASH scaling-gadget library for gfx950.
+//
+// One thread evaluates (or garbles) one gadget instance.  The k working
+// labels of a gadget live in LDS as packed words laid out [word][thread], so
+// a wavefront touches 64 consecutive banks per access; the gate list and all
+// per-modulus constants are uniform and come from the kernel argument block
+// (scalar registers).  The AES round tables are staged into LDS once per
+// block.  Nothing here uses MFMA: the work is table lookups, XORs, 32-bit
+// multiplies for digit extraction and small modular arithmetic.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/redash.h"
+#include "device.hpp"
+#include "plan.hpp"
+
+namespace redash {
+
+struct SeedKey {
+    uint32_t w[44];
+};
+
+// ---------------------------------------------------------------------------
+// Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
+// ---------------------------------------------------------------------------
+template <int BLOCK>
+__global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__restrict__ in,
+                                                const uint32_t *__restrict__ tab, uint32_t *__restrict__ out) {
+    extern __shared__ uint32_t lds[];
+    uint32_t *TT = lds;
+    uint32_t *L = lds + kTableWords;
+    const int tid = threadIdx.x;
+    stage_round_tables(TT, tid, BLOCK);
+    __syncthreads();
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
+    if (a >= P.n) return;  // no barrier follows
+    const uint64_t n = P.n;
+
+    for (uint32_t i = 0; i < P.k; ++i) {
+        const ModConst &mc = P.mod[i];
+        const uint32_t *src = in + static_cast<uint64_t>(mc.woff) * n + a;
+        for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = src[static_cast<uint64_t>(w) * n];
+    }
+
+    const uint64_t tau0 = (P.a0 + a) * P.G;
+    uint64_t toff = 0;
+    bool phaseB = false;
+    for (uint32_t g = 0; g < P.G; ++g) {
+        const uint32_t d = P.gate[g];
+        if (gate_phase(d) && !phaseB) {
+            // End of the division step: the remaining-modulus labels are the
+            // gadget's outputs on R; the scaling-modulus slots restart as
+            // accumulators at the all-zero label.
+            phaseB = true;
+            for (uint32_t b = 0; b < P.u; ++b) {
+                const ModConst &mc = P.mod[P.R[b]];
+                uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
+                for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = L[(mc.woff + w) * BLOCK + tid];
+            }
+            for (uint32_t s = 0; s < P.t; ++s) {
+                const ModConst &mc = P.mod[P.S[s]];
+                for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = 0;
+            }
+        }
+        const ModConst &mq = P.mod[gate_src(d)];
+        const ModConst &mm = P.mod[gate_dst(d)];
+        const uint32_t q = mq.m;
+        const uint32_t *Lsrc = L + mq.woff * BLOCK + tid;
+        uint32_t *Ldst = L + mm.woff * BLOCK + tid;
+
+        // Colour of the digit label: its first residue.  The row is fetched
+        // before the hash so the load latency hides under the AES rounds.
+        const uint32_t w0 = Lsrc[0];
+        // A residue >= q only occurs in a malformed input label; it selects
+        // the implicit zero row, the output is garbage and decode flags it.
+        uint32_t colour = w0 & mq.mask;
+        if (colour >= q) colour = 0;
+        uint32_t row[kMaxW];
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) row[w] = 0;
+        if (colour != 0) {
+            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * mm.W;
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w)
+                if (w < static_cast<int>(mm.W)) row[w] = rp[w];
+        }
+        toff += n * (q - 1) * mm.W;
+
+        uint32_t x[4] = {w0, 0, 0, 0};
+#pragma unroll
+        for (int w = 1; w < kMaxW; ++w)
+            if (w < static_cast<int>(mq.W)) x[w & 3] ^= Lsrc[w * BLOCK];
+        uint32_t V[8];
+        hash_fraction(TT, x[0], x[1], x[2], x[3], tau0 + g, P.gid, mm.m != 2, V);
+
+        const uint32_t coeff = gate_coeff(d);
+        if (mm.m == 2) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const uint32_t E = bits_word(V, w) ^ row[w];
+                uint32_t l = Ldst[w * BLOCK];
+                if (gate_kind(d) == 0 || (coeff & 1u)) l ^= E;  // sub: q^{-1} = 1 mod 2
+                Ldst[w * BLOCK] = l;
+            }
+        } else {
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w) {
+                if (w < static_cast<int>(mm.W)) {
+                    const bool last = (w + 1 == static_cast<int>(mm.W));
+                    const uint32_t nres = last ? mm.glast : mm.g;
+                    uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
+                    const uint32_t rw = row[w];
+                    const uint32_t l = Ldst[w * BLOCK];
+                    uint32_t res = 0;
+                    // Digits come out least significant first: position nres-1 down to 0.
+                    if (gate_kind(d) == 0) {
+                        for (uint32_t j = nres; j-- > 0;) {
+                            uint32_t pd;
+                            if (j) {
+                                const uint32_t qd = div_m(D, mm);
+                                pd = D - qd * mm.m;
+                                D = qd;
+                            } else {
+                                pd = D;
+                            }
+                            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
+                            res |= mul_mod(coeff, sub_mod(field(l, j, mm), e, mm.m), mm) << (mm.b * j);
+                        }
+                    } else {
+                        for (uint32_t j = nres; j-- > 0;) {
+                            uint32_t pd;
+                            if (j) {
+                                const uint32_t qd = div_m(D, mm);
+                                pd = D - qd * mm.m;
+                                D = qd;
+                            } else {
+                                pd = D;
+                            }
+                            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
+                            res |= add_mod(field(l, j, mm), mul_mod(coeff, e, mm), mm.m) << (mm.b * j);
+                        }
+                    }
+                    Ldst[w * BLOCK] = res;
+                }
+            }
+        }
+    }
+    for (uint32_t s = 0; s < P.t; ++s) {
+        const ModConst &mc = P.mod[P.S[s]];
+        uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
+        for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = L[(mc.woff + w) * BLOCK + tid];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Garbler: offsets, zero-labels, garbled rows.
+// ---------------------------------------------------------------------------
+
+// Offsets R_m: digits of rho(1, i) in the radices (m-1, m, m, ...), then
+// residue 0 incremented so that it is a unit of Z_m.  One thread per modulus.
+__global__ void __launch_bounds__(64) k_offsets(const Plan P, const SeedKey key, uint32_t *__restrict__ offsets) {
+    __shared__ uint32_t TT[kTableWords];
+    stage_round_tables(TT, threadIdx.x, 64);
+    __syncthreads();
+    const uint32_t i = threadIdx.x;
+    if (i >= P.k) return;
+    const ModConst &mc = P.mod[i];
+    uint32_t V[8];
+    prg_fraction(TT, key.w, 1u, i, V);
+    uint32_t words[kMaxW] = {0, 0, 0, 0, 0, 0};
+    for (uint32_t r = 0; r < mc.lam; ++r) {
+        const uint32_t radix = r ? mc.m : mc.m - 1;
+        uint32_t dgt = frac_mul_carry(V, radix);
+        if (r == 0) dgt += 1;
+        const uint32_t w = r / mc.g, pos = r % mc.g;
+#pragma unroll
+        for (int ww = 0; ww < kMaxW; ++ww)
+            if (ww == static_cast<int>(w)) words[ww] |= dgt << (mc.b * pos);
+    }
+    for (uint32_t w = 0; w < mc.W; ++w) {
+#pragma unroll
+        for (int ww = 0; ww < kMaxW; ++ww)
+            if (ww == static_cast<int>(w)) offsets[mc.woff + w] = words[ww];
+    }
+}
+
+__device__ __forceinline__ uint32_t inverse_unit(uint32_t r, const ModConst &mc) {
+    // r^(m-2) mod m (m prime, r != 0)
+    uint32_t e = mc.m - 2, base = r, acc = 1 % mc.m;
+    while (e) {
+        if (e & 1u) acc = mul_mod(acc, base, mc);
+        base = mul_mod(base, base, mc);
+        e >>= 1;
+    }
+    return acc;
+}
+
+template <int BLOCK>
+__global__ void __launch_bounds__(BLOCK) k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets,
+                                                  uint32_t *__restrict__ zin, uint32_t *__restrict__ zout,
+                                                  uint32_t *__restrict__ tab) {
+    extern __shared__ uint32_t lds[];
+    uint32_t *TT = lds;
+    uint32_t *Rl = lds + kTableWords;                   // offsets, P.total_words
+    uint32_t *L = lds + kTableWords + P.total_words;    // [word][BLOCK]
+    const int tid = threadIdx.x;
+    stage_round_tables(TT, tid, BLOCK);
+    for (uint32_t i = tid; i < P.total_words; i += BLOCK) Rl[i] = offsets[i];
+    __syncthreads();
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
+    if (a >= P.n) return;  // no barrier follows
+    const uint64_t n = P.n;
+    const uint64_t ga = P.a0 + a;
+
+    // Input zero-labels Z (digits of rho(2, ga k + i)); the working labels
+    // start at Z - (P/2 mod m) R: the ShiftUp of Sec. 3.4 as a free constant
+    // addition on the garbler side.
+    for (uint32_t i = 0; i < P.k; ++i) {
+        const ModConst &mc = P.mod[i];
+        uint32_t V[8];
+        prg_fraction(TT, key.w, 2u, ga * P.k + i, V);
+        uint32_t *dst = zin + static_cast<uint64_t>(mc.woff) * n + a;
+        const uint32_t neg_up = (mc.m - mc.up) % mc.m;
+        for (uint32_t w = 0; w < mc.W; ++w) {
+            const uint32_t z = prg_word(V, w, mc);
+            dst[static_cast<uint64_t>(w) * n] = z;
+            L[(mc.woff + w) * BLOCK + tid] = label_axpy(z, Rl[mc.woff + w], neg_up, w, mc);
+        }
+    }
+
+    const uint64_t tau0 = ga * P.G;
+    uint64_t toff = 0;
+    bool phaseB = false;
+    for (uint32_t g = 0; g < P.G; ++g) {
+        const uint32_t d = P.gate[g];
+        if (gate_phase(d) && !phaseB) {
+            phaseB = true;
+            for (uint32_t b = 0; b < P.u; ++b) {  // R outputs, plus the ShiftDown constant
+                const ModConst &mc = P.mod[P.R[b]];
+                uint32_t *dst = zout + static_cast<uint64_t>(mc.woff) * n + a;
+                for (uint32_t w = 0; w < mc.W; ++w)
+                    dst[static_cast<uint64_t>(w) * n] =
+                        label_axpy(L[(mc.woff + w) * BLOCK + tid], Rl[mc.woff + w], mc.down, w, mc);
+            }
+            for (uint32_t s = 0; s < P.t; ++s) {
+                const ModConst &mc = P.mod[P.S[s]];
+                for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = 0;
+            }
+        }
+        const ModConst &mq = P.mod[gate_src(d)];
+        const ModConst &mm = P.mod[gate_dst(d)];
+        const uint32_t q = mq.m;
+        const uint32_t *Rq = Rl + mq.woff;
+        const uint32_t *Rm = Rl + mm.woff;
+        uint32_t A0[kMaxW];
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) A0[w] = (w < static_cast<int>(mq.W)) ? L[(mq.woff + w) * BLOCK + tid] : 0u;
+        const uint32_t c0 = A0[0] & mq.mask;
+        const uint32_t rq0 = Rq[0] & mq.mask;
+        const uint32_t rinv = inverse_unit(rq0, mq);
+        // v0: the value whose label has colour 0.
+        const uint32_t v0 = mul_mod((q - c0) % q, rinv, mq);
+        const uint64_t tau = tau0 + g;
+
+        // B0 = H(A0 + v0 Rq) - (v0 mod m) Rm   (row reduction)
+        uint32_t B0[kMaxW];
+        {
+            uint32_t Av[kMaxW];
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w)
+                Av[w] = (w < static_cast<int>(mq.W)) ? label_axpy(A0[w], Rq[w], v0, w, mq) : 0u;
+            uint32_t x[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w) x[w & 3] ^= Av[w];
+            uint32_t V[8];
+            hash_fraction(TT, x[0], x[1], x[2], x[3], tau, P.gid, mm.m != 2, V);
+            const uint32_t negv = (mm.m - v0 % mm.m) % mm.m;
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w)
+                B0[w] = (w < static_cast<int>(mm.W)) ? label_axpy(pad_word(V, w, mm), Rm[w], negv, w, mm) : 0u;
+        }
+        // Rows: for every v != v0, row[colour(A0 + v Rq)] = B0 + (v mod m) Rm - H(A0 + v Rq).
+        uint32_t Av[kMaxW];
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) Av[w] = A0[w];
+        const uint64_t gate_base = toff + a * (q - 1) * mm.W;
+        for (uint32_t v = 0; v < q; ++v) {
+            const uint32_t c = Av[0] & mq.mask;
+            if (v != v0 && c != 0) {  // c != 0 holds for every v != v0 since R_q[0] is a unit
+                uint32_t x[4] = {0, 0, 0, 0};
+#pragma unroll
+                for (int w = 0; w < kMaxW; ++w) x[w & 3] ^= Av[w];
+                uint32_t V[8];
+                hash_fraction(TT, x[0], x[1], x[2], x[3], tau, P.gid, mm.m != 2, V);
+                uint32_t *rp = tab + gate_base + static_cast<uint64_t>(c - 1) * mm.W;
+                const uint32_t vm = v % mm.m;
+#pragma unroll
+                for (int w = 0; w < kMaxW; ++w) {
+                    if (w < static_cast<int>(mm.W)) {
+                        const uint32_t h = pad_word(V, w, mm);
+                        rp[w] = label_sub(label_axpy(B0[w], Rm[w], vm, w, mm), h, w, mm);
+                    }
+                }
+            }
+#pragma unroll
+            for (int w = 0; w < kMaxW; ++w)
+                if (w < static_cast<int>(mq.W)) Av[w] = label_axpy(Av[w], Rq[w], 1u, w, mq);
+        }
+        toff += n * (q - 1) * mm.W;
+
+        // The same free operation on zero-labels that the evaluator applies.
+        const uint32_t coeff = gate_coeff(d);
+        for (uint32_t w = 0; w < mm.W; ++w) {
+            uint32_t l = L[(mm.woff + w) * BLOCK + tid];
+            uint32_t b0 = 0;
+#pragma unroll
+            for (int ww = 0; ww < kMaxW; ++ww)
+                if (ww == static_cast<int>(w)) b0 = B0[ww];
+            l = gate_kind(d) == 0 ? label_scaled_sub(l, b0, coeff, w, mm) : label_axpy(l, b0, coeff, w, mm);
+            L[(mm.woff + w) * BLOCK + tid] = l;
+        }
+    }
+    for (uint32_t s = 0; s < P.t; ++s) {  // S outputs, plus the ShiftDown constant
+        const ModConst &mc = P.mod[P.S[s]];
+        uint32_t *dst = zout + static_cast<uint64_t>(mc.woff) * n + a;
+        for (uint32_t w = 0; w < mc.W; ++w)
+            dst[static_cast<uint64_t>(w) * n] =
+                label_axpy(L[(mc.woff + w) * BLOCK + tid], Rl[mc.woff + w], mc.down, w, mc);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Encode (stand-in for oblivious transfer) and decode.
+// ---------------------------------------------------------------------------
+template <int BLOCK>
+__global__ void __launch_bounds__(BLOCK) k_encode(const Plan P, const int64_t *__restrict__ x,
+                                                  const uint32_t *__restrict__ zero,
+                                                  const uint32_t *__restrict__ offsets, uint32_t *__restrict__ lab) {
+    __shared__ uint32_t Rl[kMaxK * kMaxW];
+    for (uint32_t i = threadIdx.x; i < P.total_words; i += BLOCK) Rl[i] = offsets[i];
+    __syncthreads();
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + threadIdx.x;
+    if (a >= P.n) return;
+    const uint64_t n = P.n;
+    int64_t r = x[a] % static_cast<int64_t>(P.P);
+    if (r < 0) r += static_cast<int64_t>(P.P);
+    for (uint32_t i = 0; i < P.k; ++i) {
+        const ModConst &mc = P.mod[i];
+        const uint32_t v = static_cast<uint32_t>(static_cast<uint64_t>(r) % mc.m);
+        const uint64_t base = static_cast<uint64_t>(mc.woff) * n + a;
+        for (uint32_t w = 0; w < mc.W; ++w)
+            lab[base + static_cast<uint64_t>(w) * n] = label_axpy(zero[base + static_cast<uint64_t>(w) * n],
+                                                                  Rl[mc.woff + w], v, w, mc);
+    }
+}
+
+__global__ void k_zero_u64(uint64_t *p) { *p = 0; }
+
+template <int BLOCK>
+__global__ void __launch_bounds__(BLOCK) k_decode(const Plan P, const uint32_t *__restrict__ Y,
+                                                  const uint32_t *__restrict__ O, const uint32_t *__restrict__ offsets,
+                                                  int64_t *__restrict__ y, unsigned long long *__restrict__ bad) {
+    __shared__ uint32_t Rl[kMaxK * kMaxW];
+    for (uint32_t i = threadIdx.x; i < P.total_words; i += BLOCK) Rl[i] = offsets[i];
+    __syncthreads();
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + threadIdx.x;
+    if (a >= P.n) return;
+    const uint64_t n = P.n;
+    bool ok = true;
+    uint32_t v[kMaxK];
+    for (uint32_t i = 0; i < P.k; ++i) {
+        const ModConst &mc = P.mod[i];
+        const uint64_t base = static_cast<uint64_t>(mc.woff) * n + a;
+        const uint32_t y0 = Y[base] & mc.mask, o0 = O[base] & mc.mask;
+        const uint32_t vi = mul_mod(sub_mod(y0, o0, mc.m), inverse_unit(Rl[mc.woff] & mc.mask, mc), mc);
+        for (uint32_t w = 0; w < mc.W; ++w) {
+            const uint64_t at = base + static_cast<uint64_t>(w) * n;
+            if (label_axpy(O[at], Rl[mc.woff + w], vi, w, mc) != Y[at]) ok = false;
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j)
+            if (j == static_cast<int>(i)) v[j] = vi;
+    }
+    // Garner: mixed-radix digits d_i of the CRT value, then y = sum d_i prod_{l<i} m_l.
+    uint64_t val = 0, weight = 1;
+    uint32_t dig[kMaxK];
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+        if (i < static_cast<int>(P.k)) {
+            const ModConst &mc = P.mod[i];
+            uint32_t cur = 0, wmod = 1 % mc.m;  // sum_{j<i} d_j prod_{l<j} m_l  (mod m_i)
+#pragma unroll
+            for (int j = 0; j < kMaxK; ++j) {
+                if (j < i) {
+                    cur = add_mod(cur, mul_mod(dig[j] % mc.m, wmod, mc), mc.m);
+                    wmod = mul_mod(wmod, P.mod[j].m % mc.m, mc);
+                }
+            }
+            // wmod = prod_{l<i} m_l mod m_i, a unit since the base is coprime
+            dig[i] = mul_mod(sub_mod(v[i], cur, mc.m), inverse_unit(wmod, mc), mc);
+            val += static_cast<uint64_t>(dig[i]) * weight;
+            weight *= mc.m;
+        }
+    }
+    int64_t out = static_cast<int64_t>(val);
+    if (val >= P.P / 2) out -= static_cast<int64_t>(P.P);
+    y[a] = out;
+    if (!ok) atomicAdd(bad, 1ull);
+}
+
+// ---------------------------------------------------------------------------
+// The hash alone.
+// ---------------------------------------------------------------------------
+template <int BLOCK>
+__global__ void __launch_bounds__(BLOCK) k_hash(const ModConst mq, const ModConst mm, uint64_t count,
+                                                const uint32_t *__restrict__ lab, uint32_t gid,
+                                                const uint64_t *__restrict__ tau, uint32_t *__restrict__ out) {
+    __shared__ uint32_t TT[kTableWords];
+    stage_round_tables(TT, threadIdx.x, BLOCK);
+    __syncthreads();
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + threadIdx.x;
+    if (a >= count) return;
+    uint32_t x[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int w = 0; w < kMaxW; ++w)
+        if (w < static_cast<int>(mq.W)) x[w & 3] ^= lab[static_cast<uint64_t>(w) * count + a];
+    uint32_t V[8];
+    hash_fraction(TT, x[0], x[1], x[2], x[3], tau[a], gid, mm.m != 2, V);
+#pragma unroll
+    for (int w = 0; w < kMaxW; ++w)
+        if (w < static_cast<int>(mm.W)) out[static_cast<uint64_t>(w) * count + a] = pad_word(V, w, mm);
+}
+
+// ---------------------------------------------------------------------------
+// Host side.
+// ---------------------------------------------------------------------------
+namespace {
+
+size_t eval_lds_bytes(const Plan &P, int block) {
+    return (static_cast<size_t>(kTableWords) + static_cast<size_t>(P.total_words) * block) * 4;
+}
+size_t garble_lds_bytes(const Plan &P, int block) {
+    return (static_cast<size_t>(kTableWords) + P.total_words + static_cast<size_t>(P.total_words) * block) * 4;
+}
+
+// Largest LDS allocation a block may request on the current device.
+int max_lds_bytes(size_t *out) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return REDASH_E_HIP;
+    *out = static_cast<size_t>(v);
+    return REDASH_OK;
+}
+
+// Allows a kernel to use more than the default 64 KiB of dynamic LDS.
+int allow_lds(const void *kernel, size_t bytes) {
+    if (bytes <= 64 * 1024) return REDASH_OK;
+    return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes)) ==
+                   hipSuccess
+               ? REDASH_OK
+               : REDASH_E_HIP;
+}
+
+unsigned grid_for(uint64_t n, int block) { return static_cast<unsigned>((n + block - 1) / block); }
+
+int launched() {
+    return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
+}
+
+// Launches k_eval with the largest block (256, 128 or 64 threads) whose LDS
+// footprint fits the device.
+template <int BLOCK>
+int try_eval(const Plan &P, size_t max_lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
+             hipStream_t stream, bool *done) {
+    const size_t lds = eval_lds_bytes(P, BLOCK);
+    if (*done || lds > max_lds) return REDASH_OK;
+    *done = true;
+    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<BLOCK>), lds);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_eval<BLOCK>, dim3(grid_for(P.n, BLOCK)), dim3(BLOCK), lds, stream, P, in, tab, out);
+    return launched();
+}
+
+template <int BLOCK>
+int try_garble(const Plan &P, size_t max_lds, const SeedKey &key, const uint32_t *offsets, uint32_t *zin,
+               uint32_t *zout, uint32_t *tab, hipStream_t stream, bool *done) {
+    const size_t lds = garble_lds_bytes(P, BLOCK);
+    if (*done || lds > max_lds) return REDASH_OK;
+    *done = true;
+    int rc = allow_lds(reinterpret_cast<const void *>(&k_garble<BLOCK>), lds);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_garble<BLOCK>, dim3(grid_for(P.n, BLOCK)), dim3(BLOCK), lds, stream, P, key, offsets, zin,
+                       zout, tab);
+    return launched();
+}
+
+SeedKey seed_key(uint64_t seed) {
+    RoundKeys rk = make_seed_round_keys(seed);
+    SeedKey k;
+    memcpy(k.w, rk.w, sizeof k.w);
+    return k;
+}
+
+}  // namespace
+
+}  // namespace redash
+
+using namespace redash;
+
+extern "C" {
+
+int redash_plan(const redash_params *p, redash_sizes *out) {
+    if (!p || !out) return REDASH_E_NULL;
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    out->label_words = P.n * P.total_words;
+    uint64_t tw = 0;
+    for (uint32_t g = 0; g < P.G; ++g) {
+        const uint32_t d = P.gate[g];
+        tw += P.n * (P.mod[gate_src(d)].m - 1) * P.mod[gate_dst(d)].W;
+    }
+    out->table_words = tw;
+    out->offset_words = P.total_words;
+    out->gates = P.G;
+    return REDASH_OK;
+}
+
+int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero, uint32_t *d_out_zero,
+                        uint32_t *d_tables, hipStream_t stream) {
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    if (!d_offsets) return REDASH_E_NULL;
+    if (P.n > 0 && (!d_in_zero || !d_out_zero || !d_tables)) return REDASH_E_NULL;
+    const SeedKey key = seed_key(P.seed);
+    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(64), 0, stream, P, key, d_offsets);
+    if ((rc = launched())) return rc;
+    if (P.n == 0) return REDASH_OK;
+    size_t max_lds = 0;
+    if ((rc = max_lds_bytes(&max_lds))) return rc;
+    bool done = false;
+    if ((rc = try_garble<256>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
+    if ((rc = try_garble<128>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
+    if ((rc = try_garble<64>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
+    return done ? REDASH_OK : REDASH_E_PARAM;
+}
+
+int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_in_zero, const uint32_t *d_offsets,
+                  uint32_t *d_in_labels, hipStream_t stream) {
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    if (!d_offsets) return REDASH_E_NULL;
+    if (P.n == 0) return REDASH_OK;
+    if (!d_x || !d_in_zero || !d_in_labels) return REDASH_E_NULL;
+    hipLaunchKernelGGL(k_encode<256>, dim3(grid_for(P.n, 256)), dim3(256), 0, stream, P, d_x, d_in_zero, d_offsets,
+                       d_in_labels);
+    return launched();
+}
+
+int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
+                      uint32_t *d_out_labels, hipStream_t stream) {
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    if (P.n == 0) return REDASH_OK;
+    if (!d_in_labels || !d_tables || !d_out_labels) return REDASH_E_NULL;
+    size_t max_lds = 0;
+    if ((rc = max_lds_bytes(&max_lds))) return rc;
+    bool done = false;
+    if ((rc = try_eval<256>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
+    if ((rc = try_eval<128>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
+    if ((rc = try_eval<64>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
+    return done ? REDASH_OK : REDASH_E_PARAM;
+}
+
+int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,
+                  const uint32_t *d_offsets, int64_t *d_y, uint64_t *d_bad_count, hipStream_t stream) {
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    if (!d_offsets || !d_bad_count) return REDASH_E_NULL;
+    if (P.n > 0 && (!d_out_labels || !d_out_zero || !d_y)) return REDASH_E_NULL;
+    unsigned long long *bad = reinterpret_cast<unsigned long long *>(d_bad_count);
+    hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, stream, reinterpret_cast<uint64_t *>(bad));
+    if ((rc = launched())) return rc;
+    if (P.n == 0) return REDASH_OK;
+    hipLaunchKernelGGL(k_decode<256>, dim3(grid_for(P.n, 256)), dim3(256), 0, stream, P, d_out_labels, d_out_zero,
+                       d_offsets, d_y, bad);
+    return launched();
+}
+
+int redash_hash_labels(uint32_t q, uint32_t m, uint64_t count, const uint32_t *d_labels, uint32_t gadget_id,
+                       const uint64_t *d_tau, uint32_t *d_out, hipStream_t stream) {
+    auto ok_mod = [](uint32_t v) {
+        if (v < 2 || v > 255) return false;
+        for (uint32_t d = 2; d * d <= v; ++d)
+            if (v % d == 0) return false;
+        return true;
+    };
+    if (!ok_mod(q) || !ok_mod(m)) return REDASH_E_PARAM;
+    if (count == 0) return REDASH_OK;
+    if (!d_labels || !d_tau || !d_out) return REDASH_E_NULL;
+    ModConst mq, mm;
+    fill_mod_const(q, &mq);
+    fill_mod_const(m, &mm);
+    hipLaunchKernelGGL(k_hash<256>, dim3(grid_for(count, 256)), dim3(256), 0, stream, mq, mm, count, d_labels,
+                       gadget_id, d_tau, d_out);
+    return launched();
+}
+
+const char *redash_strerror(int code) {
+    switch (code) {
+        case REDASH_OK: return "ok";
+        case REDASH_E_PARAM: return "invalid parameters";
+        case REDASH_E_NULL: return "null pointer";
+        case REDASH_E_HIP: return "HIP launch or runtime error";
+        case REDASH_E_LABEL: return "output label failed the decode check";
+        default: return "unknown error";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point that include/redash.h declares, validates parameters like
+the oracle does, and reports the same buffer sizes as the oracle's layouts."""
+
+from __future__ import annotations
+
+import ctypes
+
+import pytest
+
+from oracle import oracle as O
+from oracle import rns
+from paper_2506_14489_amd import binding as B
+from paper_2506_14489_amd import workloads as WL
+
+
+def test_library_exports_every_declared_symbol():
+    names = B.declared_symbols()
+    assert set(names) == {"redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale",
+                          "redash_decode", "redash_hash_labels", "redash_strerror"}
+    L = B.lib()
+    for n in names:
+        assert hasattr(L, n), n
+        assert ctypes.cast(getattr(L, n), ctypes.c_void_p).value
+
+
+def test_params_struct_layout_matches_header():
+    # k, moduli[16], t, scale_idx[16] (4-byte) then n, seed, a0 (8-byte)
+    assert ctypes.sizeof(B.Params) == 4 * 34 + 8 * 3
+    assert B.Params.n.offset == 136 and B.Params.a0.offset == 152
+    assert ctypes.sizeof(B.Sizes) == 24
+
+
+def test_strerror_texts():
+    assert B.strerror(0) == "ok"
+    for code in (-1, -2, -3, -4):
+        assert B.strerror(code) != "unknown error"
+    assert B.strerror(42) == "unknown error"
+
+
+PLAN_CASES = [(w.moduli, w.scale_idx) for w in WL.CONFIGS] + [
+    (tuple(WL.PRIMES_12), (10, 11)), (tuple(WL.PRIMES_12), (9,)), ((2, 3), (1,)), ((2, 3, 5), (1, 2)),
+    (tuple(rns.first_primes(15)), (13, 14)), (tuple(rns.first_primes(15)), (1, 5, 9)), ((2, 97, 251), (2,)),
+    ((2, 3, 5, 7, 11, 13), (1, 2, 3, 4, 5)),
+]
+
+
+@pytest.mark.parametrize("moduli,S", PLAN_CASES)
+@pytest.mark.parametrize("n", [0, 1, 1000])
+def test_plan_sizes_match_oracle(moduli, S, n):
+    sz = B.redash_plan(B.make_params(moduli, S, n, 0))
+    osz = O.sizes(O.make_params(list(moduli), list(S), n, 0), n)
+    assert sz["label_words"] == osz["label_words"]
+    assert sz["table_words"] == osz["table_words"]
+    assert sz["offset_words"] == osz["offset_words"]
+    assert sz["gates"] == osz["gates"]
+    k, t = len(moduli), len(S)
+    assert sz["gates"] == k * (k - 1) // 2 + t * (k - t)
+
+
+@pytest.mark.parametrize("m", rns.first_primes(12) + [97, 107, 167, 173, 251])
+def test_label_words_match_oracle(m):
+    assert B.label_words_of(m) == O.words(m)
+
+
+BAD = [
+    ([3, 5, 7], [2]),
+    ([2, 3, 5], [0]),
+    ([2, 3, 4], [2]),
+    ([3, 2, 5], [2]),
+    ([2, 3, 5], [1, 1]),
+    ([2, 3, 5], [0, 1, 2]),
+    ([2], [0]),
+    ([2, 3, 5, 7, 11, 13, 17, 19, 23, 29, 31, 37, 41, 241, 251], [14]),
+    ([2, 3, 257], [2]),
+    ([2, 3, 5], [3]),
+    ([2, 3, 5], []),
+    (list(rns.first_primes(16)), [15]),
+]
+
+
+@pytest.mark.parametrize("moduli,S", BAD)
+def test_bad_params_rejected_like_the_oracle(moduli, S):
+    bp = B.make_params(moduli[:16], S, 1, 0)
+    assert B.plan_rc(bp) == B.REDASH_E_PARAM
+    if len(moduli) <= 16:
+        assert O.check_params(O.make_params(moduli, S, 1, 0)) == -1
+
+
+def test_null_params():
+    L = B.lib()
+    s = B.Sizes()
+    assert L.redash_plan(None, ctypes.byref(s)) == B.REDASH_E_NULL
+    assert L.redash_plan(ctypes.byref(B.make_params([2, 3], [1], 1, 0)), None) == B.REDASH_E_NULL
+
+
+def test_valid_extremes_accepted():
+    # largest k, P just below 2^63 is rejected above; first 15 primes are accepted
+    assert B.plan_rc(B.make_params(rns.first_primes(15), [14], 1, 0)) == 0
+    assert B.plan_rc(B.make_params([2, 251], [1], 1, 0)) == 0
+
+
+def test_batched_table_footprint():
+    """64 GB of garbled rows for the 16x64x56x56 map (fits one 288 GB GPU)."""
+    w = WL.BATCHED
+    sz = B.redash_plan(B.make_params(w.moduli, w.scale_idx, w.n, w.seed))
+    assert sz["table_words"] * 4 == 19932 * w.n
+    assert sz["label_words"] * 4 == 252 * w.n
+
+
+def test_entry_points_validate_before_any_device_work():
+    """Invalid parameters and NULL buffers are rejected on the host, before
+    any HIP call, so this runs without a GPU."""
+    L = B.lib()
+    bad = B.make_params([3, 5, 7], [2], 4, 0)  # P odd
+    good = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 4, 0)
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below returns early
+    assert L.redash_eval_scale(ctypes.byref(bad), fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_garble_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_encode(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_decode(ctypes.byref(bad), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_eval_scale(ctypes.byref(good), None, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_encode(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_decode(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_hash_labels(4, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_hash_labels(3, 256, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_hash_labels(3, 5, 1, None, 0, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(None, fake, fake, fake, None) == B.REDASH_E_NULL

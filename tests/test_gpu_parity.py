@@ -1,0 +1,267 @@
+"""GPU parity of the HIP library against the CPU oracle (bit-exact).
+
+Small cases: every word of every output is compared with the oracle, at sizes
+that span several 256-thread blocks and end in a ragged tail.  Full-size
+workloads (the batched conv map and the ResNet-18 layers) run in the launch
+configuration the benchmark times; there every gadget is checked through
+decode = floor(x/s) with all labels valid, and a seeded sample of gadgets is
+compared word by word with the oracle garbling that one gadget.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import oracle as O  # noqa: E402
+from oracle import rns  # noqa: E402
+from paper_2506_14489_amd import binding as B  # noqa: E402
+from paper_2506_14489_amd import workloads as WL  # noqa: E402
+
+import gpu_helpers as H  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU containers
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+
+def _floor_div(x: np.ndarray, s: int) -> np.ndarray:
+    return np.floor_divide(x, s)
+
+
+def _params_pair(moduli, S, n, seed, a0=0):
+    return B.make_params(moduli, S, n, seed, a0), O.make_params(moduli, S, n, seed)
+
+
+# ---------------------------------------------------------------------------
+# hash
+# ---------------------------------------------------------------------------
+
+HASH_PAIRS = [(2, 3), (3, 2), (37, 2), (2, 37), (11, 13), (5, 3), (37, 31), (17, 19), (97, 251), (251, 97),
+              (3, 5), (7, 37)]
+
+
+@pytest.mark.parametrize("q,m", HASH_PAIRS)
+def test_hash_matches_oracle(q, m):
+    count = 300
+    rng = np.random.default_rng(q * 1000 + m)
+    lam_q = O.lam(q)
+    res = rng.integers(0, q, size=(count, lam_q)).astype(np.uint32)
+    words = np.stack([O.pk32_pack(q, r) for r in res])            # count x W_q
+    tau = rng.integers(0, 2 ** 62, size=count, dtype=np.int64)
+    gid = int(rng.integers(0, 2 ** 32))
+    Wq, Wm = B.label_words_of(q), B.label_words_of(m)
+    lab = H.to_dev(np.ascontiguousarray(words.T.reshape(-1)))     # SoA
+    out = torch.empty(Wm * count, dtype=torch.int32, device="cuda")
+    B.redash_hash_labels(q, m, count, lab, gid, H.to_dev(tau), out)
+    got = H.to_u32(out).reshape(Wm, count).T
+    for a in range(count):
+        exp = O.pk32_pack(m, O.hash_label(q, m, res[a], gid, int(tau[a])))
+        assert np.array_equal(got[a], exp), (q, m, a)
+    assert Wq == len(words[0])
+
+
+# ---------------------------------------------------------------------------
+# small cases: garble, encode, eval, decode, word for word
+# ---------------------------------------------------------------------------
+
+SMALL = [
+    # name, moduli, S, n, seed, a0
+    ("tiny", WL.TINY.moduli, WL.TINY.scale_idx, 1024, 0, 0),
+    ("tiny-ragged", WL.TINY.moduli, WL.TINY.scale_idx, 777, 0, 0),
+    ("dense", WL.DENSE.moduli, WL.DENSE.scale_idx, 4096, 1, 0),
+    ("conv-tail", WL.CONV.moduli, WL.CONV.scale_idx, 600, 2, 65536 - 600),
+    ("batched-head", WL.BATCHED.moduli, WL.BATCHED.scale_idx, 300, 3, 0),
+    ("resnet-1147", tuple(WL.PRIMES_12), (10, 11), 260, 11, 1000),
+    ("k15-product", tuple(rns.first_primes(15)), (13, 14), 300, 77, 5),
+    ("base-235-by-15", (2, 3, 5), (1, 2), 30, 5, 0),
+    ("base-2357-by-35", (2, 3, 5, 7), (2, 3), 210, 6, 0),
+    ("k2", (2, 3), (1,), 6, 9, 0),
+    ("large-moduli", (2, 97, 251), (2,), 300, 12, 3),
+]
+
+
+def _small_inputs(moduli, n, seed):
+    P = rns.cardinality(moduli)
+    rng = np.random.default_rng(seed + 1000)
+    x = rng.integers(-(P // 2), P // 2, size=n, dtype=np.int64)
+    if n >= 2:
+        x[0], x[1] = -(P // 2), P // 2 - 1  # both ends of the signed range
+    return x
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_garble_matches_oracle(case):
+    name, moduli, S, n, seed, a0 = case
+    bp, op = _params_pair(moduli, S, n, seed, a0)
+    buf = B.Buffers(bp)
+    B.redash_garble_scale(bp, buf.offsets, buf.in_zero, buf.out_zero, buf.tables)
+    torch.cuda.synchronize()
+    offs, zin, zout, tab = O.garble(op, a0, n)
+    assert np.array_equal(H.to_u32(buf.offsets), offs)
+    assert np.array_equal(H.to_u32(buf.in_zero), zin)
+    assert np.array_equal(H.to_u32(buf.out_zero), zout)
+    assert np.array_equal(H.to_u32(buf.tables)[: len(tab)], tab)
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_eval_on_oracle_tables_matches_oracle(case):
+    name, moduli, S, n, seed, a0 = case
+    bp, op = _params_pair(moduli, S, n, seed, a0)
+    offs, zin, zout, tab = O.garble(op, a0, n)
+    x = _small_inputs(moduli, n, seed)
+    X = O.encode(op, x, zin, offs)
+    Y = O.evaluate(op, a0, n, X, tab)
+    out = torch.empty(len(X), dtype=torch.int32, device="cuda")
+    B.redash_eval_scale(bp, H.to_dev(X), H.to_dev(tab), out)
+    torch.cuda.synchronize()
+    got = H.to_u32(out)
+    assert np.array_equal(got, Y)
+    y, bad = O.decode(op, got, zout, offs)
+    s = rns.cardinality([moduli[i] for i in S])
+    assert bad.sum() == 0 and np.array_equal(y, _floor_div(x, s))
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_encode_and_decode_match_oracle(case):
+    name, moduli, S, n, seed, a0 = case
+    bp, op = _params_pair(moduli, S, n, seed, a0)
+    offs, zin, zout, _ = O.garble(op, a0, n, with_tables=False)
+    x = _small_inputs(moduli, n, seed)
+    lab = torch.empty(len(zin), dtype=torch.int32, device="cuda")
+    B.redash_encode(bp, H.to_dev(x), H.to_dev(zin), H.to_dev(offs), lab)
+    torch.cuda.synchronize()
+    X = O.encode(op, x, zin, offs)
+    assert np.array_equal(H.to_u32(lab), X)
+    # decode: labels of floor(x/s) under the output zero-labels, one corrupted
+    s = rns.cardinality([moduli[i] for i in S])
+    Yv = O.encode(op, _floor_div(x, s), zout, offs)
+    bad_at = n // 2
+    view = O.label_view(Yv, op, n, len(moduli) - 1)
+    m_last = moduli[-1]
+    r = O.pk32_unpack(m_last, view[:, bad_at].copy())
+    r[-1] = (r[-1] + 1) % m_last
+    view[:, bad_at] = O.pk32_pack(m_last, r)
+    y = torch.empty(n, dtype=torch.int64, device="cuda")
+    badc = torch.zeros(1, dtype=torch.int64, device="cuda")
+    B.redash_decode(bp, H.to_dev(Yv), H.to_dev(zout), H.to_dev(offs), y, badc)
+    torch.cuda.synchronize()
+    oy, obad = O.decode(op, Yv, zout, offs)
+    assert np.array_equal(y.cpu().numpy(), oy)
+    assert int(badc.item()) == int(obad.sum()) == 1
+    keep = np.arange(n) != bad_at
+    assert np.array_equal(oy[keep], _floor_div(x, s)[keep])
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_gpu_pipeline_decodes_floor(case):
+    name, moduli, S, n, seed, a0 = case
+    bp = B.make_params(moduli, S, n, seed, a0)
+    x = _small_inputs(moduli, n, seed)
+    buf = H.gpu_pipeline(bp, x)
+    s = rns.cardinality([moduli[i] for i in S])
+    assert int(buf.bad.item()) == 0
+    assert np.array_equal(buf.y.cpu().numpy()[:n], _floor_div(x, s))
+
+
+def test_eval_is_repeatable_and_leaves_inputs():
+    """The benchmark calls eval repeatedly on the same buffers."""
+    w = WL.DENSE
+    bp = B.make_params(w.moduli, w.scale_idx, 2048, w.seed)
+    x = _small_inputs(w.moduli, 2048, 4)
+    buf = H.gpu_pipeline(bp, x)
+    first = H.to_u32(buf.out_labels).copy()
+    inp = H.to_u32(buf.in_labels).copy()
+    for _ in range(3):
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.to_u32(buf.out_labels), first)
+    assert np.array_equal(H.to_u32(buf.in_labels), inp)
+
+
+def test_empty_calls_are_noops():
+    bp = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 0, 0)
+    sz = B.redash_plan(bp)
+    assert sz["label_words"] == 0 and sz["table_words"] == 0
+    offs = torch.empty(sz["offset_words"], dtype=torch.int32, device="cuda")
+    e = torch.empty(1, dtype=torch.int32, device="cuda")
+    B.redash_garble_scale(bp, offs, e, e, e)
+    B.redash_eval_scale(bp, e, e, e)
+    bad = torch.full((1,), 7, dtype=torch.int64, device="cuda")
+    B.redash_decode(bp, e, e, offs, torch.empty(1, dtype=torch.int64, device="cuda"), bad)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 0
+    assert np.array_equal(H.to_u32(offs), O.garble(O.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 1, 0), 0, 1)[0])
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads in the benchmark's launch configuration
+# ---------------------------------------------------------------------------
+
+def _sample_gadgets(n: int, seed: int, count: int = 96) -> np.ndarray:
+    rng = np.random.default_rng(seed + 777)
+    head = np.arange(min(16, n))
+    tail = np.arange(max(0, n - 16), n)
+    mid = rng.choice(n, size=min(count, n), replace=False)
+    return np.unique(np.concatenate([head, tail, mid])).astype(np.int64)
+
+
+def _check_full(w: WL.Workload, n_sample: int):
+    x = WL.make_inputs(w)
+    n = w.n
+    bp = B.make_params(w.moduli, w.scale_idx, n, w.seed)
+    op = O.make_params(list(w.moduli), list(w.scale_idx), 1, w.seed)
+    buf = H.gpu_pipeline(bp, x)
+    # every gadget: decode = floor(x/s) and every label valid
+    assert int(buf.bad.item()) == 0
+    assert np.array_equal(buf.y.cpu().numpy()[:n], _floor_div(x, w.s))
+    # sampled gadgets, word for word against the oracle garbling that gadget
+    gad = _sample_gadgets(n, w.seed, n_sample)
+    gates = O.gate_list(op)
+    gq = H.gate_list_sizes(gates, w.moduli)
+    li = H.label_index(w.moduli, n, gad)
+    ti = H.table_index(gq, n, gad)
+    g_zin = H.gather(buf.in_zero, li)
+    g_zout = H.gather(buf.out_zero, li)
+    g_out = H.gather(buf.out_labels, li)
+    g_tab = H.gather(buf.tables, ti)
+    k_words = len(li) // len(gad)
+    per_tab = len(ti) // len(gad)
+    offs_all = H.to_u32(buf.offsets)
+    for j, a in enumerate(gad):
+        offs, zin, zout, tab = O.garble(op, int(a), 1)
+        assert np.array_equal(offs_all, offs)
+        # reorder this gadget's words out of the gathered (modulus, word, gadget) order
+        sel = np.arange(k_words) * len(gad) + j
+        assert np.array_equal(g_zin[sel], zin), a
+        assert np.array_equal(g_zout[sel], zout), a
+        # expected evaluator output: output zero-label + floor(x/s) * R
+        Yexp = O.encode(op, np.array([_floor_div(x[a], w.s)]), zout, offs)
+        assert np.array_equal(g_out[sel], Yexp), a
+        # rows: gate blocks of (q-1) W words, gadget-major inside each gate
+        tsel, base = [], 0
+        for (q, W) in gq:
+            per = (q - 1) * W
+            tsel.append(base + j * per + np.arange(per))
+            base += len(gad) * per
+        assert np.array_equal(g_tab[np.concatenate(tsel)], tab), a
+    assert per_tab * len(gad) == len(ti)
+    del buf
+    torch.cuda.empty_cache()
+
+
+def test_full_size_conv():
+    _check_full(WL.CONV, 256)
+
+
+def test_full_size_batched():
+    """The benchmark workload: 16x64x56x56 gadgets, 12 primes, s = 37."""
+    _check_full(WL.BATCHED, 160)
+
+
+@pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
+def test_full_size_resnet18_layer(layer):
+    _check_full(layer, 24)
