@@ -7,6 +7,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "aes_tables.hpp"
 #include "plan.hpp"
 
@@ -20,6 +22,26 @@ constexpr int kMaxW = 6;  // largest W over moduli 2..255 (m = 3, 5, 17, 19)
 
 __device__ __forceinline__ void stage_round_tables(uint32_t *lds_tables, int tid, int nthreads) {
     for (int i = tid; i < kTableWords; i += nthreads) lds_tables[i] = g_round_tables.v[i];
+}
+
+// Calls f(std::integral_constant<int, J>{}) for J = 0 .. N-1: every index is
+// a compile-time constant, so arrays indexed by it stay in registers.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (N > 0) {
+        static_for<N - 1>(f);
+        f(std::integral_constant<int, N - 1>{});
+    }
+}
+
+// 24 x 24 -> low 32 bits (v_mul_u32_u24), as an unsigned value: HIP's
+// __umul24 returns int, and a right shift of that would be arithmetic.
+__device__ __forceinline__ uint32_t mul24(uint32_t a, uint32_t b) {
+    return static_cast<uint32_t>(__umul24(a, b));
+}
+
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);  // truth table of a ^ b ^ c
 }
 
 // ---------------------------------------------------------------------------
@@ -36,14 +58,17 @@ __device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, u
     s3 ^= rk(3);
 #pragma unroll
     for (int r = 1; r < 10; ++r) {
-        uint32_t t0 = T[s0 & 255] ^ T[256 + ((s1 >> 8) & 255)] ^ T[512 + ((s2 >> 16) & 255)] ^ T[768 + (s3 >> 24)];
-        uint32_t t1 = T[s1 & 255] ^ T[256 + ((s2 >> 8) & 255)] ^ T[512 + ((s3 >> 16) & 255)] ^ T[768 + (s0 >> 24)];
-        uint32_t t2 = T[s2 & 255] ^ T[256 + ((s3 >> 8) & 255)] ^ T[512 + ((s0 >> 16) & 255)] ^ T[768 + (s1 >> 24)];
-        uint32_t t3 = T[s3 & 255] ^ T[256 + ((s0 >> 8) & 255)] ^ T[512 + ((s1 >> 16) & 255)] ^ T[768 + (s2 >> 24)];
-        s0 = t0 ^ rk(4 * r);
-        s1 = t1 ^ rk(4 * r + 1);
-        s2 = t2 ^ rk(4 * r + 2);
-        s3 = t3 ^ rk(4 * r + 3);
+        // two 3-input XORs (v_bitop3_b32) per output column
+        uint32_t t0 = xor3(T[s0 & 255], T[256 + ((s1 >> 8) & 255)], T[512 + ((s2 >> 16) & 255)]);
+        uint32_t t1 = xor3(T[s1 & 255], T[256 + ((s2 >> 8) & 255)], T[512 + ((s3 >> 16) & 255)]);
+        uint32_t t2 = xor3(T[s2 & 255], T[256 + ((s3 >> 8) & 255)], T[512 + ((s0 >> 16) & 255)]);
+        uint32_t t3 = xor3(T[s3 & 255], T[256 + ((s0 >> 8) & 255)], T[512 + ((s1 >> 16) & 255)]);
+        const uint32_t u0 = T[768 + (s3 >> 24)], u1 = T[768 + (s0 >> 24)], u2 = T[768 + (s1 >> 24)],
+                       u3 = T[768 + (s2 >> 24)];
+        s0 = xor3(t0, u0, rk(4 * r));
+        s1 = xor3(t1, u1, rk(4 * r + 1));
+        s2 = xor3(t2, u2, rk(4 * r + 2));
+        s3 = xor3(t3, u3, rk(4 * r + 3));
     }
     // S(x) sits in byte 0 of TE2/TE3, byte 1 of TE0/TE3, byte 2 of TE0/TE1, byte 3 of TE1/TE2.
     uint32_t o0 = (T[512 + (s0 & 255)] & 0xffu) | (T[768 + ((s1 >> 8) & 255)] & 0xff00u) |
@@ -58,6 +83,43 @@ __device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, u
     s1 = o1 ^ rk(41);
     s2 = o2 ^ rk(42);
     s3 = o3 ^ rk(43);
+}
+
+// NB independent blocks encrypted round by round, so that the table reads of
+// all blocks are in flight together.
+template <int NB, typename KeyFn>
+__device__ __forceinline__ void aes128_encrypt_n(const uint32_t *__restrict__ T, uint32_t (&s)[NB][4], KeyFn rk) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) s[b][c] ^= rk(c);
+#pragma unroll
+    for (int r = 1; r < 10; ++r) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
+            const uint32_t t0 = xor3(T[s0 & 255], T[256 + ((s1 >> 8) & 255)], T[512 + ((s2 >> 16) & 255)]);
+            const uint32_t t1 = xor3(T[s1 & 255], T[256 + ((s2 >> 8) & 255)], T[512 + ((s3 >> 16) & 255)]);
+            const uint32_t t2 = xor3(T[s2 & 255], T[256 + ((s3 >> 8) & 255)], T[512 + ((s0 >> 16) & 255)]);
+            const uint32_t t3 = xor3(T[s3 & 255], T[256 + ((s0 >> 8) & 255)], T[512 + ((s1 >> 16) & 255)]);
+            s[b][0] = xor3(t0, T[768 + (s3 >> 24)], rk(4 * r));
+            s[b][1] = xor3(t1, T[768 + (s0 >> 24)], rk(4 * r + 1));
+            s[b][2] = xor3(t2, T[768 + (s1 >> 24)], rk(4 * r + 2));
+            s[b][3] = xor3(t3, T[768 + (s2 >> 24)], rk(4 * r + 3));
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
+        s[b][0] = ((T[512 + (s0 & 255)] & 0xffu) | (T[768 + ((s1 >> 8) & 255)] & 0xff00u) |
+                   (T[(s2 >> 16) & 255] & 0xff0000u) | (T[256 + (s3 >> 24)] & 0xff000000u)) ^ rk(40);
+        s[b][1] = ((T[512 + (s1 & 255)] & 0xffu) | (T[768 + ((s2 >> 8) & 255)] & 0xff00u) |
+                   (T[(s3 >> 16) & 255] & 0xff0000u) | (T[256 + (s0 >> 24)] & 0xff000000u)) ^ rk(41);
+        s[b][2] = ((T[512 + (s2 & 255)] & 0xffu) | (T[768 + ((s3 >> 8) & 255)] & 0xff00u) |
+                   (T[(s0 >> 16) & 255] & 0xff0000u) | (T[256 + (s1 >> 24)] & 0xff000000u)) ^ rk(42);
+        s[b][3] = ((T[512 + (s3 & 255)] & 0xffu) | (T[768 + ((s0 >> 8) & 255)] & 0xff00u) |
+                   (T[(s1 >> 16) & 255] & 0xff0000u) | (T[256 + (s2 >> 24)] & 0xff000000u)) ^ rk(43);
+    }
 }
 
 struct HashKey {
@@ -89,8 +151,8 @@ __device__ __forceinline__ uint32_t sub_mod(uint32_t a, uint32_t b, uint32_t m) 
 }
 
 __device__ __forceinline__ uint32_t mul_mod(uint32_t c, uint32_t a, const ModConst &mc) {
-    uint32_t p = __umul24(c, a);  // both < 256
-    return p - __umul24(div_m(p, mc), mc.m);
+    uint32_t p = mul24(c, a);  // both < 256
+    return p - mul24(div_m(p, mc), mc.m);
 }
 
 __device__ __forceinline__ uint32_t field(uint32_t word, uint32_t pos, const ModConst &mc) {
@@ -174,6 +236,60 @@ __device__ __forceinline__ uint32_t digits_word(uint32_t (&V)[8], uint32_t w, co
     return out | D;  // the most significant digit is residue 0 of the word
 }
 
+// floor(x / d) for a 32-bit x with constants from division_constants().
+__device__ __forceinline__ uint32_t div_const(uint32_t x, uint32_t M, uint32_t s, uint32_t fix) {
+    const uint32_t t = __umulhi(x, M);
+    return fix ? (t + ((x - t) >> 1)) >> s : t >> s;
+}
+
+// Evaluator fast path for one packed word over Z_m (m > 2, mc.fast set).
+// D holds the word's nres pad digits as a base-m number (residue 0 the most
+// significant digit).  For each residue j, with pad digit p, row residue r
+// and label residue l:
+//   sub gate (ACC = false): l <- c (l - p - r)      computed as c (l + 2m - p - r) < 3 m^2
+//   acc gate (ACC = true):  l <- l + c (p + r)      computed unreduced, < 2 m^2
+// followed by one multiply-shift reduction.  D is first split as
+// hi * m^nlo + lo so that every further digit division works on < 2^24.
+template <bool ACC>
+__device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t last, uint32_t rw, uint32_t l, uint32_t c,
+                                              const ModConst &mc) {
+    const uint32_t m = mc.m, b = mc.b, mask = mc.mask;
+    const uint32_t nres = last ? mc.glast : mc.g;
+    const uint32_t nlo = last ? mc.nlo[1] : mc.nlo[0];
+    uint32_t hi = D, lo = 0;
+    if (nlo) {
+        hi = div_const(D, last ? mc.lo_M[1] : mc.lo_M[0], last ? mc.lo_s[1] : mc.lo_s[0],
+                       last ? mc.lo_fix[1] : mc.lo_fix[0]);
+        lo = D - mul24(hi, last ? mc.pw_lo[1] : mc.pw_lo[0]);
+    }
+    auto residue = [&](uint32_t p, uint32_t j) -> uint32_t {
+        const uint32_t r = (rw >> (b * j)) & mask;
+        const uint32_t lj = (l >> (b * j)) & mask;
+        const uint32_t v = ACC ? lj + mul24(c, p + r) : mul24(c, lj + 2 * m - p - r);
+        const uint32_t q = mul24(v, mc.red_M) >> mc.red_s;
+        return (v - mul24(q, m)) << (b * j);
+    };
+    uint32_t res = 0;
+    const uint32_t nhi = nres - nlo;
+    // low part: positions nres-1 down to nhi (least significant digit first)
+    uint32_t x = lo;
+    for (uint32_t j = nres - 1; j > nhi; --j) {
+        const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
+        res |= residue(x - mul24(q, m), j);
+        x = q;
+    }
+    if (nlo) res |= residue(x, nhi);
+    // high part: positions nhi-1 down to 0
+    x = hi;
+    for (uint32_t j = nhi - 1; j > 0; --j) {
+        const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
+        res |= residue(x - mul24(q, m), j);
+        x = q;
+    }
+    res |= residue(x, 0);
+    return res;
+}
+
 // For m = 2 (128-bit fraction in V[0..3]) digit r is bit 127 - r of V, so
 // word w is the bit reversal of limb 3 - w.
 __device__ __forceinline__ uint32_t bits_word(const uint32_t (&V)[8], uint32_t w) {
@@ -213,6 +329,42 @@ __device__ __forceinline__ void hash_fraction(const uint32_t *T, uint32_t x0, ui
         V[7] = s3 ^ i3;
     } else {
         V[4] = V[5] = V[6] = V[7] = 0;
+    }
+}
+
+// The hash fractions of NG gates that share one input label (folded into
+// x0..x3): gate j uses tweak tau + j and two blocks (a gate whose output
+// modulus is 2 only reads V[j][0..3]).
+template <int NG>
+__device__ __forceinline__ void hash_fraction_n(const uint32_t *T, uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
+                                                uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
+    const uint32_t u0 = x2, u1 = x3, u2 = x2 ^ x0, u3 = x3 ^ x1;
+    uint32_t s[2 * NG][4];
+    uint32_t k0[2 * NG], k1[2 * NG];
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint64_t tw = (tau + static_cast<uint64_t>(j)) * 4u + static_cast<uint64_t>(h);
+            k0[2 * j + h] = static_cast<uint32_t>(tw);
+            k1[2 * j + h] = static_cast<uint32_t>(tw >> 32);
+            s[2 * j + h][0] = u0 ^ k0[2 * j + h];
+            s[2 * j + h][1] = u1 ^ k1[2 * j + h];
+            s[2 * j + h][2] = u2;
+            s[2 * j + h][3] = u3 ^ gid;
+        }
+    }
+    aes128_encrypt_n<2 * NG>(T, s, HashKey{});
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // Matyas-Meyer-Oseas feed-forward of the block input u ^ T
+            V[j][4 * h + 0] = s[2 * j + h][0] ^ u0 ^ k0[2 * j + h];
+            V[j][4 * h + 1] = s[2 * j + h][1] ^ u1 ^ k1[2 * j + h];
+            V[j][4 * h + 2] = s[2 * j + h][2] ^ u2;
+            V[j][4 * h + 3] = s[2 * j + h][3] ^ u3 ^ gid;
+        }
     }
 }
 

@@ -29,12 +29,14 @@ uint32_t ipow(uint32_t m, uint32_t e) {
     return static_cast<uint32_t>(r);
 }
 
-// Division constants for floor(x / m), x a 32-bit value below x_bound.
-void division_constants(uint32_t m, uint64_t x_bound, ModConst *mc) {
-    if (m == 2) {  // a plain shift; umulhi(x, 2^31) >> 0 = x >> 1
-        mc->divM = 0x80000000u;
-        mc->divS = 0;
-        mc->div_fix = 0;
+}  // namespace
+
+void division_constants(uint32_t m, uint64_t x_bound, uint32_t *outM, uint32_t *outS, uint32_t *outFix) {
+    if ((m & (m - 1)) == 0) {  // a power of two (m >= 2): umulhi(x, 2^(32-e)) = x >> e
+        const uint32_t e = bit_length(m) - 1;
+        *outM = 1u << (32 - e);
+        *outS = 0;
+        *outFix = 0;
         return;
     }
     // Round-up magic: s = floor(log2 m), M = ceil(2^(32+s) / m) < 2^32 for m
@@ -45,10 +47,11 @@ void division_constants(uint32_t m, uint64_t x_bound, ModConst *mc) {
     unsigned __int128 two = static_cast<unsigned __int128>(1) << (32 + s);
     unsigned __int128 M = (two + m - 1) / m;
     unsigned __int128 err = M * m - two;
-    if (M < (static_cast<unsigned __int128>(1) << 32) && static_cast<unsigned __int128>(x_bound) * err < two) {
-        mc->divM = static_cast<uint32_t>(M);
-        mc->divS = s;
-        mc->div_fix = 0;
+    if (M < (static_cast<unsigned __int128>(1) << 32) &&
+        static_cast<unsigned __int128>(x_bound - 1) * err < two) {
+        *outM = static_cast<uint32_t>(M);
+        *outS = s;
+        *outFix = 0;
         return;
     }
     // General 32-bit case: l = ceil(log2 m), M' = floor(2^32 (2^l - m) / m) + 1,
@@ -56,12 +59,27 @@ void division_constants(uint32_t m, uint64_t x_bound, ModConst *mc) {
     uint32_t l = bit_length(m - 1);
     unsigned __int128 Mp = ((static_cast<unsigned __int128>(1) << 32) *
                             ((static_cast<unsigned __int128>(1) << l) - m)) / m + 1;
-    mc->divM = static_cast<uint32_t>(Mp);
-    mc->divS = l - 1;
-    mc->div_fix = 1;
+    *outM = static_cast<uint32_t>(Mp);
+    *outS = l - 1;
+    *outFix = 1;
 }
 
-}  // namespace
+bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *outM, uint32_t *outS) {
+    if (x_bound > (1u << 24)) return false;
+    for (uint32_t s = 31; s >= 1; --s) {
+        const uint64_t two = 1ull << s;
+        const uint64_t M = (two + m - 1) / m;
+        if (M >= (1u << 24)) continue;
+        if ((x_bound - 1) * M >= (1ull << 32)) continue;
+        const uint64_t err = M * m - two;  // < m
+        if ((x_bound - 1) * err < two) {
+            *outM = static_cast<uint32_t>(M);
+            *outS = s;
+            return true;
+        }
+    }
+    return false;
+}
 
 uint32_t inverse_mod(uint32_t a, uint32_t m) {
     a %= m;
@@ -105,7 +123,24 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     // constants, so the bound covers them as well.
     uint64_t sq = static_cast<uint64_t>(m) * m;
     if (sq > bound) bound = sq;
-    division_constants(m, bound, mc);
+    division_constants(m, bound, &mc->divM, &mc->divS, &mc->div_fix);
+
+    if (m == 2) return;  // labels over Z_2 are bit vectors; no fast path needed
+    bool ok = mul24_constants(m, 3 * sq, &mc->red_M, &mc->red_s);
+    uint64_t part = 1;
+    for (int k = 0; k < 2; ++k) {
+        const uint32_t nres = k ? mc->glast : mc->g;
+        const uint32_t nlo = nres / 2, nhi = nres - nlo;
+        mc->nlo[k] = nlo;
+        mc->pw_lo[k] = ipow(m, nlo);
+        if (nlo) division_constants(mc->pw_lo[k], static_cast<uint64_t>(ipow(m, nres)), &mc->lo_M[k], &mc->lo_s[k],
+                                    &mc->lo_fix[k]);
+        const uint64_t hi = ipow(m, nhi), lo = ipow(m, nlo);
+        if (hi > part) part = hi;
+        if (lo > part) part = lo;
+    }
+    ok = ok && mul24_constants(m, part, &mc->sd_M, &mc->sd_s) && part < (1u << 24);
+    mc->fast = ok ? 1u : 0u;
 }
 
 int build_plan(const redash_params *p, Plan *pl) {
@@ -191,6 +226,18 @@ int build_plan(const redash_params *p, Plan *pl) {
         }
     }
     pl->G = G;
+    // Chunks: split every run of gates with one digit label into 4s, 2s and 1s.
+    for (uint32_t g = 0; g < G;) {
+        uint32_t run = 1;
+        while (g + run < G && gate_src(pl->gate[g + run]) == gate_src(pl->gate[g])) ++run;
+        for (uint32_t done = 0; done < run;) {
+            const uint32_t left = run - done;
+            const uint32_t len = left >= 4 ? 4 : (left >= 2 ? 2 : 1);
+            pl->gate[g + done] |= len << 24;
+            done += len;
+        }
+        g += run;
+    }
     return REDASH_OK;
 }
 

@@ -33,16 +33,32 @@ struct ModConst {
     uint32_t divM, divS, div_fix;
     uint32_t up;       // (P/2) mod m      (ShiftUp)
     uint32_t down;     // (P/(2s)) mod m   (ShiftDown)
+    // Evaluator fast path (fast == 1 when every bound below holds):
+    //  * red: floor(x/m) = (x * red_M) >> red_s for every x < 3 m^2, with
+    //    x * red_M < 2^32 (24-bit multiplies) -- one reduction per residue;
+    //  * sd: the same for every x below the larger part of a split word;
+    //  * a word's nres digits D (nres = g, or glast for the last word) are
+    //    split once as D = hi * m^nlo + lo, nlo = floor(nres/2), using the
+    //    32-bit division floor(D / m^nlo) described by lo_M/lo_s/lo_fix
+    //    (index 0: full word, 1: last word).
+    uint32_t fast;
+    uint32_t red_M, red_s, sd_M, sd_s;
+    uint32_t nlo[2], pw_lo[2], lo_M[2], lo_s[2], lo_fix[2];
 };
 
 // Gate descriptor packed in one word:
 //   bits 0-3 src modulus index, 4-7 dst modulus index, 8 kind (0 sub, 1 acc),
-//   9 phase (0 A, 1 B), 16-23 coefficient.
+//   9 phase (0 A, 1 B), 16-23 coefficient, 24-26 chunk length.
+// A chunk is a run of 1, 2 or 4 consecutive gates with the same digit label
+// (hence distinct destinations): the evaluator hashes them together.  The
+// chunk length is stored on the chunk's first gate and is 0 elsewhere.
 constexpr uint32_t gate_src(uint32_t d) { return d & 15u; }
 constexpr uint32_t gate_dst(uint32_t d) { return (d >> 4) & 15u; }
 constexpr uint32_t gate_kind(uint32_t d) { return (d >> 8) & 1u; }
 constexpr uint32_t gate_phase(uint32_t d) { return (d >> 9) & 1u; }
 constexpr uint32_t gate_coeff(uint32_t d) { return (d >> 16) & 255u; }
+constexpr uint32_t gate_chunk(uint32_t d) { return (d >> 24) & 7u; }
+constexpr int kMaxChunk = 4;
 
 struct Plan {
     uint32_t k, t, u, G;
@@ -67,6 +83,14 @@ uint32_t label_words(uint32_t m);
 
 // Fills one ModConst for modulus m (everything except woff, up, down).
 void fill_mod_const(uint32_t m, ModConst *mc);
+
+// Constants for floor(x / d), every x < x_bound (x_bound <= 2^32): if fix is
+// 0, umulhi(x, M) >> s; otherwise the round-up method with a fix-up step.
+void division_constants(uint32_t d, uint64_t x_bound, uint32_t *M, uint32_t *s, uint32_t *fix);
+
+// 24-bit multiply-shift constants: floor(x / m) = (x * M) >> s for every
+// x < x_bound with x * M < 2^32 and M < 2^24.  Returns false if none exist.
+bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *M, uint32_t *s);
 
 uint32_t inverse_mod(uint32_t a, uint32_t m);
 

@@ -24,6 +24,107 @@ struct SeedKey {
 // ---------------------------------------------------------------------------
 // Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
 // ---------------------------------------------------------------------------
+
+// Applies one gate's free operation to its destination label (packed words
+// at Ldst[w * stride]): E = row + pad, then L <- c (L - E) (sub: division
+// step and the recursion of Eq. rns_to_mrs) or L <- L + c E (acc: the
+// mixed-radix recombination onto a scaling modulus).
+__device__ __forceinline__ void eval_update(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
+                                            const uint32_t (&row)[kMaxW], uint32_t *Ldst, int stride) {
+    const uint32_t coeff = gate_coeff(d);
+    if (mm.m == 2) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t E = bits_word(V, w) ^ row[w];
+            uint32_t l = Ldst[w * stride];
+            if (gate_kind(d) == 0 || (coeff & 1u)) l ^= E;  // sub: q^{-1} = 1 mod 2
+            Ldst[w * stride] = l;
+        }
+    } else if (mm.fast) {
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) {
+            if (w < static_cast<int>(mm.W)) {
+                const uint32_t last = (w + 1 == static_cast<int>(mm.W)) ? 1u : 0u;
+                const uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
+                const uint32_t l = Ldst[w * stride];
+                Ldst[w * stride] = gate_kind(d) == 0 ? fast_word<false>(D, last, row[w], l, coeff, mm)
+                                                     : fast_word<true>(D, last, row[w], l, coeff, mm);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) {
+            if (w < static_cast<int>(mm.W)) {
+                const bool last = (w + 1 == static_cast<int>(mm.W));
+                const uint32_t nres = last ? mm.glast : mm.g;
+                uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
+                const uint32_t rw = row[w];
+                const uint32_t l = Ldst[w * stride];
+                uint32_t res = 0;
+                // Digits come out least significant first: position nres-1 down to 0.
+                for (uint32_t j = nres; j-- > 0;) {
+                    uint32_t pd;
+                    if (j) {
+                        const uint32_t qd = div_m(D, mm);
+                        pd = D - qd * mm.m;
+                        D = qd;
+                    } else {
+                        pd = D;
+                    }
+                    const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
+                    const uint32_t lj = field(l, j, mm);
+                    const uint32_t r = gate_kind(d) == 0 ? mul_mod(coeff, sub_mod(lj, e, mm.m), mm)
+                                                         : add_mod(lj, mul_mod(coeff, e, mm), mm.m);
+                    res |= r << (mm.b * j);
+                }
+                Ldst[w * stride] = res;
+            }
+        }
+    }
+}
+
+// Evaluates the NG gates g..g+NG-1, which share one digit label: the rows of
+// all of them are requested first (the colour is known before hashing), the
+// 2 NG AES blocks run interleaved, then each destination is updated.
+template <int NG, int BLOCK>
+__device__ __forceinline__ void eval_chunk(const Plan &P, uint32_t g, uint64_t &toff, const uint32_t *TT, uint32_t *L,
+                                           int tid, uint64_t a, uint64_t tau0, const uint32_t *__restrict__ tab) {
+    const uint64_t n = P.n;
+    uint32_t dd[NG];
+    ModConst mm[NG];
+    static_for<NG>([&](auto j) {
+        dd[j] = P.gate[g + j];
+        mm[j] = P.mod[gate_dst(dd[j])];
+    });
+    const ModConst mq = P.mod[gate_src(dd[0])];
+    const uint32_t q = mq.m;
+    const uint32_t *Lsrc = L + mq.woff * BLOCK + tid;
+    const uint32_t w0 = Lsrc[0];
+    // A residue >= q only occurs in a malformed input label; it selects the
+    // implicit zero row, the output is garbage and decode flags it.
+    uint32_t colour = w0 & mq.mask;
+    if (colour >= q) colour = 0;
+    uint32_t row[NG][kMaxW];
+    static_for<NG>([&](auto j) {
+        static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
+        if (colour != 0) {
+            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * mm[j].W;
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(mm[j].W)) row[j][w] = rp[w];
+            });
+        }
+        toff += n * (q - 1) * mm[j].W;
+    });
+    uint32_t x[4] = {w0, 0, 0, 0};
+    static_for<kMaxW - 1>([&](auto w1) {
+        constexpr int w = decltype(w1)::value + 1;
+        if (w < static_cast<int>(mq.W)) x[w & 3] ^= Lsrc[w * BLOCK];
+    });
+    uint32_t V[NG][8];
+    hash_fraction_n<NG>(TT, x[0], x[1], x[2], x[3], tau0 + g, P.gid, V);
+    static_for<NG>([&](auto j) { eval_update(dd[j], mm[j], V[j], row[j], L + mm[j].woff * BLOCK + tid, BLOCK); });
+}
+
 template <int BLOCK>
 __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__restrict__ in,
                                                 const uint32_t *__restrict__ tab, uint32_t *__restrict__ out) {
@@ -46,7 +147,7 @@ __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__
     const uint64_t tau0 = (P.a0 + a) * P.G;
     uint64_t toff = 0;
     bool phaseB = false;
-    for (uint32_t g = 0; g < P.G; ++g) {
+    for (uint32_t g = 0; g < P.G;) {
         const uint32_t d = P.gate[g];
         if (gate_phase(d) && !phaseB) {
             // End of the division step: the remaining-modulus labels are the
@@ -63,87 +164,16 @@ __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__
                 for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = 0;
             }
         }
-        const ModConst &mq = P.mod[gate_src(d)];
-        const ModConst &mm = P.mod[gate_dst(d)];
-        const uint32_t q = mq.m;
-        const uint32_t *Lsrc = L + mq.woff * BLOCK + tid;
-        uint32_t *Ldst = L + mm.woff * BLOCK + tid;
-
-        // Colour of the digit label: its first residue.  The row is fetched
-        // before the hash so the load latency hides under the AES rounds.
-        const uint32_t w0 = Lsrc[0];
-        // A residue >= q only occurs in a malformed input label; it selects
-        // the implicit zero row, the output is garbage and decode flags it.
-        uint32_t colour = w0 & mq.mask;
-        if (colour >= q) colour = 0;
-        uint32_t row[kMaxW];
-#pragma unroll
-        for (int w = 0; w < kMaxW; ++w) row[w] = 0;
-        if (colour != 0) {
-            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * mm.W;
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w)
-                if (w < static_cast<int>(mm.W)) row[w] = rp[w];
-        }
-        toff += n * (q - 1) * mm.W;
-
-        uint32_t x[4] = {w0, 0, 0, 0};
-#pragma unroll
-        for (int w = 1; w < kMaxW; ++w)
-            if (w < static_cast<int>(mq.W)) x[w & 3] ^= Lsrc[w * BLOCK];
-        uint32_t V[8];
-        hash_fraction(TT, x[0], x[1], x[2], x[3], tau0 + g, P.gid, mm.m != 2, V);
-
-        const uint32_t coeff = gate_coeff(d);
-        if (mm.m == 2) {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const uint32_t E = bits_word(V, w) ^ row[w];
-                uint32_t l = Ldst[w * BLOCK];
-                if (gate_kind(d) == 0 || (coeff & 1u)) l ^= E;  // sub: q^{-1} = 1 mod 2
-                Ldst[w * BLOCK] = l;
-            }
+        const uint32_t len = gate_chunk(d);
+        if (len == 4) {
+            eval_chunk<4, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
+            g += 4;
+        } else if (len == 2) {
+            eval_chunk<2, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
+            g += 2;
         } else {
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w) {
-                if (w < static_cast<int>(mm.W)) {
-                    const bool last = (w + 1 == static_cast<int>(mm.W));
-                    const uint32_t nres = last ? mm.glast : mm.g;
-                    uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
-                    const uint32_t rw = row[w];
-                    const uint32_t l = Ldst[w * BLOCK];
-                    uint32_t res = 0;
-                    // Digits come out least significant first: position nres-1 down to 0.
-                    if (gate_kind(d) == 0) {
-                        for (uint32_t j = nres; j-- > 0;) {
-                            uint32_t pd;
-                            if (j) {
-                                const uint32_t qd = div_m(D, mm);
-                                pd = D - qd * mm.m;
-                                D = qd;
-                            } else {
-                                pd = D;
-                            }
-                            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
-                            res |= mul_mod(coeff, sub_mod(field(l, j, mm), e, mm.m), mm) << (mm.b * j);
-                        }
-                    } else {
-                        for (uint32_t j = nres; j-- > 0;) {
-                            uint32_t pd;
-                            if (j) {
-                                const uint32_t qd = div_m(D, mm);
-                                pd = D - qd * mm.m;
-                                D = qd;
-                            } else {
-                                pd = D;
-                            }
-                            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
-                            res |= add_mod(field(l, j, mm), mul_mod(coeff, e, mm), mm.m) << (mm.b * j);
-                        }
-                    }
-                    Ldst[w * BLOCK] = res;
-                }
-            }
+            eval_chunk<1, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
+            g += 1;
         }
     }
     for (uint32_t s = 0; s < P.t; ++s) {
