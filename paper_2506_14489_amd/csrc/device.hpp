@@ -34,6 +34,36 @@ __device__ __forceinline__ void static_for(F &&f) {
     }
 }
 
+// Takes the first word of a small register array and shifts the rest down:
+// a rolled loop can walk the array while every index stays a constant (a
+// runtime index would move the array to scratch memory).
+template <int N>
+__device__ __forceinline__ uint32_t next_word(uint32_t (&a)[N]) {
+    const uint32_t v = a[0];
+#pragma unroll
+    for (int j = 0; j + 1 < N; ++j) a[j] = a[j + 1];
+    return v;
+}
+
+// The value itself, through an empty asm statement that the optimizer cannot
+// see into (no instruction is emitted).  Used on the digit x - q m: if it is
+// merged into the following arithmetic, the compiler rewrites the product q m
+// as one it cannot prove to be 24-bit and emits a quarter-rate multiply.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+// A wave-uniform value masked to 24 bits in the calling block.  Instruction
+// selection only uses v_mul_u32_u24 when it sees both operands' 24-bit bound
+// in the same basic block; a mask hoisted out of the block (as the compiler
+// does with a plain expression) is invisible to it, and the multiply becomes
+// the quarter-rate 32-bit one.  The empty volatile asm keeps the mask here.
+__device__ __forceinline__ uint32_t uniform24(uint32_t v) {
+    asm volatile("" : "+s"(v));
+    return v & 0xffffffu;
+}
+
 // 24 x 24 -> low 32 bits (v_mul_u32_u24), as an unsigned value: HIP's
 // __umul24 returns int, and a right shift of that would be arithmetic.
 __device__ __forceinline__ uint32_t mul24(uint32_t a, uint32_t b) {
@@ -44,87 +74,130 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
     return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);  // truth table of a ^ b ^ c
 }
 
-// ---------------------------------------------------------------------------
-// AES-128 encryption of one block held as four little-endian column words.
-// Rounds 1..9 use TE0..TE3; the last round takes each S-box byte from the
-// table in which it already sits at the right byte position.
-// ---------------------------------------------------------------------------
-template <typename KeyFn>
-__device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, uint32_t &s0, uint32_t &s1,
-                                               uint32_t &s2, uint32_t &s3, KeyFn rk) {
-    s0 ^= rk(0);
-    s1 ^= rk(1);
-    s2 ^= rk(2);
-    s3 ^= rk(3);
-#pragma unroll
-    for (int r = 1; r < 10; ++r) {
-        // two 3-input XORs (v_bitop3_b32) per output column
-        uint32_t t0 = xor3(T[s0 & 255], T[256 + ((s1 >> 8) & 255)], T[512 + ((s2 >> 16) & 255)]);
-        uint32_t t1 = xor3(T[s1 & 255], T[256 + ((s2 >> 8) & 255)], T[512 + ((s3 >> 16) & 255)]);
-        uint32_t t2 = xor3(T[s2 & 255], T[256 + ((s3 >> 8) & 255)], T[512 + ((s0 >> 16) & 255)]);
-        uint32_t t3 = xor3(T[s3 & 255], T[256 + ((s0 >> 8) & 255)], T[512 + ((s1 >> 16) & 255)]);
-        const uint32_t u0 = T[768 + (s3 >> 24)], u1 = T[768 + (s0 >> 24)], u2 = T[768 + (s1 >> 24)],
-                       u3 = T[768 + (s2 >> 24)];
-        s0 = xor3(t0, u0, rk(4 * r));
-        s1 = xor3(t1, u1, rk(4 * r + 1));
-        s2 = xor3(t2, u2, rk(4 * r + 2));
-        s3 = xor3(t3, u3, rk(4 * r + 3));
+// Round-table access policies.  te(t, w, k) = TEt[byte k of w] and
+// sb4(w0, w1, w2, w3) = the column (S(byte 0 of w0), S(byte 1 of w1),
+// S(byte 2 of w2), S(byte 3 of w3)) of the last round.
+//
+// FourTables: TE0..TE3 back to back (1024 words); each S-box byte is taken
+// from the table in which it already sits at the right byte position.
+struct FourTables {
+    const uint32_t *T;
+    __device__ __forceinline__ uint32_t te(int t, uint32_t w, int k) const {
+        return T[256 * t + ((w >> (8 * k)) & 255u)];
     }
-    // S(x) sits in byte 0 of TE2/TE3, byte 1 of TE0/TE3, byte 2 of TE0/TE1, byte 3 of TE1/TE2.
-    uint32_t o0 = (T[512 + (s0 & 255)] & 0xffu) | (T[768 + ((s1 >> 8) & 255)] & 0xff00u) |
-                  (T[(s2 >> 16) & 255] & 0xff0000u) | (T[256 + (s3 >> 24)] & 0xff000000u);
-    uint32_t o1 = (T[512 + (s1 & 255)] & 0xffu) | (T[768 + ((s2 >> 8) & 255)] & 0xff00u) |
-                  (T[(s3 >> 16) & 255] & 0xff0000u) | (T[256 + (s0 >> 24)] & 0xff000000u);
-    uint32_t o2 = (T[512 + (s2 & 255)] & 0xffu) | (T[768 + ((s3 >> 8) & 255)] & 0xff00u) |
-                  (T[(s0 >> 16) & 255] & 0xff0000u) | (T[256 + (s1 >> 24)] & 0xff000000u);
-    uint32_t o3 = (T[512 + (s3 & 255)] & 0xffu) | (T[768 + ((s0 >> 8) & 255)] & 0xff00u) |
-                  (T[(s1 >> 16) & 255] & 0xff0000u) | (T[256 + (s2 >> 24)] & 0xff000000u);
-    s0 = o0 ^ rk(40);
-    s1 = o1 ^ rk(41);
-    s2 = o2 ^ rk(42);
-    s3 = o3 ^ rk(43);
+    __device__ __forceinline__ uint32_t sb4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) const {
+        // S(x) is byte 0 of TE2, byte 1 of TE3, byte 2 of TE0, byte 3 of TE1
+        return (T[512 + (w0 & 255u)] & 0xffu) | (T[768 + ((w1 >> 8) & 255u)] & 0xff00u) |
+               (T[(w2 >> 16) & 255u] & 0xff0000u) | (T[256 + (w3 >> 24)] & 0xff000000u);
+    }
+};
+
+// PermTE0: TE0 in 32 copies; entry x is the 256-byte LDS row x, copy c at
+// byte 4c of the row (the upper 128 bytes of every row are free for other
+// data).  Lane l reads copy l mod 32, which sits in bank l mod 32, so a
+// wavefront's lookups never conflict, and one v_perm_b32 builds the address
+// 256 x + 4 (l mod 32) straight from the state word.  TE1..3 are byte
+// rotations of TE0.
+constexpr int kReplicas = 32;
+constexpr uint32_t kTableRowBytes = 256;
+constexpr uint32_t kTableRegionBytes = 256 * kTableRowBytes;  // 64 KiB
+
+// The table region must start at LDS address 0: the kernels that use it
+// declare no static LDS, so their dynamic LDS array begins there, and the
+// absolute address then needs no base addition per lookup.
+typedef __attribute__((address_space(3))) const uint32_t lds_u32;
+typedef __attribute__((address_space(3))) uint32_t lds_u32_rw;
+
+struct PermTE0 {
+    uint32_t lane_off;  // 4 (lane mod 32), below 128
+    __device__ __forceinline__ uint32_t te0(uint32_t w, int k) const {
+        // address bytes: [lane_off, byte k of w, 0, 0]
+        const uint32_t addr = __builtin_amdgcn_perm(w, lane_off, 0x0c0c0000u | ((4u + k) << 8));
+        return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
+    }
+    __device__ __forceinline__ uint32_t te(int t, uint32_t w, int k) const {
+        const uint32_t v = te0(w, k);
+        return t == 0 ? v : __builtin_amdgcn_alignbit(v, v, 32 - 8 * t);  // rotate left by 8t
+    }
+    __device__ __forceinline__ uint32_t sb4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) const {
+        // TE0[x] holds S(x) in byte 1: gather byte 1 of the four entries
+        const uint32_t lo = __builtin_amdgcn_perm(te0(w1, 1), te0(w0, 0), 0x0c0c0501u);
+        const uint32_t hi = __builtin_amdgcn_perm(te0(w3, 3), te0(w2, 2), 0x05010c0cu);
+        return lo | hi;
+    }
+};
+
+__device__ __forceinline__ void stage_perm_te0(uint32_t *lds, int tid, int nthreads) {
+    // the lower 32 words of each 64-word row: TE0[row] in every copy
+    for (int i = tid; i < 256 * kReplicas; i += nthreads) lds[(i / kReplicas) * 64 + (i % kReplicas)] = g_round_tables.v[i / kReplicas];
 }
+
+__device__ __forceinline__ PermTE0 perm_te0() { return PermTE0{4u * (threadIdx.x % kReplicas)}; }
 
 // NB independent blocks encrypted round by round, so that the table reads of
 // all blocks are in flight together.
-template <int NB, typename KeyFn>
-__device__ __forceinline__ void aes128_encrypt_n(const uint32_t *__restrict__ T, uint32_t (&s)[NB][4], KeyFn rk) {
+template <int NB, typename Tab, typename KeyFn>
+__device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB][4], KeyFn rk) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int c = 0; c < 4; ++c) s[b][c] ^= rk(c);
-#pragma unroll
+    // Rounds 1..9 stay a loop (the round keys are uniform loads): the
+    // instruction cache holds the whole gate loop that way.
+#pragma unroll 1
     for (int r = 1; r < 10; ++r) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-            const uint32_t t0 = xor3(T[s0 & 255], T[256 + ((s1 >> 8) & 255)], T[512 + ((s2 >> 16) & 255)]);
-            const uint32_t t1 = xor3(T[s1 & 255], T[256 + ((s2 >> 8) & 255)], T[512 + ((s3 >> 16) & 255)]);
-            const uint32_t t2 = xor3(T[s2 & 255], T[256 + ((s3 >> 8) & 255)], T[512 + ((s0 >> 16) & 255)]);
-            const uint32_t t3 = xor3(T[s3 & 255], T[256 + ((s0 >> 8) & 255)], T[512 + ((s1 >> 16) & 255)]);
-            s[b][0] = xor3(t0, T[768 + (s3 >> 24)], rk(4 * r));
-            s[b][1] = xor3(t1, T[768 + (s0 >> 24)], rk(4 * r + 1));
-            s[b][2] = xor3(t2, T[768 + (s1 >> 24)], rk(4 * r + 2));
-            s[b][3] = xor3(t3, T[768 + (s2 >> 24)], rk(4 * r + 3));
+            const uint32_t t0 = xor3(T.te(0, s0, 0), T.te(1, s1, 1), T.te(2, s2, 2));
+            const uint32_t t1 = xor3(T.te(0, s1, 0), T.te(1, s2, 1), T.te(2, s3, 2));
+            const uint32_t t2 = xor3(T.te(0, s2, 0), T.te(1, s3, 1), T.te(2, s0, 2));
+            const uint32_t t3 = xor3(T.te(0, s3, 0), T.te(1, s0, 1), T.te(2, s1, 2));
+            s[b][0] = xor3(t0, T.te(3, s3, 3), rk(4 * r));
+            s[b][1] = xor3(t1, T.te(3, s0, 3), rk(4 * r + 1));
+            s[b][2] = xor3(t2, T.te(3, s1, 3), rk(4 * r + 2));
+            s[b][3] = xor3(t3, T.te(3, s2, 3), rk(4 * r + 3));
         }
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-        s[b][0] = ((T[512 + (s0 & 255)] & 0xffu) | (T[768 + ((s1 >> 8) & 255)] & 0xff00u) |
-                   (T[(s2 >> 16) & 255] & 0xff0000u) | (T[256 + (s3 >> 24)] & 0xff000000u)) ^ rk(40);
-        s[b][1] = ((T[512 + (s1 & 255)] & 0xffu) | (T[768 + ((s2 >> 8) & 255)] & 0xff00u) |
-                   (T[(s3 >> 16) & 255] & 0xff0000u) | (T[256 + (s0 >> 24)] & 0xff000000u)) ^ rk(41);
-        s[b][2] = ((T[512 + (s2 & 255)] & 0xffu) | (T[768 + ((s3 >> 8) & 255)] & 0xff00u) |
-                   (T[(s0 >> 16) & 255] & 0xff0000u) | (T[256 + (s1 >> 24)] & 0xff000000u)) ^ rk(42);
-        s[b][3] = ((T[512 + (s3 & 255)] & 0xffu) | (T[768 + ((s0 >> 8) & 255)] & 0xff00u) |
-                   (T[(s1 >> 16) & 255] & 0xff0000u) | (T[256 + (s2 >> 24)] & 0xff000000u)) ^ rk(43);
+        s[b][0] = T.sb4(s0, s1, s2, s3) ^ rk(40);
+        s[b][1] = T.sb4(s1, s2, s3, s0) ^ rk(41);
+        s[b][2] = T.sb4(s2, s3, s0, s1) ^ rk(42);
+        s[b][3] = T.sb4(s3, s0, s1, s2) ^ rk(43);
     }
 }
 
+// One block held as four little-endian column words, on the four tables.
+template <typename KeyFn>
+__device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, uint32_t &s0, uint32_t &s1,
+                                               uint32_t &s2, uint32_t &s3, KeyFn rk) {
+    uint32_t s[1][4] = {{s0, s1, s2, s3}};
+    aes128_encrypt_n<1>(FourTables{T}, s, rk);
+    s0 = s[0][0];
+    s1 = s[0][1];
+    s2 = s[0][2];
+    s3 = s[0][3];
+}
+
+__constant__ RoundKeys c_hash_key = kHashKey;
+
 struct HashKey {
-    __device__ __forceinline__ uint32_t operator()(int i) const { return kHashKey.w[i]; }
+    __device__ __forceinline__ uint32_t operator()(int i) const { return c_hash_key.w[i]; }
 };
+
+// Round keys held in LDS (every lane reads the same word, a broadcast):
+// unlike scalar loads, LDS reads complete in order with the table reads, so
+// the wait counters never have to drain inside the round loop.
+struct LdsKey {
+    const uint32_t *w;
+    __device__ __forceinline__ uint32_t operator()(int i) const { return w[i]; }
+};
+
+__device__ __forceinline__ void stage_hash_key(uint32_t *lds, int tid, int nthreads) {
+    for (int i = tid; i < 44; i += nthreads) lds[i] = c_hash_key.w[i];
+}
 
 struct ArgKey {
     const uint32_t *w;
@@ -140,14 +213,18 @@ __device__ __forceinline__ uint32_t div_m(uint32_t x, const ModConst &mc) {
     return t >> mc.divS;
 }
 
+// By value (a reference-returning min would make the compiler keep its
+// operands in scratch memory).
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
 __device__ __forceinline__ uint32_t add_mod(uint32_t a, uint32_t b, uint32_t m) {
     uint32_t s = a + b;
-    return min(s, s - m);  // s - m wraps above s exactly when s < m
+    return umin(s, s - m);  // s - m wraps above s exactly when s < m
 }
 
 __device__ __forceinline__ uint32_t sub_mod(uint32_t a, uint32_t b, uint32_t m) {
     uint32_t d = a - b;
-    return min(d, d + m);  // d wraps when a < b; d + m then lands in [0, m)
+    return umin(d, d + m);  // d wraps when a < b; d + m then lands in [0, m)
 }
 
 __device__ __forceinline__ uint32_t mul_mod(uint32_t c, uint32_t a, const ModConst &mc) {
@@ -251,21 +328,22 @@ __device__ __forceinline__ uint32_t div_const(uint32_t x, uint32_t M, uint32_t s
 // followed by one multiply-shift reduction.  D is first split as
 // hi * m^nlo + lo so that every further digit division works on < 2^24.
 template <bool ACC>
-__device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t last, uint32_t rw, uint32_t l, uint32_t c,
+__device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_t nlo, uint32_t lo_M, uint32_t lo_s,
+                                              uint32_t pw_lo, uint32_t rw, uint32_t l, uint32_t c,
                                               const ModConst &mc) {
     const uint32_t m = mc.m, b = mc.b, mask = mc.mask;
-    const uint32_t nres = last ? mc.glast : mc.g;
-    const uint32_t nlo = last ? mc.nlo[1] : mc.nlo[0];
     uint32_t hi = D, lo = 0;
     if (nlo) {
-        hi = div_const(D, last ? mc.lo_M[1] : mc.lo_M[0], last ? mc.lo_s[1] : mc.lo_s[0],
-                       last ? mc.lo_fix[1] : mc.lo_fix[0]);
-        lo = D - mul24(hi, last ? mc.pw_lo[1] : mc.pw_lo[0]);
+        hi = __umulhi(D, lo_M) >> lo_s;
+        lo = D - mul24(hi, pw_lo);
     }
+    // mc.two_m (= 2m) is a separate field on purpose: were the compiler to
+    // see it as 2 * m, it would fold "+ 2m - (x - q m)" into (q + 2) m, a
+    // product it cannot prove to be 24-bit (quarter-rate multiply).
     auto residue = [&](uint32_t p, uint32_t j) -> uint32_t {
         const uint32_t r = (rw >> (b * j)) & mask;
         const uint32_t lj = (l >> (b * j)) & mask;
-        const uint32_t v = ACC ? lj + mul24(c, p + r) : mul24(c, lj + 2 * m - p - r);
+        const uint32_t v = ACC ? lj + mul24(c, p + r) : mul24(c, lj + mc.two_m - p - r);
         const uint32_t q = mul24(v, mc.red_M) >> mc.red_s;
         return (v - mul24(q, m)) << (b * j);
     };
@@ -273,21 +351,95 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t last, uint32_
     const uint32_t nhi = nres - nlo;
     // low part: positions nres-1 down to nhi (least significant digit first)
     uint32_t x = lo;
+#pragma unroll 2
     for (uint32_t j = nres - 1; j > nhi; --j) {
         const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
-        res |= residue(x - mul24(q, m), j);
+        res |= residue(opaque(x - mul24(q, m)), j);
         x = q;
     }
     if (nlo) res |= residue(x, nhi);
     // high part: positions nhi-1 down to 0
     x = hi;
+#pragma unroll 2
     for (uint32_t j = nhi - 1; j > 0; --j) {
         const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
-        res |= residue(x - mul24(q, m), j);
+        res |= residue(opaque(x - mul24(q, m)), j);
         x = q;
     }
     res |= residue(x, 0);
     return res;
+}
+
+// fast_word with the residue count and field width known at compile time:
+// every loop unrolled, every shift an immediate.
+template <bool ACC, int NRES, int B>
+__device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo,
+                                                uint32_t rw, uint32_t l, uint32_t c, const ModConst &mc) {
+    constexpr int NLO = NRES / 2, NHI = NRES - NLO;
+    constexpr uint32_t MASK = (1u << B) - 1u;
+    const uint32_t m = uniform24(mc.m);
+    c = uniform24(c);
+    uint32_t hi = D, lo = 0;
+    if constexpr (NLO > 0) {
+        hi = __umulhi(D, lo_M) >> lo_s;
+        lo = D - mul24(hi, pw_lo);
+    }
+    uint32_t res = 0;
+    // Every multiply below must see both operands' 24-bit bound in this block
+    // (v_mul_u32_u24): shifted quotients and the sub gate's difference go
+    // through a bit-field extract of width 24 or 16, whose bound the
+    // instruction selector always sees (one op, like the shift it replaces).
+    auto residue = [&](uint32_t p, auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const uint32_t r = (rw >> (B * j)) & MASK;
+        const uint32_t lj = (l >> (B * j)) & MASK;
+        const uint32_t v = ACC ? lj + mul24(c, __builtin_amdgcn_ubfe(p + r, 0, 16))
+                               : mul24(c, __builtin_amdgcn_ubfe(lj + mc.two_m - p - r, 0, 16));
+        const uint32_t q = __builtin_amdgcn_ubfe(mul24(v, mc.red_M), mc.red_s, 24);
+        // (opaque: a shift folded into the product would widen its operand)
+        res |= opaque(v - mul24(q, m)) << (B * j);
+    };
+    // low part: positions NRES-1 down to NHI; high part: NHI-1 down to 0
+    uint32_t x = lo;
+    static_for<NLO>([&](auto k) {
+        constexpr int j = NRES - 1 - decltype(k)::value;
+        if constexpr (j > NHI) {
+            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
+            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
+            x = q;
+        } else {
+            residue(x, std::integral_constant<int, j>{});
+        }
+    });
+    x = hi;
+    static_for<NHI>([&](auto k) {
+        constexpr int j = NHI - 1 - decltype(k)::value;
+        if constexpr (j > 0) {
+            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
+            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
+            x = q;
+        } else {
+            residue(x, std::integral_constant<int, 0>{});
+        }
+    });
+    return res;
+}
+
+// Dispatch on (residues in the word, bits per residue): the combinations
+// of the primes up to 37 are unrolled, anything else takes the loops.
+template <bool ACC>
+__device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uint32_t nlo, uint32_t lo_M,
+                                                  uint32_t lo_s, uint32_t pw_lo, uint32_t rw, uint32_t l, uint32_t c,
+                                                  const ModConst &mc) {
+    switch (nres | (mc.b << 8)) {
+#define REDASH_FW(NR, BB) \
+    case (NR) | ((BB) << 8): return fast_word_c<ACC, NR, BB>(D, lo_M, lo_s, pw_lo, rw, l, c, mc);
+        REDASH_FW(16, 2) REDASH_FW(1, 2) REDASH_FW(10, 3) REDASH_FW(6, 3) REDASH_FW(8, 4) REDASH_FW(6, 4)
+        REDASH_FW(3, 4) REDASH_FW(6, 5) REDASH_FW(5, 5) REDASH_FW(3, 5) REDASH_FW(2, 5) REDASH_FW(1, 5)
+        REDASH_FW(5, 6)
+#undef REDASH_FW
+        default: return fast_word<ACC>(D, nres, nlo, lo_M, lo_s, pw_lo, rw, l, c, mc);
+    }
 }
 
 // For m = 2 (128-bit fraction in V[0..3]) digit r is bit 127 - r of V, so
@@ -317,27 +469,32 @@ __device__ __forceinline__ void hash_fraction(const uint32_t *T, uint32_t x0, ui
         V[2] = s2 ^ i2;
         V[3] = s3 ^ i3;
     }
+    // (scalars rather than array stores inside the branch, which the
+    // compiler would otherwise route through scratch memory)
+    uint32_t h0 = 0, h1 = 0, h2 = 0, h3 = 0;
     if (two_blocks) {
         const uint64_t tw1 = tw + 1u;
         const uint32_t k0 = static_cast<uint32_t>(tw1), k1 = static_cast<uint32_t>(tw1 >> 32);
         uint32_t s0 = u0 ^ k0, s1 = u1 ^ k1, s2 = u2, s3 = u3 ^ gid;
         const uint32_t i0 = s0, i1 = s1, i2 = s2, i3 = s3;
         aes128_encrypt(T, s0, s1, s2, s3, HashKey{});
-        V[4] = s0 ^ i0;
-        V[5] = s1 ^ i1;
-        V[6] = s2 ^ i2;
-        V[7] = s3 ^ i3;
-    } else {
-        V[4] = V[5] = V[6] = V[7] = 0;
+        h0 = s0 ^ i0;
+        h1 = s1 ^ i1;
+        h2 = s2 ^ i2;
+        h3 = s3 ^ i3;
     }
+    V[4] = h0;
+    V[5] = h1;
+    V[6] = h2;
+    V[7] = h3;
 }
 
 // The hash fractions of NG gates that share one input label (folded into
 // x0..x3): gate j uses tweak tau + j and two blocks (a gate whose output
 // modulus is 2 only reads V[j][0..3]).
-template <int NG>
-__device__ __forceinline__ void hash_fraction_n(const uint32_t *T, uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
-                                                uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
+template <int NG, typename Tab, typename KeyFn>
+__device__ __forceinline__ void hash_fraction_n(const Tab &T, KeyFn rk, uint32_t x0, uint32_t x1, uint32_t x2,
+                                                uint32_t x3, uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
     const uint32_t u0 = x2, u1 = x3, u2 = x2 ^ x0, u3 = x3 ^ x1;
     uint32_t s[2 * NG][4];
     uint32_t k0[2 * NG], k1[2 * NG];
@@ -354,7 +511,7 @@ __device__ __forceinline__ void hash_fraction_n(const uint32_t *T, uint32_t x0, 
             s[2 * j + h][3] = u3 ^ gid;
         }
     }
-    aes128_encrypt_n<2 * NG>(T, s, HashKey{});
+    aes128_encrypt_n<2 * NG>(T, s, rk);
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
 #pragma unroll

@@ -81,6 +81,23 @@ bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *outM, uint32_t *out
     return false;
 }
 
+uint32_t assign_label_rows(Plan *pl, uint32_t gap_rows) {
+    uint32_t gap_used = 0, plain_used = 0;
+    for (uint32_t i = 0; i < pl->k; ++i) {
+        ModConst &mc = pl->mod[i];
+        if (gap_used + mc.W <= gap_rows) {
+            mc.lgap = 1;
+            mc.lrow = gap_used;
+            gap_used += mc.W;
+        } else {
+            mc.lgap = 0;
+            mc.lrow = plain_used;
+            plain_used += mc.W;
+        }
+    }
+    return plain_used;
+}
+
 uint32_t inverse_mod(uint32_t a, uint32_t m) {
     a %= m;
     for (uint32_t x = 1; x < m; ++x)
@@ -126,20 +143,32 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     division_constants(m, bound, &mc->divM, &mc->divS, &mc->div_fix);
 
     if (m == 2) return;  // labels over Z_2 are bit vectors; no fast path needed
+    mc->two_m = 2 * m;
     bool ok = mul24_constants(m, 3 * sq, &mc->red_M, &mc->red_s);
     uint64_t part = 1;
     for (int k = 0; k < 2; ++k) {
         const uint32_t nres = k ? mc->glast : mc->g;
         const uint32_t nlo = nres / 2, nhi = nres - nlo;
-        mc->nlo[k] = nlo;
-        mc->pw_lo[k] = ipow(m, nlo);
-        if (nlo) division_constants(mc->pw_lo[k], static_cast<uint64_t>(ipow(m, nres)), &mc->lo_M[k], &mc->lo_s[k],
-                                    &mc->lo_fix[k]);
+        uint32_t M = 0, sh = 0, fix = 0;
+        if (nlo) division_constants(ipow(m, nlo), static_cast<uint64_t>(ipow(m, nres)), &M, &sh, &fix);
+        ok = ok && fix == 0;  // the fast path has no fix-up step
+        if (k) {
+            mc->nlo_l = nlo;
+            mc->pw_lo_l = ipow(m, nlo);
+            mc->lo_M_l = M;
+            mc->lo_s_l = sh;
+        } else {
+            mc->nlo_f = nlo;
+            mc->pw_lo_f = ipow(m, nlo);
+            mc->lo_M_f = M;
+            mc->lo_s_f = sh;
+        }
         const uint64_t hi = ipow(m, nhi), lo = ipow(m, nlo);
         if (hi > part) part = hi;
         if (lo > part) part = lo;
     }
-    ok = ok && mul24_constants(m, part, &mc->sd_M, &mc->sd_s) && part < (1u << 24);
+    // (the split's parts also feed signed 24-bit multiply-adds: below 2^23)
+    ok = ok && mul24_constants(m, part, &mc->sd_M, &mc->sd_s) && part < (1u << 23);
     mc->fast = ok ? 1u : 0u;
 }
 

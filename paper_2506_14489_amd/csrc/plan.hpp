@@ -36,14 +36,24 @@ struct ModConst {
     // Evaluator fast path (fast == 1 when every bound below holds):
     //  * red: floor(x/m) = (x * red_M) >> red_s for every x < 3 m^2, with
     //    x * red_M < 2^32 (24-bit multiplies) -- one reduction per residue;
-    //  * sd: the same for every x below the larger part of a split word;
+    //  * sd: the same for every x below the larger part of a split word
+    //    (parts below 2^23);
     //  * a word's nres digits D (nres = g, or glast for the last word) are
-    //    split once as D = hi * m^nlo + lo, nlo = floor(nres/2), using the
-    //    32-bit division floor(D / m^nlo) described by lo_M/lo_s/lo_fix
-    //    (index 0: full word, 1: last word).
+    //    split once as D = hi * m^nlo + lo, nlo = floor(nres/2), using
+    //    floor(D / m^nlo) = umulhi(D, lo_M) >> lo_s (exact for every D below
+    //    m^nres; the fast path requires it without a fix-up step).  Suffix
+    //    _f: full words, _l: the last word.  (Separate fields, not arrays:
+    //    a selected array element would be indexed at run time.)
     uint32_t fast;
+    uint32_t two_m;  // 2m
     uint32_t red_M, red_s, sd_M, sd_s;
-    uint32_t nlo[2], pw_lo[2], lo_M[2], lo_s[2], lo_fix[2];
+    uint32_t nlo_f, pw_lo_f, lo_M_f, lo_s_f;
+    uint32_t nlo_l, pw_lo_l, lo_M_l, lo_s_l;
+    // Where the evaluator keeps this modulus's W working words in LDS (set
+    // for the block size of the launch): lgap = 1 puts them in the free
+    // halves of the table rows, starting at row lrow of that region;
+    // lgap = 0 in the plain region after it.
+    uint32_t lgap, lrow;
 };
 
 // Gate descriptor packed in one word:
@@ -93,5 +103,10 @@ void division_constants(uint32_t d, uint64_t x_bound, uint32_t *M, uint32_t *s, 
 bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *M, uint32_t *s);
 
 uint32_t inverse_mod(uint32_t a, uint32_t m);
+
+// Places every modulus's working words either wholly in the gap region
+// (gap_rows rows available) or in the plain region; returns the number of
+// plain-region rows used.
+uint32_t assign_label_rows(Plan *pl, uint32_t gap_rows);
 
 }  // namespace redash

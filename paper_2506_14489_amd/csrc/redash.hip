@@ -23,117 +23,174 @@ struct SeedKey {
 
 // ---------------------------------------------------------------------------
 // Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
+//
+// LDS of a block (addresses from 0: the kernel declares no static LDS): the
+// 64 KiB table region (256 rows of 256 bytes, TE0 copies in the lower half
+// of each row), 48 words of round keys, then the plain label region.  Each
+// thread keeps the W working words of every modulus either in the free
+// upper halves of the table rows (32 threads' words per half row) or in the
+// plain region, as assign_label_rows() decided for the block size.
 // ---------------------------------------------------------------------------
+constexpr uint32_t kKeyBytes = 48 * 4;
+constexpr uint32_t kRestBase = kTableRegionBytes + kKeyBytes;
 
-// Applies one gate's free operation to its destination label (packed words
-// at Ldst[w * stride]): E = row + pad, then L <- c (L - E) (sub: division
-// step and the recursion of Eq. rns_to_mrs) or L <- L + c E (acc: the
-// mixed-radix recombination onto a scaling modulus).
-__device__ __forceinline__ void eval_update(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
-                                            const uint32_t (&row)[kMaxW], uint32_t *Ldst, int stride) {
+template <int BLOCK>
+struct LabelRows {
+    static constexpr uint32_t kGapRows = (256u * 32u) / BLOCK;
+    uint32_t gap_off, rest_off;  // this thread's byte offsets in the two regions
+    // byte address of word 0 of a modulus's label, and the step to word w+1
+    __device__ __forceinline__ uint32_t base(const ModConst &mc) const {
+        return mc.lgap ? mc.lrow * (BLOCK * 8u) + gap_off : mc.lrow * (BLOCK * 4u) + rest_off;
+    }
+    __device__ __forceinline__ static uint32_t step(const ModConst &mc) { return mc.lgap ? BLOCK * 8u : BLOCK * 4u; }
+    __device__ __forceinline__ static uint32_t get(uint32_t addr) {
+        return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
+    }
+    __device__ __forceinline__ static void put(uint32_t addr, uint32_t v) {
+        *reinterpret_cast<lds_u32_rw *>(static_cast<uintptr_t>(addr)) = v;
+    }
+    __device__ __forceinline__ uint32_t word(const ModConst &mc, uint32_t w) const { return get(base(mc) + w * step(mc)); }
+    __device__ __forceinline__ void set(const ModConst &mc, uint32_t w, uint32_t v) const {
+        put(base(mc) + w * step(mc), v);
+    }
+};
+
+template <int BLOCK>
+__device__ __forceinline__ LabelRows<BLOCK> label_rows(uint32_t tid) {
+    return LabelRows<BLOCK>{(tid >> 5) * 256u + 128u + (tid & 31u) * 4u, kRestBase + tid * 4u};
+}
+
+// Moduli without the fast constants (41..61 and the largest ones): one
+// residue at a time with 32-bit divisions, in rolled loops; the gadget
+// configurations in use all take the fast path.
+template <int BLOCK>
+__device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
+                                                    uint32_t (&row)[kMaxW], const LabelRows<BLOCK> &LR) {
     const uint32_t coeff = gate_coeff(d);
-    if (mm.m == 2) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const uint32_t E = bits_word(V, w) ^ row[w];
-            uint32_t l = Ldst[w * stride];
-            if (gate_kind(d) == 0 || (coeff & 1u)) l ^= E;  // sub: q^{-1} = 1 mod 2
-            Ldst[w * stride] = l;
-        }
-    } else if (mm.fast) {
-#pragma unroll
-        for (int w = 0; w < kMaxW; ++w) {
-            if (w < static_cast<int>(mm.W)) {
-                const uint32_t last = (w + 1 == static_cast<int>(mm.W)) ? 1u : 0u;
-                const uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
-                const uint32_t l = Ldst[w * stride];
-                Ldst[w * stride] = gate_kind(d) == 0 ? fast_word<false>(D, last, row[w], l, coeff, mm)
-                                                     : fast_word<true>(D, last, row[w], l, coeff, mm);
+    uint32_t addr = LR.base(mm);
+    for (uint32_t w = 0; w < mm.W; ++w, addr += LR.step(mm)) {
+        const bool last = (w + 1 == mm.W);
+        const uint32_t nres = last ? mm.glast : mm.g;
+        uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
+        const uint32_t rw = next_word(row);
+        const uint32_t l = LR.get(addr);
+        uint32_t res = 0;
+        // Digits come out least significant first: position nres-1 down to 0.
+        for (uint32_t j = nres; j-- > 0;) {
+            uint32_t pd;
+            if (j) {
+                const uint32_t qd = div_m(D, mm);
+                pd = D - qd * mm.m;
+                D = qd;
+            } else {
+                pd = D;
             }
+            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
+            const uint32_t lj = field(l, j, mm);
+            const uint32_t r = gate_kind(d) == 0 ? mul_mod(coeff, sub_mod(lj, e, mm.m), mm)
+                                                 : add_mod(lj, mul_mod(coeff, e, mm), mm.m);
+            res |= r << (mm.b * j);
         }
-    } else {
-#pragma unroll
-        for (int w = 0; w < kMaxW; ++w) {
-            if (w < static_cast<int>(mm.W)) {
-                const bool last = (w + 1 == static_cast<int>(mm.W));
-                const uint32_t nres = last ? mm.glast : mm.g;
-                uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
-                const uint32_t rw = row[w];
-                const uint32_t l = Ldst[w * stride];
-                uint32_t res = 0;
-                // Digits come out least significant first: position nres-1 down to 0.
-                for (uint32_t j = nres; j-- > 0;) {
-                    uint32_t pd;
-                    if (j) {
-                        const uint32_t qd = div_m(D, mm);
-                        pd = D - qd * mm.m;
-                        D = qd;
-                    } else {
-                        pd = D;
-                    }
-                    const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
-                    const uint32_t lj = field(l, j, mm);
-                    const uint32_t r = gate_kind(d) == 0 ? mul_mod(coeff, sub_mod(lj, e, mm.m), mm)
-                                                         : add_mod(lj, mul_mod(coeff, e, mm), mm.m);
-                    res |= r << (mm.b * j);
-                }
-                Ldst[w * stride] = res;
-            }
-        }
+        LR.put(addr, res);
     }
 }
 
-// Evaluates the NG gates g..g+NG-1, which share one digit label: the rows of
-// all of them are requested first (the colour is known before hashing), the
-// 2 NG AES blocks run interleaved, then each destination is updated.
+// Applies one gate's free operation to its destination label: E = row + pad,
+// then L <- c (L - E) (sub: division step and the recursion of
+// Eq. rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination onto a
+// scaling modulus).
+template <int BLOCK>
+__device__ __forceinline__ void eval_update(uint32_t d, const ModConst &mm, uint32_t (&V)[8], uint32_t (&row)[kMaxW],
+                                            const LabelRows<BLOCK> &LR) {
+    const uint32_t coeff = gate_coeff(d);
+    if (mm.m == 2) {
+        const uint32_t base = LR.base(mm), step = LR.step(mm);
+        uint32_t l[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) l[w] = LR.get(base + w * step);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t E = bits_word(V, w) ^ row[w];
+            if (gate_kind(d) == 0 || (coeff & 1u)) l[w] ^= E;  // sub: q^{-1} = 1 mod 2
+            LR.put(base + w * step, l[w]);
+        }
+    } else if (mm.fast) {
+        // full words in a loop, the last word peeled: each with its own
+        // constants, so no per-word selection
+        const uint32_t step = LR.step(mm), base = LR.base(mm);
+        const bool acc = gate_kind(d) != 0;
+#pragma unroll 1
+        for (uint32_t w = 0; w + 1 < mm.W; ++w) {
+            const uint32_t addr = base + w * step;
+            const uint32_t l = LR.get(addr);
+            const uint32_t D = frac_mul_carry(V, mm.pw_g);
+            const uint32_t rw = next_word(row);
+            LR.put(addr, acc ? fast_word_any<true>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm)
+                             : fast_word_any<false>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm));
+        }
+        const uint32_t addr = base + (mm.W - 1) * step;
+        const uint32_t l = LR.get(addr);
+        const uint32_t D = frac_mul_carry(V, mm.pw_last);
+        const uint32_t rw = row[0];
+        LR.put(addr, acc ? fast_word_any<true>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm)
+                         : fast_word_any<false>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm));
+    } else {
+        eval_update_generic<BLOCK>(d, mm, V, row, LR);
+    }
+}
+
+// Hashes the NG gates g..g+NG-1, which share one digit label: the rows of
+// all of them are requested first (the colour is known before hashing), then
+// the 2 NG AES blocks run interleaved.  Fills V[0..NG-1] and row[0..NG-1].
 template <int NG, int BLOCK>
-__device__ __forceinline__ void eval_chunk(const Plan &P, uint32_t g, uint64_t &toff, const uint32_t *TT, uint32_t *L,
-                                           int tid, uint64_t a, uint64_t tau0, const uint32_t *__restrict__ tab) {
+__device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &toff, const PermTE0 &TT,
+                                           const uint32_t *K, const LabelRows<BLOCK> &LR, uint64_t a, uint64_t tau0,
+                                           const uint32_t *__restrict__ tab, uint32_t (&V)[kMaxChunk][8],
+                                           uint32_t (&row)[kMaxChunk][kMaxW]) {
     const uint64_t n = P.n;
-    uint32_t dd[NG];
-    ModConst mm[NG];
-    static_for<NG>([&](auto j) {
-        dd[j] = P.gate[g + j];
-        mm[j] = P.mod[gate_dst(dd[j])];
-    });
-    const ModConst mq = P.mod[gate_src(dd[0])];
+    // Local copies of the modulus constants: the compiler keeps their fields
+    // in scalar registers (a pointer into the argument block could end up in
+    // vector registers and make every loop bound derived from it divergent).
+    uint32_t Wd[NG];
+    static_for<NG>([&](auto j) { Wd[j] = P.mod[gate_dst(P.gate[g + j])].W; });
+    const ModConst mq = P.mod[gate_src(P.gate[g])];
     const uint32_t q = mq.m;
-    const uint32_t *Lsrc = L + mq.woff * BLOCK + tid;
-    const uint32_t w0 = Lsrc[0];
+    const uint32_t w0 = LR.word(mq, 0);
     // A residue >= q only occurs in a malformed input label; it selects the
     // implicit zero row, the output is garbage and decode flags it.
     uint32_t colour = w0 & mq.mask;
     if (colour >= q) colour = 0;
-    uint32_t row[NG][kMaxW];
     static_for<NG>([&](auto j) {
         static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
         if (colour != 0) {
-            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * mm[j].W;
+            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * Wd[j];
             static_for<kMaxW>([&](auto w) {
-                if (w < static_cast<int>(mm[j].W)) row[j][w] = rp[w];
+                if (w < static_cast<int>(Wd[j])) row[j][w] = rp[w];
             });
         }
-        toff += n * (q - 1) * mm[j].W;
+        toff += n * (q - 1) * Wd[j];
     });
     uint32_t x[4] = {w0, 0, 0, 0};
     static_for<kMaxW - 1>([&](auto w1) {
         constexpr int w = decltype(w1)::value + 1;
-        if (w < static_cast<int>(mq.W)) x[w & 3] ^= Lsrc[w * BLOCK];
+        if (w < static_cast<int>(mq.W)) x[w & 3] ^= LR.word(mq, w);
     });
-    uint32_t V[NG][8];
-    hash_fraction_n<NG>(TT, x[0], x[1], x[2], x[3], tau0 + g, P.gid, V);
-    static_for<NG>([&](auto j) { eval_update(dd[j], mm[j], V[j], row[j], L + mm[j].woff * BLOCK + tid, BLOCK); });
+    uint32_t Vn[NG][8];
+    hash_fraction_n<NG>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g, P.gid, Vn);
+    static_for<NG>([&](auto j) { static_for<8>([&](auto l) { V[j][l] = Vn[j][l]; }); });
 }
 
 template <int BLOCK>
 __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__restrict__ in,
                                                 const uint32_t *__restrict__ tab, uint32_t *__restrict__ out) {
     extern __shared__ uint32_t lds[];
-    uint32_t *TT = lds;
-    uint32_t *L = lds + kTableWords;
+    uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    stage_round_tables(TT, tid, BLOCK);
+    stage_perm_te0(lds, tid, BLOCK);
+    stage_hash_key(K, tid, BLOCK);
     __syncthreads();
+    const PermTE0 TT = perm_te0();
+    const LabelRows<BLOCK> LR = label_rows<BLOCK>(tid);
     const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
     if (a >= P.n) return;  // no barrier follows
     const uint64_t n = P.n;
@@ -141,7 +198,7 @@ __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__
     for (uint32_t i = 0; i < P.k; ++i) {
         const ModConst &mc = P.mod[i];
         const uint32_t *src = in + static_cast<uint64_t>(mc.woff) * n + a;
-        for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = src[static_cast<uint64_t>(w) * n];
+        for (uint32_t w = 0; w < mc.W; ++w) LR.set(mc, w, src[static_cast<uint64_t>(w) * n]);
     }
 
     const uint64_t tau0 = (P.a0 + a) * P.G;
@@ -157,29 +214,40 @@ __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__
             for (uint32_t b = 0; b < P.u; ++b) {
                 const ModConst &mc = P.mod[P.R[b]];
                 uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
-                for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = L[(mc.woff + w) * BLOCK + tid];
+                for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = LR.word(mc, w);
             }
             for (uint32_t s = 0; s < P.t; ++s) {
                 const ModConst &mc = P.mod[P.S[s]];
-                for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = 0;
+                for (uint32_t w = 0; w < mc.W; ++w) LR.set(mc, w, 0);
             }
         }
         const uint32_t len = gate_chunk(d);
+        uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW];
         if (len == 4) {
-            eval_chunk<4, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
-            g += 4;
+            hash_chunk<4, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
         } else if (len == 2) {
-            eval_chunk<2, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
-            g += 2;
+            hash_chunk<2, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
         } else {
-            eval_chunk<1, BLOCK>(P, g, toff, TT, L, tid, a, tau0, tab);
-            g += 1;
+            hash_chunk<1, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
         }
+        // One copy of the update code for every chunk size: the chunk's
+        // gates go through a queue (entry 0 is processed, the rest move down).
+#pragma unroll 1
+        for (uint32_t j = 0; j < len; ++j) {
+            const uint32_t dj = P.gate[g + j];
+            const ModConst mm = P.mod[gate_dst(dj)];
+            eval_update<BLOCK>(dj, mm, V[0], row[0], LR);
+            static_for<kMaxChunk - 1>([&](auto k) {
+                static_for<8>([&](auto l) { V[k][l] = V[k + 1][l]; });
+                static_for<kMaxW>([&](auto w) { row[k][w] = row[k + 1][w]; });
+            });
+        }
+        g += len;
     }
     for (uint32_t s = 0; s < P.t; ++s) {
         const ModConst &mc = P.mod[P.S[s]];
         uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
-        for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = L[(mc.woff + w) * BLOCK + tid];
+        for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = LR.word(mc, w);
     }
 }
 
@@ -467,9 +535,6 @@ __global__ void __launch_bounds__(BLOCK) k_hash(const ModConst mq, const ModCons
 // ---------------------------------------------------------------------------
 namespace {
 
-size_t eval_lds_bytes(const Plan &P, int block) {
-    return (static_cast<size_t>(kTableWords) + static_cast<size_t>(P.total_words) * block) * 4;
-}
 size_t garble_lds_bytes(const Plan &P, int block) {
     return (static_cast<size_t>(kTableWords) + P.total_words + static_cast<size_t>(P.total_words) * block) * 4;
 }
@@ -501,10 +566,13 @@ int launched() {
 // Launches k_eval with the largest block (256, 128 or 64 threads) whose LDS
 // footprint fits the device.
 template <int BLOCK>
-int try_eval(const Plan &P, size_t max_lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
+int try_eval(const Plan &P0, size_t max_lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
              hipStream_t stream, bool *done) {
-    const size_t lds = eval_lds_bytes(P, BLOCK);
-    if (*done || lds > max_lds) return REDASH_OK;
+    if (*done) return REDASH_OK;
+    Plan P = P0;
+    const uint32_t plain_rows = assign_label_rows(&P, LabelRows<BLOCK>::kGapRows);
+    const size_t lds = kRestBase + static_cast<size_t>(plain_rows) * BLOCK * 4;
+    if (lds > max_lds) return REDASH_OK;
     *done = true;
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<BLOCK>), lds);
     if (rc) return rc;
@@ -600,6 +668,7 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     size_t max_lds = 0;
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     bool done = false;
+    if ((rc = try_eval<512>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
     if ((rc = try_eval<256>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
     if ((rc = try_eval<128>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
     if ((rc = try_eval<64>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
