@@ -96,6 +96,7 @@ def main():
 
     from paper_2506_14489_amd import binding as B
     from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import traffic
     from paper_2506_14489_amd import workloads as WL
 
     w = WL.by_name(args.workload)
@@ -151,6 +152,8 @@ def main():
     aes_g = cost.aes_blocks_per_gadget(w.moduli, w.scale_idx)
     achieved_tops = ops_g * n / (ms_step / 1e3) / 1e12
     achieved_gbs = bytes_g * n / (ms_step / 1e3) / 1e9
+    # HBM bytes per launch from the rocprofv3 counters (None once the kernel changed)
+    traffic_b = traffic.traffic_bytes(w.name)
     result = {
         "metric": METRIC,
         "value": round(gadgets_per_s, 1),
@@ -178,7 +181,8 @@ def main():
             "peak": round(ALU_PEAK_TOPS, 2),
             "unit": "TOP/s",
             "frac": round(achieved_tops / ALU_PEAK_TOPS, 4),
-            "traffic": None,
+            "traffic": traffic_b,
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
             "kernel": "k_eval",
             "ops_per_gadget": ops_g,
         },
@@ -188,6 +192,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
             "bytes_per_gadget": round(bytes_g, 1),
+            "measured_bytes_per_gadget": None if traffic_b is None else round(traffic_b / n, 1),
         },
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
         "check": check,

@@ -563,7 +563,7 @@ int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
 
-// Launches k_eval with the largest block (256, 128 or 64 threads) whose LDS
+// Launches k_eval with the largest block (512, 256, 128 or 64 threads) whose LDS
 // footprint fits the device.
 template <int BLOCK>
 int try_eval(const Plan &P0, size_t max_lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,

@@ -1,0 +1,53 @@
+"""Measured HBM traffic of the evaluation kernel, from hardware counters.
+
+The figures were taken with two rocprofv3 counter passes over
+``bench.py`` (``--pmc FETCH_SIZE``, then ``--pmc WRITE_SIZE``; KiB per
+dispatch) and scaled by what the same counters read for a plain
+device-to-device copy of known size (``bench.py --copy-calibration 1024``:
+a 1 GiB copy reads FETCH_SIZE = 524,300 KiB and WRITE_SIZE = 1,048,576 KiB,
+so FETCH_SIZE is scaled by 2 and WRITE_SIZE by 1).
+
+A figure is only valid for the kernel it was taken on: ``traffic_bytes``
+returns None as soon as any source file of the library differs from the one
+the counters were read on (a SHA-256 over the sources, in a fixed order).
+"""
+
+from __future__ import annotations
+
+import hashlib
+import os
+
+from . import build as _build
+
+# 1 GiB device-to-device copy: counter reading -> bytes moved
+FETCH_FACTOR = 1048576 / 524300
+WRITE_FACTOR = 1048576 / 1048576
+
+# workload name -> counters per k_eval dispatch (KiB) and the source hash
+MEASURED = {
+    "batched": {
+        "kernel": "k_eval",
+        "fetch_kib": 11810928.5,  # mean of two dispatches: 11,811,062 and 11,810,795
+        "write_kib": 790272.0,
+        "sources_sha256": "4acf219d57950bf14796bbd02330e74a17980c793ea965ce0cb9fee36b3b0f1b",
+    },
+}
+
+
+def sources_sha256() -> str:
+    """SHA-256 over the library's source files (name and contents)."""
+    h = hashlib.sha256()
+    for path in sorted(_build.SOURCES + _build.HEADERS, key=os.path.basename):
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_bytes(workload: str):
+    """HBM bytes (reads + writes) per k_eval launch on ``workload``, or None
+    if no counters were taken on it or the kernel sources changed since."""
+    rec = MEASURED.get(workload)
+    if rec is None or rec["sources_sha256"] != sources_sha256():
+        return None
+    return (rec["fetch_kib"] * FETCH_FACTOR + rec["write_kib"] * WRITE_FACTOR) * 1024.0
