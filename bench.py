@@ -120,14 +120,14 @@ def main():
         f"({buf.sizes['table_words'] * 4 / 1e9:.1f} GB of tables)")
 
     for _ in range(args.warmup):
-        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, stream)
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
-        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, stream)
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0

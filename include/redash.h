@@ -110,6 +110,7 @@ typedef struct {
     uint64_t table_words;  /* all garbled tables of the n gadgets            */
     uint32_t offset_words; /* the k offsets R_m                              */
     uint32_t gates;        /* projection gates per gadget                    */
+    uint64_t work_words;   /* evaluator working storage (redash_eval_scale)  */
 } redash_sizes;
 
 /*
@@ -156,11 +157,18 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
  * digits).
  *   d_in_labels  label_words (read only).
  *   d_tables     table_words from redash_garble_scale with the same params.
- *   d_out_labels label_words, written; may not alias d_in_labels.
+ *   d_out_labels label_words, written; also holds intermediate labels while
+ *                the call runs.  May not alias d_in_labels or d_work.
+ *   d_work       work_words of working storage: the Phase-B copies of the
+ *                remaining moduli (Sec. 3.3 consumes them while the Phase-A
+ *                values are outputs).  Contents on entry are ignored and on
+ *                return unspecified; may be NULL when work_words is 0.
  * Output labels carry floor(x/s) under the garbler's output zero-labels.
+ * REDASH_E_PARAM also when n >= 2^30 (a gadget's byte offset must fit in
+ * 32 bits).
  */
 int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
-                      uint32_t *d_out_labels, hipStream_t stream);
+                      uint32_t *d_out_labels, uint32_t *d_work, hipStream_t stream);
 
 /*
  * Garbler decodes the returned labels (Sec. 2.1): v_i = (Y_i[0] - O_i[0]) *

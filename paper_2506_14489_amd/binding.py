@@ -54,6 +54,7 @@ class Sizes(ctypes.Structure):
         ("table_words", ctypes.c_uint64),
         ("offset_words", ctypes.c_uint32),
         ("gates", ctypes.c_uint32),
+        ("work_words", ctypes.c_uint64),
     ]
 
 
@@ -88,7 +89,7 @@ def lib() -> ctypes.CDLL:
         L.redash_plan.argtypes = [pp, ctypes.POINTER(Sizes)]
         L.redash_garble_scale.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_encode.argtypes = [pp, vp, vp, vp, vp, vp]
-        L.redash_eval_scale.argtypes = [pp, vp, vp, vp, vp]
+        L.redash_eval_scale.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_decode.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_hash_labels.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, vp, ctypes.c_uint32,
                                          vp, vp, vp]
@@ -146,7 +147,7 @@ def redash_plan(params: Params) -> dict:
     s = Sizes()
     _check(lib().redash_plan(ctypes.byref(params), ctypes.byref(s)), "redash_plan")
     return {"label_words": s.label_words, "table_words": s.table_words, "offset_words": s.offset_words,
-            "gates": s.gates}
+            "gates": s.gates, "work_words": s.work_words}
 
 
 def plan_rc(params: Params) -> int:
@@ -177,14 +178,15 @@ def redash_encode(params, x, in_zero, offsets, in_labels, stream=None):
         _ptr(in_labels, torch.int32, sz["label_words"], "in_labels"), _stream(stream)), "redash_encode")
 
 
-def redash_eval_scale(params, in_labels, tables, out_labels, stream=None):
+def redash_eval_scale(params, in_labels, tables, out_labels, work, stream=None):
     import torch
 
     sz = redash_plan(params)
     _check(lib().redash_eval_scale(
         ctypes.byref(params), _ptr(in_labels, torch.int32, sz["label_words"], "in_labels"),
         _ptr(tables, torch.int32, sz["table_words"], "tables"),
-        _ptr(out_labels, torch.int32, sz["label_words"], "out_labels"), _stream(stream)), "redash_eval_scale")
+        _ptr(out_labels, torch.int32, sz["label_words"], "out_labels"),
+        _ptr(work, torch.int32, sz["work_words"], "work"), _stream(stream)), "redash_eval_scale")
 
 
 def redash_decode(params, out_labels, out_zero, offsets, y, bad_count, stream=None):
@@ -231,5 +233,6 @@ class Buffers:
         self.in_labels = torch.empty(sz["label_words"], dtype=i32, device=device)
         self.out_labels = torch.empty(sz["label_words"], dtype=i32, device=device)
         self.tables = torch.empty(max(sz["table_words"], 1), dtype=i32, device=device) if tables else None
+        self.work = torch.empty(max(sz["work_words"], 1), dtype=i32, device=device)
         self.y = torch.empty(max(params.n, 1), dtype=torch.int64, device=device)
         self.bad = torch.zeros(1, dtype=torch.int64, device=device)

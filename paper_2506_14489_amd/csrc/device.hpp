@@ -74,9 +74,14 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
     return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);  // truth table of a ^ b ^ c
 }
 
-// Round-table access policies.  te(t, w, k) = TEt[byte k of w] and
-// sb4(w0, w1, w2, w3) = the column (S(byte 0 of w0), S(byte 1 of w1),
-// S(byte 2 of w2), S(byte 3 of w3)) of the last round.
+__device__ __forceinline__ uint32_t rotl8(uint32_t x) { return __builtin_amdgcn_alignbit(x, x, 24); }
+
+// Round-table access policies.  column(w0, w1, w2, w3, K, i) is one column
+// of a middle round, TE0[byte 0 of w0] ^ TE1[byte 1 of w1] ^ TE2[byte 2 of
+// w2] ^ TE3[byte 3 of w3] ^ K(i); last_column(...) is the last round's
+// column (S(byte 0 of w0), S(byte 1 of w1), S(byte 2 of w2), S(byte 3 of
+// w3)) ^ K(i).  TEt[x] = rotl(TE0[x], 8t), TE0[x] = (2S(x), S(x), S(x), 3S(x))
+// as bytes 0..3.
 //
 // FourTables: TE0..TE3 back to back (1024 words); each S-box byte is taken
 // from the table in which it already sits at the right byte position.
@@ -85,19 +90,29 @@ struct FourTables {
     __device__ __forceinline__ uint32_t te(int t, uint32_t w, int k) const {
         return T[256 * t + ((w >> (8 * k)) & 255u)];
     }
-    __device__ __forceinline__ uint32_t sb4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) const {
+    template <typename Key>
+    __device__ __forceinline__ uint32_t column(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, const Key &K,
+                                               int i) const {
+        return xor3(xor3(te(0, w0, 0), te(1, w1, 1), te(2, w2, 2)), te(3, w3, 3), K(i));
+    }
+    template <typename Key>
+    __device__ __forceinline__ uint32_t last_column(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, const Key &K,
+                                                    int i) const {
         // S(x) is byte 0 of TE2, byte 1 of TE3, byte 2 of TE0, byte 3 of TE1
-        return (T[512 + (w0 & 255u)] & 0xffu) | (T[768 + ((w1 >> 8) & 255u)] & 0xff00u) |
-               (T[(w2 >> 16) & 255u] & 0xff0000u) | (T[256 + (w3 >> 24)] & 0xff000000u);
+        return ((T[512 + (w0 & 255u)] & 0xffu) | (T[768 + ((w1 >> 8) & 255u)] & 0xff00u) |
+                (T[(w2 >> 16) & 255u] & 0xff0000u) | (T[256 + (w3 >> 24)] & 0xff000000u)) ^
+               K(i);
     }
 };
 
-// PermTE0: TE0 in 32 copies; entry x is the 256-byte LDS row x, copy c at
-// byte 4c of the row (the upper 128 bytes of every row are free for other
-// data).  Lane l reads copy l mod 32, which sits in bank l mod 32, so a
-// wavefront's lookups never conflict, and one v_perm_b32 builds the address
-// 256 x + 4 (l mod 32) straight from the state word.  TE1..3 are byte
-// rotations of TE0.
+// PermTE02: TE0 and TE2 in 32 copies each, in 256 LDS rows of 256 bytes: row
+// x holds TE0[x] in its lower 128 bytes and TE2[x] in its upper 128 bytes,
+// copy c at byte 4c of each half.  Lane l reads copy l mod 32, which sits in
+// bank l mod 32: a wavefront's lookups never conflict, whatever the indices.
+// One v_perm_b32 builds the address 256 x + 4 (l mod 32) (+ 128 for TE2)
+// straight from the state word.  Since TE1 = rotl8 TE0 and TE3 = rotl8 TE2,
+// a column is TE0[a] ^ TE2[c] ^ rotl8(TE0[b] ^ TE2[d] ^ rotr8(k)): two
+// three-input XORs and one rotation.
 constexpr int kReplicas = 32;
 constexpr uint32_t kTableRowBytes = 256;
 constexpr uint32_t kTableRegionBytes = 256 * kTableRowBytes;  // 64 KiB
@@ -108,40 +123,52 @@ constexpr uint32_t kTableRegionBytes = 256 * kTableRowBytes;  // 64 KiB
 typedef __attribute__((address_space(3))) const uint32_t lds_u32;
 typedef __attribute__((address_space(3))) uint32_t lds_u32_rw;
 
-struct PermTE0 {
-    uint32_t lane_off;  // 4 (lane mod 32), below 128
-    __device__ __forceinline__ uint32_t te0(uint32_t w, int k) const {
-        // address bytes: [lane_off, byte k of w, 0, 0]
-        const uint32_t addr = __builtin_amdgcn_perm(w, lane_off, 0x0c0c0000u | ((4u + k) << 8));
-        return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
+__device__ __forceinline__ uint32_t lds_read(uint32_t addr) {
+    return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
+}
+
+struct PermTE02 {
+    uint32_t off0, off2;  // 4 (lane mod 32), and that + 128
+    // address bytes: [offset, byte k of w, 0, 0]
+    __device__ __forceinline__ static uint32_t at(uint32_t w, uint32_t off, int k) {
+        return lds_read(__builtin_amdgcn_perm(w, off, 0x0c0c0000u | ((4u + k) << 8)));
     }
-    __device__ __forceinline__ uint32_t te(int t, uint32_t w, int k) const {
-        const uint32_t v = te0(w, k);
-        return t == 0 ? v : __builtin_amdgcn_alignbit(v, v, 32 - 8 * t);  // rotate left by 8t
+    template <typename Key>
+    __device__ __forceinline__ uint32_t column(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, const Key &K,
+                                               int i) const {
+        return xor3(at(w0, off0, 0), at(w2, off2, 2), rotl8(xor3(at(w1, off0, 1), at(w3, off2, 3), K.rot(i))));
     }
-    __device__ __forceinline__ uint32_t sb4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) const {
-        // TE0[x] holds S(x) in byte 1: gather byte 1 of the four entries
-        const uint32_t lo = __builtin_amdgcn_perm(te0(w1, 1), te0(w0, 0), 0x0c0c0501u);
-        const uint32_t hi = __builtin_amdgcn_perm(te0(w3, 3), te0(w2, 2), 0x05010c0cu);
-        return lo | hi;
+    template <typename Key>
+    __device__ __forceinline__ uint32_t last_column(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, const Key &K,
+                                                    int i) const {
+        // S(x) is byte 1 and byte 2 of TE0[x], byte 0 and byte 3 of TE2[x]
+        const uint32_t lo = __builtin_amdgcn_perm(at(w1, off0, 1), at(w0, off2, 0), 0x0c0c0500u);
+        const uint32_t hi = __builtin_amdgcn_perm(at(w3, off2, 3), at(w2, off0, 2), 0x07020c0cu);
+        return xor3(lo, hi, K(i));
     }
 };
 
-__device__ __forceinline__ void stage_perm_te0(uint32_t *lds, int tid, int nthreads) {
-    // the lower 32 words of each 64-word row: TE0[row] in every copy
-    for (int i = tid; i < 256 * kReplicas; i += nthreads) lds[(i / kReplicas) * 64 + (i % kReplicas)] = g_round_tables.v[i / kReplicas];
+__device__ __forceinline__ void stage_perm_te02(uint32_t *lds, int tid, int nthreads) {
+    // word 64 x + c: TE0[x] for c < 32, TE2[x] for 32 <= c < 64
+    for (int i = tid; i < 256 * 2 * kReplicas; i += nthreads) {
+        const int x = i >> 6, half = (i >> 5) & 1;
+        lds[i] = g_round_tables.v[512 * half + x];
+    }
 }
 
-__device__ __forceinline__ PermTE0 perm_te0() { return PermTE0{4u * (threadIdx.x % kReplicas)}; }
+__device__ __forceinline__ PermTE02 perm_te02() {
+    const uint32_t off = 4u * (threadIdx.x % kReplicas);
+    return PermTE02{off, off + 128u};
+}
 
 // NB independent blocks encrypted round by round, so that the table reads of
 // all blocks are in flight together.
-template <int NB, typename Tab, typename KeyFn>
-__device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB][4], KeyFn rk) {
+template <int NB, typename Tab, typename Key>
+__device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB][4], const Key &K) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) s[b][c] ^= rk(c);
+        for (int c = 0; c < 4; ++c) s[b][c] ^= K(c);
     // Rounds 1..9 stay a loop (the round keys are uniform loads): the
     // instruction cache holds the whole gate loop that way.
 #pragma unroll 1
@@ -149,30 +176,26 @@ __device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB]
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-            const uint32_t t0 = xor3(T.te(0, s0, 0), T.te(1, s1, 1), T.te(2, s2, 2));
-            const uint32_t t1 = xor3(T.te(0, s1, 0), T.te(1, s2, 1), T.te(2, s3, 2));
-            const uint32_t t2 = xor3(T.te(0, s2, 0), T.te(1, s3, 1), T.te(2, s0, 2));
-            const uint32_t t3 = xor3(T.te(0, s3, 0), T.te(1, s0, 1), T.te(2, s1, 2));
-            s[b][0] = xor3(t0, T.te(3, s3, 3), rk(4 * r));
-            s[b][1] = xor3(t1, T.te(3, s0, 3), rk(4 * r + 1));
-            s[b][2] = xor3(t2, T.te(3, s1, 3), rk(4 * r + 2));
-            s[b][3] = xor3(t3, T.te(3, s2, 3), rk(4 * r + 3));
+            s[b][0] = T.column(s0, s1, s2, s3, K, 4 * r);
+            s[b][1] = T.column(s1, s2, s3, s0, K, 4 * r + 1);
+            s[b][2] = T.column(s2, s3, s0, s1, K, 4 * r + 2);
+            s[b][3] = T.column(s3, s0, s1, s2, K, 4 * r + 3);
         }
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-        s[b][0] = T.sb4(s0, s1, s2, s3) ^ rk(40);
-        s[b][1] = T.sb4(s1, s2, s3, s0) ^ rk(41);
-        s[b][2] = T.sb4(s2, s3, s0, s1) ^ rk(42);
-        s[b][3] = T.sb4(s3, s0, s1, s2) ^ rk(43);
+        s[b][0] = T.last_column(s0, s1, s2, s3, K, 40);
+        s[b][1] = T.last_column(s1, s2, s3, s0, K, 41);
+        s[b][2] = T.last_column(s2, s3, s0, s1, K, 42);
+        s[b][3] = T.last_column(s3, s0, s1, s2, K, 43);
     }
 }
 
 // One block held as four little-endian column words, on the four tables.
-template <typename KeyFn>
+template <typename Key>
 __device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, uint32_t &s0, uint32_t &s1,
-                                               uint32_t &s2, uint32_t &s3, KeyFn rk) {
+                                               uint32_t &s2, uint32_t &s3, const Key &rk) {
     uint32_t s[1][4] = {{s0, s1, s2, s3}};
     aes128_encrypt_n<1>(FourTables{T}, s, rk);
     s0 = s[0][0];
@@ -183,25 +206,37 @@ __device__ __forceinline__ void aes128_encrypt(const uint32_t *__restrict__ T, u
 
 __constant__ RoundKeys c_hash_key = kHashKey;
 
+// Key policies: K(i) is round-key word i, K.rot(i) the same word rotated
+// right by 8 bits (the form the two-table column takes).
+__device__ __forceinline__ uint32_t rotr8(uint32_t x) { return __builtin_amdgcn_alignbit(x, x, 8); }
+
 struct HashKey {
     __device__ __forceinline__ uint32_t operator()(int i) const { return c_hash_key.w[i]; }
+    __device__ __forceinline__ uint32_t rot(int i) const { return rotr8(c_hash_key.w[i]); }
 };
 
 // Round keys held in LDS (every lane reads the same word, a broadcast):
 // unlike scalar loads, LDS reads complete in order with the table reads, so
-// the wait counters never have to drain inside the round loop.
+// the wait counters never have to drain inside the round loop.  The 44 words
+// are followed by their rotated forms.
+constexpr int kLdsKeyWords = 88;
 struct LdsKey {
     const uint32_t *w;
     __device__ __forceinline__ uint32_t operator()(int i) const { return w[i]; }
+    __device__ __forceinline__ uint32_t rot(int i) const { return w[44 + i]; }
 };
 
 __device__ __forceinline__ void stage_hash_key(uint32_t *lds, int tid, int nthreads) {
-    for (int i = tid; i < 44; i += nthreads) lds[i] = c_hash_key.w[i];
+    for (int i = tid; i < 44; i += nthreads) {
+        lds[i] = c_hash_key.w[i];
+        lds[44 + i] = rotr8(c_hash_key.w[i]);
+    }
 }
 
 struct ArgKey {
     const uint32_t *w;
     __device__ __forceinline__ uint32_t operator()(int i) const { return w[i]; }
+    __device__ __forceinline__ uint32_t rot(int i) const { return rotr8(w[i]); }
 };
 
 // ---------------------------------------------------------------------------
@@ -492,8 +527,8 @@ __device__ __forceinline__ void hash_fraction(const uint32_t *T, uint32_t x0, ui
 // The hash fractions of NG gates that share one input label (folded into
 // x0..x3): gate j uses tweak tau + j and two blocks (a gate whose output
 // modulus is 2 only reads V[j][0..3]).
-template <int NG, typename Tab, typename KeyFn>
-__device__ __forceinline__ void hash_fraction_n(const Tab &T, KeyFn rk, uint32_t x0, uint32_t x1, uint32_t x2,
+template <int NG, typename Tab, typename Key>
+__device__ __forceinline__ void hash_fraction_n(const Tab &T, const Key &rk, uint32_t x0, uint32_t x1, uint32_t x2,
                                                 uint32_t x3, uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
     const uint32_t u0 = x2, u1 = x3, u2 = x2 ^ x0, u3 = x3 ^ x1;
     uint32_t s[2 * NG][4];

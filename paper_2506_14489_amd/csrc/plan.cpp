@@ -81,23 +81,6 @@ bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *outM, uint32_t *out
     return false;
 }
 
-uint32_t assign_label_rows(Plan *pl, uint32_t gap_rows) {
-    uint32_t gap_used = 0, plain_used = 0;
-    for (uint32_t i = 0; i < pl->k; ++i) {
-        ModConst &mc = pl->mod[i];
-        if (gap_used + mc.W <= gap_rows) {
-            mc.lgap = 1;
-            mc.lrow = gap_used;
-            gap_used += mc.W;
-        } else {
-            mc.lgap = 0;
-            mc.lrow = plain_used;
-            plain_used += mc.W;
-        }
-    }
-    return plain_used;
-}
-
 uint32_t inverse_mod(uint32_t a, uint32_t m) {
     a %= m;
     for (uint32_t x = 1; x < m; ++x)
@@ -255,13 +238,39 @@ int build_plan(const redash_params *p, Plan *pl) {
         }
     }
     pl->G = G;
-    // Chunks: split every run of gates with one digit label into 4s, 2s and 1s.
+    // Where every label lives while the evaluator walks the gates.  Phase A
+    // reads the inputs and leaves its results in the output tensor (final
+    // for R).  Phase B works on copies of the R labels: R[0] is only ever a
+    // digit and is read in place, R[1..u-1] move to the working storage on
+    // their first update; the S slots restart as zero accumulators.
+    uint32_t wk = 0;
+    for (uint32_t b = 1; b < pl->u; ++b) {
+        pl->mod[pl->R[b]].wkoff = wk;
+        wk += pl->mod[pl->R[b]].W;
+    }
+    pl->work_words = wk;
+    uint32_t loc[kMaxK];
+    for (uint32_t i = 0; i < pl->k; ++i) loc[i] = kLocIn;
+    bool phase_b = false;
+    for (uint32_t g = 0; g < G; ++g) {
+        uint32_t &d = pl->gate[g];
+        if (gate_phase(d) && !phase_b) {
+            phase_b = true;
+            for (uint32_t a = 0; a < pl->t; ++a) loc[pl->S[a]] = kLocZero;
+        }
+        const uint32_t src = gate_src(d), dst = gate_dst(d);
+        const bool to_work = phase_b && !(is_scale & (1u << dst));
+        d |= (loc[dst] << 10) | ((to_work ? 1u : 0u) << 12) | (loc[src] << 13);
+        loc[dst] = to_work ? kLocWork : kLocOut;
+    }
+    // Chunks: split every run of gates with one digit label into pieces of
+    // kMaxChunk gates (4 or 2), then 2s and 1s.
     for (uint32_t g = 0; g < G;) {
         uint32_t run = 1;
         while (g + run < G && gate_src(pl->gate[g + run]) == gate_src(pl->gate[g])) ++run;
         for (uint32_t done = 0; done < run;) {
             const uint32_t left = run - done;
-            const uint32_t len = left >= 4 ? 4 : (left >= 2 ? 2 : 1);
+            const uint32_t len = (left >= 4 && kMaxChunk >= 4) ? 4 : (left >= 2 ? 2 : 1);
             pl->gate[g + done] |= len << 24;
             done += len;
         }

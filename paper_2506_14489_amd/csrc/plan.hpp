@@ -49,30 +49,41 @@ struct ModConst {
     uint32_t red_M, red_s, sd_M, sd_s;
     uint32_t nlo_f, pw_lo_f, lo_M_f, lo_s_f;
     uint32_t nlo_l, pw_lo_l, lo_M_l, lo_s_l;
-    // Where the evaluator keeps this modulus's W working words in LDS (set
-    // for the block size of the launch): lgap = 1 puts them in the free
-    // halves of the table rows, starting at row lrow of that region;
-    // lgap = 0 in the plain region after it.
-    uint32_t lgap, lrow;
+    // Word offset of this modulus in the evaluator's working storage (only
+    // the remaining moduli R[1..u-1] have one: their Phase-B copies).
+    uint32_t wkoff;
 };
 
 // Gate descriptor packed in one word:
 //   bits 0-3 src modulus index, 4-7 dst modulus index, 8 kind (0 sub, 1 acc),
-//   9 phase (0 A, 1 B), 16-23 coefficient, 24-26 chunk length.
-// A chunk is a run of 1, 2 or 4 consecutive gates with the same digit label
-// (hence distinct destinations): the evaluator hashes them together.  The
-// chunk length is stored on the chunk's first gate and is 0 elsewhere.
+//   9 phase (0 A, 1 B), 10-11 where the destination label's current value
+//   is, 12 where its new value goes, 13-14 where the digit label is,
+//   16-23 coefficient, 24-26 chunk length.
+// A chunk is a run of up to kMaxChunk (a power of two) consecutive gates with
+// the same digit label (hence distinct destinations): the evaluator hashes
+// them together.  The chunk length is stored on the chunk's first gate and
+// is 0 elsewhere.
 constexpr uint32_t gate_src(uint32_t d) { return d & 15u; }
 constexpr uint32_t gate_dst(uint32_t d) { return (d >> 4) & 15u; }
 constexpr uint32_t gate_kind(uint32_t d) { return (d >> 8) & 1u; }
 constexpr uint32_t gate_phase(uint32_t d) { return (d >> 9) & 1u; }
+constexpr uint32_t gate_tsrc(uint32_t d) { return (d >> 10) & 3u; }
+constexpr uint32_t gate_tdst(uint32_t d) { return (d >> 12) & 1u; }
+constexpr uint32_t gate_dsrc(uint32_t d) { return (d >> 13) & 3u; }
 constexpr uint32_t gate_coeff(uint32_t d) { return (d >> 16) & 255u; }
 constexpr uint32_t gate_chunk(uint32_t d) { return (d >> 24) & 7u; }
-constexpr int kMaxChunk = 4;
+constexpr int kMaxChunk = 2;
+
+// Label locations in the evaluator: the input LabelTensor, the output
+// LabelTensor (which also holds intermediate labels until they are final),
+// the working storage (Phase-B copies of the remaining moduli, whose Phase-A
+// values are outputs), or a fresh accumulator (the all-zero label).
+constexpr uint32_t kLocIn = 0, kLocOut = 1, kLocWork = 2, kLocZero = 3;
 
 struct Plan {
     uint32_t k, t, u, G;
     uint32_t total_words;      // sum of W over the base (words per gadget per LabelTensor)
+    uint32_t work_words;       // evaluator working words per gadget: sum of W over R[1..u-1]
     uint32_t S[kMaxK];         // scaling modulus indices, ascending
     uint32_t R[kMaxK];         // remaining modulus indices, ascending
     uint32_t is_scale_mask;    // bit i set when modulus i is a scaling modulus
@@ -103,10 +114,5 @@ void division_constants(uint32_t d, uint64_t x_bound, uint32_t *M, uint32_t *s, 
 bool mul24_constants(uint32_t m, uint64_t x_bound, uint32_t *M, uint32_t *s);
 
 uint32_t inverse_mod(uint32_t a, uint32_t m);
-
-// Places every modulus's working words either wholly in the gap region
-// (gap_rows rows available) or in the plain region; returns the number of
-// plain-region rows used.
-uint32_t assign_label_rows(Plan *pl, uint32_t gap_rows);
 
 }  // namespace redash

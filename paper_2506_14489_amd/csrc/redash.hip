@@ -1,11 +1,10 @@
 // Kernels and C ABI of the ReDASH scaling-gadget library for gfx950.
 //
-// One thread evaluates (or garbles) one gadget instance.  The k working
-// labels of a gadget live in LDS as packed words laid out [word][thread], so
-// a wavefront touches 64 consecutive banks per access; the gate list and all
-// per-modulus constants are uniform and come from the kernel argument block
-// (scalar registers).  The AES round tables are staged into LDS once per
-// block.  Nothing here uses MFMA: the work is table lookups, XORs, 32-bit
+// One thread evaluates (or garbles) one gadget instance.  Labels are packed
+// words laid out [word][gadget], so a wavefront's label accesses are 64
+// consecutive words; the gate list and all per-modulus constants are uniform
+// and come from the kernel argument block (scalar registers).  The AES round
+// tables are staged into LDS once per workgroup.  Nothing here uses MFMA: the work is table lookups, XORs, 32-bit
 // multiplies for digit extraction and small modular arithmetic.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -24,56 +23,54 @@ struct SeedKey {
 // ---------------------------------------------------------------------------
 // Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
 //
-// LDS of a block (addresses from 0: the kernel declares no static LDS): the
-// 64 KiB table region (256 rows of 256 bytes, TE0 copies in the lower half
-// of each row), 48 words of round keys, then the plain label region.  Each
-// thread keeps the W working words of every modulus either in the free
-// upper halves of the table rows (32 threads' words per half row) or in the
-// plain region, as assign_label_rows() decided for the block size.
+// LDS of a workgroup (addresses from 0: the kernel declares no static LDS):
+// the 64 KiB two-table image, then the 88 round-key words.  Two workgroups
+// share a CU.  The working labels stay in global memory, mostly in L2: the
+// output tensor (and the working storage for Phase-B copies) holds every
+// intermediate label, each gate reads its destination label and its table
+// row before the AES runs and writes the destination back after it.
 // ---------------------------------------------------------------------------
-constexpr uint32_t kKeyBytes = 48 * 4;
-constexpr uint32_t kRestBase = kTableRegionBytes + kKeyBytes;
+constexpr uint32_t kEvalLdsBytes = kTableRegionBytes + kLdsKeyWords * 4;
 
-template <int BLOCK>
-struct LabelRows {
-    static constexpr uint32_t kGapRows = (256u * 32u) / BLOCK;
-    uint32_t gap_off, rest_off;  // this thread's byte offsets in the two regions
-    // byte address of word 0 of a modulus's label, and the step to word w+1
-    __device__ __forceinline__ uint32_t base(const ModConst &mc) const {
-        return mc.lgap ? mc.lrow * (BLOCK * 8u) + gap_off : mc.lrow * (BLOCK * 4u) + rest_off;
+// The four places a label can be (kLocIn, kLocOut, kLocWork, kLocZero) for
+// one thread: word w of a label starts at base + (offset + w) n, and the
+// thread's gadget adds its byte offset 4 a (below 2^32).
+struct LabelBufs {
+    const uint32_t *in;
+    uint32_t *out, *work;
+    uint64_t n;
+    uint32_t aoff;
+    // word 0 of modulus mc's label in place `loc` (not kLocZero); uniform
+    __device__ __forceinline__ const uint32_t *base(uint32_t loc, const ModConst &mc) const {
+        if (loc == kLocIn) return in + static_cast<uint64_t>(mc.woff) * n;
+        if (loc == kLocOut) return out + static_cast<uint64_t>(mc.woff) * n;
+        return work + static_cast<uint64_t>(mc.wkoff) * n;
     }
-    __device__ __forceinline__ static uint32_t step(const ModConst &mc) { return mc.lgap ? BLOCK * 8u : BLOCK * 4u; }
-    __device__ __forceinline__ static uint32_t get(uint32_t addr) {
-        return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
+    __device__ __forceinline__ uint32_t *dest(uint32_t to_work, const ModConst &mc) const {
+        return to_work ? work + static_cast<uint64_t>(mc.wkoff) * n : out + static_cast<uint64_t>(mc.woff) * n;
     }
-    __device__ __forceinline__ static void put(uint32_t addr, uint32_t v) {
-        *reinterpret_cast<lds_u32_rw *>(static_cast<uintptr_t>(addr)) = v;
+    __device__ __forceinline__ uint32_t get(const uint32_t *b, uint32_t w) const {
+        return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(b + w * n) + aoff);
     }
-    __device__ __forceinline__ uint32_t word(const ModConst &mc, uint32_t w) const { return get(base(mc) + w * step(mc)); }
-    __device__ __forceinline__ void set(const ModConst &mc, uint32_t w, uint32_t v) const {
-        put(base(mc) + w * step(mc), v);
+    __device__ __forceinline__ void put(uint32_t *b, uint32_t w, uint32_t v) const {
+        *reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(b + w * n) + aoff) = v;
     }
 };
-
-template <int BLOCK>
-__device__ __forceinline__ LabelRows<BLOCK> label_rows(uint32_t tid) {
-    return LabelRows<BLOCK>{(tid >> 5) * 256u + 128u + (tid & 31u) * 4u, kRestBase + tid * 4u};
-}
 
 // Moduli without the fast constants (41..61 and the largest ones): one
 // residue at a time with 32-bit divisions, in rolled loops; the gadget
 // configurations in use all take the fast path.
-template <int BLOCK>
 __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
-                                                    uint32_t (&row)[kMaxW], const LabelRows<BLOCK> &LR) {
+                                                    uint32_t (&row)[kMaxW], uint32_t (&tgt)[kMaxW],
+                                                    const LabelBufs &LB) {
     const uint32_t coeff = gate_coeff(d);
-    uint32_t addr = LR.base(mm);
-    for (uint32_t w = 0; w < mm.W; ++w, addr += LR.step(mm)) {
+    uint32_t *dst = LB.dest(gate_tdst(d), mm);
+    for (uint32_t w = 0; w < mm.W; ++w) {
         const bool last = (w + 1 == mm.W);
         const uint32_t nres = last ? mm.glast : mm.g;
         uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
         const uint32_t rw = next_word(row);
-        const uint32_t l = LR.get(addr);
+        const uint32_t l = next_word(tgt);
         uint32_t res = 0;
         // Digits come out least significant first: position nres-1 down to 0.
         for (uint32_t j = nres; j-- > 0;) {
@@ -91,89 +88,95 @@ __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &
                                                  : add_mod(lj, mul_mod(coeff, e, mm), mm.m);
             res |= r << (mm.b * j);
         }
-        LR.put(addr, res);
+        LB.put(dst, w, res);
     }
 }
 
-// Applies one gate's free operation to its destination label: E = row + pad,
-// then L <- c (L - E) (sub: division step and the recursion of
-// Eq. rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination onto a
-// scaling modulus).
-template <int BLOCK>
+// Applies one gate's free operation to its destination label (in tgt):
+// E = row + pad, then L <- c (L - E) (sub: division step and the recursion
+// of Eq. rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination
+// onto a scaling modulus), and stores the new label.
 __device__ __forceinline__ void eval_update(uint32_t d, const ModConst &mm, uint32_t (&V)[8], uint32_t (&row)[kMaxW],
-                                            const LabelRows<BLOCK> &LR) {
+                                            uint32_t (&tgt)[kMaxW], const LabelBufs &LB) {
     const uint32_t coeff = gate_coeff(d);
+    uint32_t *dst = LB.dest(gate_tdst(d), mm);
     if (mm.m == 2) {
-        const uint32_t base = LR.base(mm), step = LR.step(mm);
-        uint32_t l[4];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) l[w] = LR.get(base + w * step);
+        const bool flip = gate_kind(d) == 0 || (coeff & 1u);  // sub: q^{-1} = 1 mod 2
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const uint32_t E = bits_word(V, w) ^ row[w];
-            if (gate_kind(d) == 0 || (coeff & 1u)) l[w] ^= E;  // sub: q^{-1} = 1 mod 2
-            LR.put(base + w * step, l[w]);
+            LB.put(dst, w, flip ? tgt[w] ^ E : tgt[w]);
         }
     } else if (mm.fast) {
         // full words in a loop, the last word peeled: each with its own
         // constants, so no per-word selection
-        const uint32_t step = LR.step(mm), base = LR.base(mm);
         const bool acc = gate_kind(d) != 0;
 #pragma unroll 1
         for (uint32_t w = 0; w + 1 < mm.W; ++w) {
-            const uint32_t addr = base + w * step;
-            const uint32_t l = LR.get(addr);
+            const uint32_t l = next_word(tgt);
             const uint32_t D = frac_mul_carry(V, mm.pw_g);
             const uint32_t rw = next_word(row);
-            LR.put(addr, acc ? fast_word_any<true>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm)
-                             : fast_word_any<false>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm));
+            LB.put(dst, w,
+                   acc ? fast_word_any<true>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm)
+                       : fast_word_any<false>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm));
         }
-        const uint32_t addr = base + (mm.W - 1) * step;
-        const uint32_t l = LR.get(addr);
+        const uint32_t l = tgt[0];
         const uint32_t D = frac_mul_carry(V, mm.pw_last);
         const uint32_t rw = row[0];
-        LR.put(addr, acc ? fast_word_any<true>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm)
-                         : fast_word_any<false>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm));
+        LB.put(dst, mm.W - 1,
+               acc ? fast_word_any<true>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm)
+                   : fast_word_any<false>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm));
     } else {
-        eval_update_generic<BLOCK>(d, mm, V, row, LR);
+        eval_update_generic(d, mm, V, row, tgt, LB);
     }
 }
 
-// Hashes the NG gates g..g+NG-1, which share one digit label: the rows of
-// all of them are requested first (the colour is known before hashing), then
-// the 2 NG AES blocks run interleaved.  Fills V[0..NG-1] and row[0..NG-1].
-template <int NG, int BLOCK>
-__device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &toff, const PermTE0 &TT,
-                                           const uint32_t *K, const LabelRows<BLOCK> &LR, uint64_t a, uint64_t tau0,
+// Hashes the NG gates g..g+NG-1, which share one digit label: reads the
+// digit label, requests every gate's row (the colour is known before
+// hashing) and destination label, then runs the 2 NG AES blocks
+// interleaved.  Fills V, row and tgt for the NG gates.
+template <int NG>
+__device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &toff, const PermTE02 &TT,
+                                           const uint32_t *K, const LabelBufs &LB, uint64_t a, uint64_t tau0,
                                            const uint32_t *__restrict__ tab, uint32_t (&V)[kMaxChunk][8],
-                                           uint32_t (&row)[kMaxChunk][kMaxW]) {
+                                           uint32_t (&row)[kMaxChunk][kMaxW], uint32_t (&tgt)[kMaxChunk][kMaxW]) {
     const uint64_t n = P.n;
     // Local copies of the modulus constants: the compiler keeps their fields
     // in scalar registers (a pointer into the argument block could end up in
     // vector registers and make every loop bound derived from it divergent).
-    uint32_t Wd[NG];
-    static_for<NG>([&](auto j) { Wd[j] = P.mod[gate_dst(P.gate[g + j])].W; });
-    const ModConst mq = P.mod[gate_src(P.gate[g])];
+    const uint32_t d0 = P.gate[g];
+    const ModConst mq = P.mod[gate_src(d0)];
     const uint32_t q = mq.m;
-    const uint32_t w0 = LR.word(mq, 0);
-    // A residue >= q only occurs in a malformed input label; it selects the
-    // implicit zero row, the output is garbage and decode flags it.
-    uint32_t colour = w0 & mq.mask;
-    if (colour >= q) colour = 0;
-    static_for<NG>([&](auto j) {
-        static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
-        if (colour != 0) {
-            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * Wd[j];
-            static_for<kMaxW>([&](auto w) {
-                if (w < static_cast<int>(Wd[j])) row[j][w] = rp[w];
-            });
-        }
-        toff += n * (q - 1) * Wd[j];
-    });
-    uint32_t x[4] = {w0, 0, 0, 0};
+    const uint32_t *dig = LB.base(gate_dsrc(d0), mq);
+    uint32_t x[4] = {LB.get(dig, 0), 0, 0, 0};
     static_for<kMaxW - 1>([&](auto w1) {
         constexpr int w = decltype(w1)::value + 1;
-        if (w < static_cast<int>(mq.W)) x[w & 3] ^= LR.word(mq, w);
+        if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
+    });
+    // A residue >= q only occurs in a malformed input label; it selects the
+    // implicit zero row, the output is garbage and decode flags it.
+    uint32_t colour = LB.get(dig, 0) & mq.mask;
+    if (colour >= q) colour = 0;
+    static_for<NG>([&](auto j) {
+        const uint32_t dj = P.gate[g + j];
+        const ModConst &md = P.mod[gate_dst(dj)];
+        const uint32_t Wd = md.W;
+        static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
+        if (colour != 0) {
+            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * Wd;
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(Wd)) row[j][w] = rp[w];
+            });
+        }
+        toff += n * (q - 1) * Wd;
+        static_for<kMaxW>([&](auto w) { tgt[j][w] = 0; });
+        const uint32_t tsrc = gate_tsrc(dj);
+        if (tsrc != kLocZero) {
+            const uint32_t *tp = LB.base(tsrc, md);
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(Wd)) tgt[j][w] = LB.get(tp, w);
+            });
+        }
     });
     uint32_t Vn[NG][8];
     hash_fraction_n<NG>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g, P.gid, Vn);
@@ -182,53 +185,29 @@ __device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &
 
 template <int BLOCK>
 __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__restrict__ in,
-                                                const uint32_t *__restrict__ tab, uint32_t *__restrict__ out) {
+                                                const uint32_t *__restrict__ tab, uint32_t *out, uint32_t *work) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    stage_perm_te0(lds, tid, BLOCK);
+    stage_perm_te02(lds, tid, BLOCK);
     stage_hash_key(K, tid, BLOCK);
     __syncthreads();
-    const PermTE0 TT = perm_te0();
-    const LabelRows<BLOCK> LR = label_rows<BLOCK>(tid);
+    const PermTE02 TT = perm_te02();
     const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
     if (a >= P.n) return;  // no barrier follows
-    const uint64_t n = P.n;
-
-    for (uint32_t i = 0; i < P.k; ++i) {
-        const ModConst &mc = P.mod[i];
-        const uint32_t *src = in + static_cast<uint64_t>(mc.woff) * n + a;
-        for (uint32_t w = 0; w < mc.W; ++w) LR.set(mc, w, src[static_cast<uint64_t>(w) * n]);
-    }
+    const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(a) * 4u};
 
     const uint64_t tau0 = (P.a0 + a) * P.G;
     uint64_t toff = 0;
-    bool phaseB = false;
     for (uint32_t g = 0; g < P.G;) {
-        const uint32_t d = P.gate[g];
-        if (gate_phase(d) && !phaseB) {
-            // End of the division step: the remaining-modulus labels are the
-            // gadget's outputs on R; the scaling-modulus slots restart as
-            // accumulators at the all-zero label.
-            phaseB = true;
-            for (uint32_t b = 0; b < P.u; ++b) {
-                const ModConst &mc = P.mod[P.R[b]];
-                uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
-                for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = LR.word(mc, w);
-            }
-            for (uint32_t s = 0; s < P.t; ++s) {
-                const ModConst &mc = P.mod[P.S[s]];
-                for (uint32_t w = 0; w < mc.W; ++w) LR.set(mc, w, 0);
-            }
-        }
-        const uint32_t len = gate_chunk(d);
-        uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW];
-        if (len == 4) {
-            hash_chunk<4, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
+        const uint32_t len = gate_chunk(P.gate[g]);
+        uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW], tgt[kMaxChunk][kMaxW];
+        if (kMaxChunk >= 4 && len == 4) {
+            hash_chunk<(kMaxChunk >= 4 ? 4 : 1)>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
         } else if (len == 2) {
-            hash_chunk<2, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
+            hash_chunk<2>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
         } else {
-            hash_chunk<1, BLOCK>(P, g, toff, TT, K, LR, a, tau0, tab, V, row);
+            hash_chunk<1>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
         }
         // One copy of the update code for every chunk size: the chunk's
         // gates go through a queue (entry 0 is processed, the rest move down).
@@ -236,18 +215,16 @@ __global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__
         for (uint32_t j = 0; j < len; ++j) {
             const uint32_t dj = P.gate[g + j];
             const ModConst mm = P.mod[gate_dst(dj)];
-            eval_update<BLOCK>(dj, mm, V[0], row[0], LR);
+            eval_update(dj, mm, V[0], row[0], tgt[0], LB);
             static_for<kMaxChunk - 1>([&](auto k) {
                 static_for<8>([&](auto l) { V[k][l] = V[k + 1][l]; });
-                static_for<kMaxW>([&](auto w) { row[k][w] = row[k + 1][w]; });
+                static_for<kMaxW>([&](auto w) {
+                    row[k][w] = row[k + 1][w];
+                    tgt[k][w] = tgt[k + 1][w];
+                });
             });
         }
         g += len;
-    }
-    for (uint32_t s = 0; s < P.t; ++s) {
-        const ModConst &mc = P.mod[P.S[s]];
-        uint32_t *dst = out + static_cast<uint64_t>(mc.woff) * n + a;
-        for (uint32_t w = 0; w < mc.W; ++w) dst[static_cast<uint64_t>(w) * n] = LR.word(mc, w);
     }
 }
 
@@ -563,22 +540,9 @@ int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
 
-// Launches k_eval with the largest block (512, 256, 128 or 64 threads) whose LDS
-// footprint fits the device.
-template <int BLOCK>
-int try_eval(const Plan &P0, size_t max_lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
-             hipStream_t stream, bool *done) {
-    if (*done) return REDASH_OK;
-    Plan P = P0;
-    const uint32_t plain_rows = assign_label_rows(&P, LabelRows<BLOCK>::kGapRows);
-    const size_t lds = kRestBase + static_cast<size_t>(plain_rows) * BLOCK * 4;
-    if (lds > max_lds) return REDASH_OK;
-    *done = true;
-    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<BLOCK>), lds);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_eval<BLOCK>, dim3(grid_for(P.n, BLOCK)), dim3(BLOCK), lds, stream, P, in, tab, out);
-    return launched();
-}
+// Block size of the evaluator: two workgroups of 512 threads share a CU
+// (2 x 64.3 KiB of LDS), i.e. four waves per SIMD.
+constexpr int kEvalBlock = 512;
 
 template <int BLOCK>
 int try_garble(const Plan &P, size_t max_lds, const SeedKey &key, const uint32_t *offsets, uint32_t *zin,
@@ -622,6 +586,7 @@ int redash_plan(const redash_params *p, redash_sizes *out) {
     out->table_words = tw;
     out->offset_words = P.total_words;
     out->gates = P.G;
+    out->work_words = P.n * P.work_words;
     return REDASH_OK;
 }
 
@@ -659,20 +624,20 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
 }
 
 int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
-                      uint32_t *d_out_labels, hipStream_t stream) {
+                      uint32_t *d_out_labels, uint32_t *d_work, hipStream_t stream) {
     Plan P;
     int rc = build_plan(p, &P);
     if (rc) return rc;
+    if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
     if (P.n == 0) return REDASH_OK;
-    if (!d_in_labels || !d_tables || !d_out_labels) return REDASH_E_NULL;
+    if (!d_in_labels || !d_tables || !d_out_labels || (P.work_words && !d_work)) return REDASH_E_NULL;
     size_t max_lds = 0;
     if ((rc = max_lds_bytes(&max_lds))) return rc;
-    bool done = false;
-    if ((rc = try_eval<512>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
-    if ((rc = try_eval<256>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
-    if ((rc = try_eval<128>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
-    if ((rc = try_eval<64>(P, max_lds, d_in_labels, d_tables, d_out_labels, stream, &done))) return rc;
-    return done ? REDASH_OK : REDASH_E_PARAM;
+    if (kEvalLdsBytes > max_lds) return REDASH_E_HIP;
+    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), kEvalLdsBytes))) return rc;
+    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, kEvalBlock)), dim3(kEvalBlock), kEvalLdsBytes, stream,
+                       P, d_in_labels, d_tables, d_out_labels, d_work);
+    return launched();
 }
 
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,

@@ -75,7 +75,7 @@ def gpu_pipeline(params, x: np.ndarray, device="cuda"):
     B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables)
     xd = torch.from_numpy(np.ascontiguousarray(x, dtype=np.int64)).to(device)
     B.redash_encode(params, xd, buf.in_zero, buf.offsets, buf.in_labels)
-    B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels)
+    B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work)
     B.redash_decode(params, buf.out_labels, buf.out_zero, buf.offsets, buf.y, buf.bad)
     torch.cuda.synchronize()
     return buf

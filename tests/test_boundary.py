@@ -28,7 +28,9 @@ def test_params_struct_layout_matches_header():
     # k, moduli[16], t, scale_idx[16] (4-byte) then n, seed, a0 (8-byte)
     assert ctypes.sizeof(B.Params) == 4 * 34 + 8 * 3
     assert B.Params.n.offset == 136 and B.Params.a0.offset == 152
-    assert ctypes.sizeof(B.Sizes) == 24
+    # label_words, table_words (8-byte), offset_words, gates (4-byte), work_words (8-byte)
+    assert ctypes.sizeof(B.Sizes) == 32
+    assert B.Sizes.work_words.offset == 24
 
 
 def test_strerror_texts():
@@ -56,6 +58,16 @@ def test_plan_sizes_match_oracle(moduli, S, n):
     assert sz["gates"] == osz["gates"]
     k, t = len(moduli), len(S)
     assert sz["gates"] == k * (k - 1) // 2 + t * (k - t)
+
+
+@pytest.mark.parametrize("moduli,S", PLAN_CASES)
+def test_work_words(moduli, S):
+    """The evaluator's working storage holds the Phase-B copies of the
+    remaining moduli after the first one (R[0] is only ever a digit)."""
+    n = 777
+    R = [i for i in range(len(moduli)) if i not in S]
+    sz = B.redash_plan(B.make_params(moduli, S, n, 0))
+    assert sz["work_words"] == n * sum(O.words(moduli[i]) for i in R[1:])
 
 
 @pytest.mark.parametrize("m", rns.first_primes(12) + [97, 107, 167, 173, 251])
@@ -115,12 +127,16 @@ def test_entry_points_validate_before_any_device_work():
     bad = B.make_params([3, 5, 7], [2], 4, 0)  # P odd
     good = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 4, 0)
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below returns early
-    assert L.redash_eval_scale(ctypes.byref(bad), fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_eval_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_garble_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_encode(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_decode(ctypes.byref(bad), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
-    assert L.redash_eval_scale(ctypes.byref(good), None, fake, fake, None) == B.REDASH_E_NULL
-    assert L.redash_eval_scale(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(ctypes.byref(good), fake, None, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(ctypes.byref(good), fake, fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
+    huge = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 1 << 30, 0)
+    assert L.redash_eval_scale(ctypes.byref(huge), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_garble_scale(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
     assert L.redash_encode(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
@@ -128,4 +144,4 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_hash_labels(4, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 256, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 5, 1, None, 0, fake, fake, None) == B.REDASH_E_NULL
-    assert L.redash_eval_scale(None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale(None, fake, fake, fake, fake, None) == B.REDASH_E_NULL

@@ -116,7 +116,8 @@ def test_eval_on_oracle_tables_matches_oracle(case):
     X = O.encode(op, x, zin, offs)
     Y = O.evaluate(op, a0, n, X, tab)
     out = torch.empty(len(X), dtype=torch.int32, device="cuda")
-    B.redash_eval_scale(bp, H.to_dev(X), H.to_dev(tab), out)
+    work = torch.empty(max(B.redash_plan(bp)["work_words"], 1), dtype=torch.int32, device="cuda")
+    B.redash_eval_scale(bp, H.to_dev(X), H.to_dev(tab), out, work)
     torch.cuda.synchronize()
     got = H.to_u32(out)
     assert np.array_equal(got, Y)
@@ -176,7 +177,7 @@ def test_eval_is_repeatable_and_leaves_inputs():
     first = H.to_u32(buf.out_labels).copy()
     inp = H.to_u32(buf.in_labels).copy()
     for _ in range(3):
-        B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels)
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels, buf.work)
     torch.cuda.synchronize()
     assert np.array_equal(H.to_u32(buf.out_labels), first)
     assert np.array_equal(H.to_u32(buf.in_labels), inp)
@@ -189,7 +190,7 @@ def test_empty_calls_are_noops():
     offs = torch.empty(sz["offset_words"], dtype=torch.int32, device="cuda")
     e = torch.empty(1, dtype=torch.int32, device="cuda")
     B.redash_garble_scale(bp, offs, e, e, e)
-    B.redash_eval_scale(bp, e, e, e)
+    B.redash_eval_scale(bp, e, e, e, e)
     bad = torch.full((1,), 7, dtype=torch.int64, device="cuda")
     B.redash_decode(bp, e, e, offs, torch.empty(1, dtype=torch.int64, device="cuda"), bad)
     torch.cuda.synchronize()
