@@ -26,6 +26,8 @@ METRIC = "garbled scaling gadgets evaluated/sec (1 GPU) + % HBM roofline"
 HBM_PEAK_GBS = 8000.0
 # int32 vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one lane-op per lane per clock)
 ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# LDS: 128 bytes per clock per CU (32 banks x 4 bytes)
+LDS_PEAK_GBS = 256 * 128 * 2.4e9 / 1e9
 
 
 def log(*a):
@@ -149,6 +151,7 @@ def main():
     gadgets_per_s = n / (ms_step / 1e3)
     bytes_g = cost.bytes_per_gadget(w.moduli, w.scale_idx)
     ops_g = cost.ops_per_gadget(w.moduli, w.scale_idx)
+    lds_g = cost.lds_bytes_per_gadget(w.moduli, w.scale_idx)
     aes_g = cost.aes_blocks_per_gadget(w.moduli, w.scale_idx)
     achieved_tops = ops_g * n / (ms_step / 1e3) / 1e12
     achieved_gbs = bytes_g * n / (ms_step / 1e3) / 1e9
@@ -193,6 +196,13 @@ def main():
             "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
             "bytes_per_gadget": round(bytes_g, 1),
             "measured_bytes_per_gadget": None if traffic_b is None else round(traffic_b / n, 1),
+        },
+        "lds": {
+            "achieved": round(lds_g * n / (ms_step / 1e3) / 1e9, 1),
+            "peak": round(LDS_PEAK_GBS, 1),
+            "unit": "GB/s",
+            "frac": round(lds_g * n / (ms_step / 1e3) / 1e9 / LDS_PEAK_GBS, 4),
+            "bytes_per_gadget": lds_g,
         },
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
         "check": check,

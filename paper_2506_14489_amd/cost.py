@@ -6,18 +6,24 @@ Per gadget (structure of the gate list in include/redash.h):
     words) plus, per projection gate q -> m, one W_m-word row, read with
     probability (q-1)/q because the colour-0 row is implicit (row reduction);
   * AES-128 blocks: two per gate, one when the output modulus is 2;
-  * algorithmic 32-bit integer operations of the table formulation:
-      - per AES block: 10 rounds x 16 (byte extract + table read + XOR)
-        + 4 initial key XORs = 484, plus 12 XORs for tweak and feed-forward;
+  * algorithmic 32-bit integer (vector ALU) operations of the table
+    formulation:
+      - per AES block: 10 rounds x 16 lookups, each an index extraction and
+        one XOR (the 16 XORs of a round combine 4 table words and the round
+        key per column; the table reads themselves are LDS reads, counted
+        separately below), + 4 initial key XORs = 324, plus 12 XORs for the
+        tweak and the feed-forward;
       - per gate: W_q + 1 for folding the input label and sigma;
       - per output word (m > 2): 8 limb multiply-adds of 4 operations each;
       - per output residue (m > 2): 14 (digit split 3, row add 3, free
-        operation 5, field extract and insert 3); per word for m = 2: 3.
+        operation 5, field extract and insert 3); per word for m = 2: 3;
+  * LDS table reads: 160 4-byte lookups per AES block (T-table AES).
 """
 
 from __future__ import annotations
 
-AES_OPS_PER_BLOCK = 484 + 12
+AES_OPS_PER_BLOCK = 10 * 16 * 2 + 4 + 12
+AES_LOOKUPS_PER_BLOCK = 10 * 16
 LIMB_OPS_PER_WORD = 8 * 4
 OPS_PER_RESIDUE = 14
 
@@ -70,6 +76,11 @@ def ops_per_gadget(moduli, scale_idx) -> int:
         else:
             total += LIMB_OPS_PER_WORD * words(m) + OPS_PER_RESIDUE * lam(m)
     return total
+
+
+def lds_bytes_per_gadget(moduli, scale_idx) -> int:
+    """Bytes of AES round-table reads per gadget (4-byte lookups)."""
+    return 4 * AES_LOOKUPS_PER_BLOCK * aes_blocks_per_gadget(moduli, scale_idx)
 
 
 def table_bytes_per_gadget(moduli, scale_idx) -> int:

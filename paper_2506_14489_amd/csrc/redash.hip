@@ -24,13 +24,16 @@ struct SeedKey {
 // Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
 //
 // LDS of a workgroup (addresses from 0: the kernel declares no static LDS):
-// the 64 KiB two-table image, then the 88 round-key words.  Two workgroups
-// share a CU.  The working labels stay in global memory, mostly in L2: the
+// the 64 KiB two-table image, then the 88 round-key words.  The working labels stay in global memory, mostly in L2: the
 // output tensor (and the working storage for Phase-B copies) holds every
 // intermediate label, each gate reads its destination label and its table
 // row before the AES runs and writes the destination back after it.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kEvalLdsBytes = kTableRegionBytes + kLdsKeyWords * 4;
+// Two workgroups of 768 threads share a CU (2 x 64.3 KiB of LDS): six waves
+// per SIMD, which caps the kernel at 80 VGPRs.
+constexpr int kEvalBlock = 768;
+constexpr int kEvalWaves = 6;
 
 // The four places a label can be (kLocIn, kLocOut, kLocWork, kLocZero) for
 // one thread: word w of a label starts at base + (offset + w) n, and the
@@ -49,11 +52,13 @@ struct LabelBufs {
     __device__ __forceinline__ uint32_t *dest(uint32_t to_work, const ModConst &mc) const {
         return to_work ? work + static_cast<uint64_t>(mc.wkoff) * n : out + static_cast<uint64_t>(mc.woff) * n;
     }
+    // (opaque: the zero extension of the offset must sit next to the access,
+    // or the scalar-base addressing form is not selected)
     __device__ __forceinline__ uint32_t get(const uint32_t *b, uint32_t w) const {
-        return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(b + w * n) + aoff);
+        return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(b + w * n) + opaque(aoff));
     }
     __device__ __forceinline__ void put(uint32_t *b, uint32_t w, uint32_t v) const {
-        *reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(b + w * n) + aoff) = v;
+        *reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(b + w * n) + opaque(aoff)) = v;
     }
 };
 
@@ -184,7 +189,8 @@ __device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &
 }
 
 template <int BLOCK>
-__global__ void __launch_bounds__(BLOCK) k_eval(const Plan P, const uint32_t *__restrict__ in,
+__global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))
+k_eval(const Plan P, const uint32_t *__restrict__ in,
                                                 const uint32_t *__restrict__ tab, uint32_t *out, uint32_t *work) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
@@ -539,10 +545,6 @@ unsigned grid_for(uint64_t n, int block) { return static_cast<unsigned>((n + blo
 int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
-
-// Block size of the evaluator: two workgroups of 512 threads share a CU
-// (2 x 64.3 KiB of LDS), i.e. four waves per SIMD.
-constexpr int kEvalBlock = 512;
 
 template <int BLOCK>
 int try_garble(const Plan &P, size_t max_lds, const SeedKey &key, const uint32_t *offsets, uint32_t *zin,

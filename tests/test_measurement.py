@@ -85,6 +85,26 @@ def test_aes_blocks_count_hash_calls():
     assert len(O.hash_label(3, 5, [0] * O.lam(3), 7, 1)) == O.lam(5)
 
 
+def test_op_model_constants():
+    """T-table AES: 10 rounds of 16 lookups; a lookup is one index
+    extraction and one XOR of vector ALU work and one 4-byte LDS read."""
+    assert cost.AES_OPS_PER_BLOCK == 10 * 16 * 2 + 4 + 12
+    assert cost.AES_LOOKUPS_PER_BLOCK == 160
+    w = WL.by_name("batched")
+    assert cost.lds_bytes_per_gadget(w.moduli, w.scale_idx) == 153 * 160 * 4
+    # every gate of the base (2, 3, 37) scaled by 37: AES, fold, limb and residue terms
+    assert cost.ops_per_gadget([2, 3, 37], [2]) == (
+        (1 * cost.AES_OPS_PER_BLOCK + cost.words(37) + 1 + 3 * cost.words(2))
+        + (2 * cost.AES_OPS_PER_BLOCK + cost.words(37) + 1 + cost.LIMB_OPS_PER_WORD * cost.words(3)
+           + cost.OPS_PER_RESIDUE * cost.lam(3))
+        + (2 * cost.AES_OPS_PER_BLOCK + cost.words(2) + 1 + cost.LIMB_OPS_PER_WORD * cost.words(3)
+           + cost.OPS_PER_RESIDUE * cost.lam(3))
+        + (2 * cost.AES_OPS_PER_BLOCK + cost.words(2) + 1 + cost.LIMB_OPS_PER_WORD * cost.words(37)
+           + cost.OPS_PER_RESIDUE * cost.lam(37))
+        + (2 * cost.AES_OPS_PER_BLOCK + cost.words(3) + 1 + cost.LIMB_OPS_PER_WORD * cost.words(37)
+           + cost.OPS_PER_RESIDUE * cost.lam(37)))
+
+
 def test_traffic_only_for_unchanged_sources(monkeypatch):
     rec = traffic.MEASURED["batched"]
     monkeypatch.setitem(rec, "sources_sha256", traffic.sources_sha256())
