@@ -127,6 +127,11 @@ __device__ __forceinline__ uint32_t lds_read(uint32_t addr) {
     return *reinterpret_cast<lds_u32 *>(static_cast<uintptr_t>(addr));
 }
 
+typedef __attribute__((address_space(3))) const uint8_t lds_u8;
+__device__ __forceinline__ uint32_t lds_read_u8(uint32_t addr) {
+    return *reinterpret_cast<lds_u8 *>(static_cast<uintptr_t>(addr));
+}
+
 struct PermTE02 {
     uint32_t off0, off2;  // 4 (lane mod 32), and that + 128
     // address bytes: [offset, byte k of w, 0, 0]
@@ -407,9 +412,14 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_
 
 // fast_word with the residue count and field width known at compile time:
 // every loop unrolled, every shift an immediate.
-template <bool ACC, int NRES, int B>
+//
+// With TAB, the product c (v mod m) mod m comes from the gate's byte table in
+// LDS (v < 3m, see free_op_table): tk is the table's LDS address, plus 2m for
+// a sub gate, so the sub gate's byte address is lj + tk - p - r.
+template <bool ACC, int NRES, int B, bool TAB>
 __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo,
-                                                uint32_t rw, uint32_t l, uint32_t c, const ModConst &mc) {
+                                                uint32_t rw, uint32_t l, uint32_t c, const ModConst &mc,
+                                                uint32_t tk) {
     constexpr int NLO = NRES / 2, NHI = NRES - NLO;
     constexpr uint32_t MASK = (1u << B) - 1u;
     const uint32_t m = uniform24(mc.m);
@@ -428,11 +438,20 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
         constexpr int j = decltype(jc)::value;
         const uint32_t r = (rw >> (B * j)) & MASK;
         const uint32_t lj = (l >> (B * j)) & MASK;
-        const uint32_t v = ACC ? lj + mul24(c, __builtin_amdgcn_ubfe(p + r, 0, 16))
-                               : mul24(c, __builtin_amdgcn_ubfe(lj + mc.two_m - p - r, 0, 16));
-        const uint32_t q = __builtin_amdgcn_ubfe(mul24(v, mc.red_M), mc.red_s, 24);
-        // (opaque: a shift folded into the product would widen its operand)
-        res |= opaque(v - mul24(q, m)) << (B * j);
+        if constexpr (TAB) {
+            if constexpr (ACC) {
+                const uint32_t x = lj + lds_read_u8(tk + p + r);  // < 2m
+                res |= umin(x, x - m) << (B * j);
+            } else {
+                res |= lds_read_u8(lj + tk - p - r) << (B * j);
+            }
+        } else {
+            const uint32_t v = ACC ? lj + mul24(c, __builtin_amdgcn_ubfe(p + r, 0, 16))
+                                   : mul24(c, __builtin_amdgcn_ubfe(lj + mc.two_m - p - r, 0, 16));
+            const uint32_t q = __builtin_amdgcn_ubfe(mul24(v, mc.red_M), mc.red_s, 24);
+            // (opaque: a shift folded into the product would widen its operand)
+            res |= opaque(v - mul24(q, m)) << (B * j);
+        }
     };
     // low part: positions NRES-1 down to NHI; high part: NHI-1 down to 0
     uint32_t x = lo;
@@ -462,13 +481,13 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
 
 // Dispatch on (residues in the word, bits per residue): the combinations
 // of the primes up to 37 are unrolled, anything else takes the loops.
-template <bool ACC>
+template <bool ACC, bool TAB>
 __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uint32_t nlo, uint32_t lo_M,
                                                   uint32_t lo_s, uint32_t pw_lo, uint32_t rw, uint32_t l, uint32_t c,
-                                                  const ModConst &mc) {
+                                                  const ModConst &mc, uint32_t tk) {
     switch (nres | (mc.b << 8)) {
 #define REDASH_FW(NR, BB) \
-    case (NR) | ((BB) << 8): return fast_word_c<ACC, NR, BB>(D, lo_M, lo_s, pw_lo, rw, l, c, mc);
+    case (NR) | ((BB) << 8): return fast_word_c<ACC, NR, BB, TAB>(D, lo_M, lo_s, pw_lo, rw, l, c, mc, tk);
         REDASH_FW(16, 2) REDASH_FW(1, 2) REDASH_FW(10, 3) REDASH_FW(6, 3) REDASH_FW(8, 4) REDASH_FW(6, 4)
         REDASH_FW(3, 4) REDASH_FW(6, 5) REDASH_FW(5, 5) REDASH_FW(3, 5) REDASH_FW(2, 5) REDASH_FW(1, 5)
         REDASH_FW(5, 6)

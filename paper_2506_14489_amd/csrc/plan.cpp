@@ -262,7 +262,10 @@ int build_plan(const redash_params *p, Plan *pl) {
         const bool to_work = phase_b && !(is_scale & (1u << dst));
         d |= (loc[dst] << 10) | ((to_work ? 1u : 0u) << 12) | (loc[src] << 13);
         loc[dst] = to_work ? kLocWork : kLocOut;
+        const ModConst &md = pl->mod[dst];
+        if (g < kMaxTables && md.m > 2 && md.m <= kTableMaxModulus && md.fast) d |= 1u << 15;
     }
+    pl->ntab = G < kMaxTables ? G : kMaxTables;
     // Chunks: split every run of gates with one digit label into pieces of
     // kMaxChunk gates (4 or 2), then 2s and 1s.
     for (uint32_t g = 0; g < G;) {

@@ -57,8 +57,9 @@ struct ModConst {
 // Gate descriptor packed in one word:
 //   bits 0-3 src modulus index, 4-7 dst modulus index, 8 kind (0 sub, 1 acc),
 //   9 phase (0 A, 1 B), 10-11 where the destination label's current value
-//   is, 12 where its new value goes, 13-14 where the digit label is,
-//   16-23 coefficient, 24-26 chunk length.
+//   is, 12 where its new value goes, 13-14 where the digit label is, 15 the
+//   gate's free operation uses a byte table (see below), 16-23 coefficient,
+//   24-26 chunk length.
 // A chunk is a run of up to kMaxChunk (a power of two) consecutive gates with
 // the same digit label (hence distinct destinations): the evaluator hashes
 // them together.  The chunk length is stored on the chunk's first gate and
@@ -70,9 +71,19 @@ constexpr uint32_t gate_phase(uint32_t d) { return (d >> 9) & 1u; }
 constexpr uint32_t gate_tsrc(uint32_t d) { return (d >> 10) & 3u; }
 constexpr uint32_t gate_tdst(uint32_t d) { return (d >> 12) & 1u; }
 constexpr uint32_t gate_dsrc(uint32_t d) { return (d >> 13) & 3u; }
+constexpr uint32_t gate_tab(uint32_t d) { return (d >> 15) & 1u; }
 constexpr uint32_t gate_coeff(uint32_t d) { return (d >> 16) & 255u; }
 constexpr uint32_t gate_chunk(uint32_t d) { return (d >> 24) & 7u; }
 constexpr int kMaxChunk = 2;
+
+// Free-operation tables: gate g < ntab whose output modulus m satisfies
+// 2 < m <= kTableMaxModulus (and has the fast constants) gets 128 bytes of
+// LDS holding c (v mod m) mod m for v < 3m, c the gate's coefficient.  The
+// evaluator then needs no multiply and no reduction per residue.  A table of
+// at most 128 bytes spans the 32 LDS banks once: lookups never conflict.
+constexpr uint32_t kTableBytes = 128;
+constexpr uint32_t kTableMaxModulus = 42;  // 3m <= 128
+constexpr uint32_t kMaxTables = 125;       // keeps two evaluator workgroups per CU
 
 // Label locations in the evaluator: the input LabelTensor, the output
 // LabelTensor (which also holds intermediate labels until they are final),
@@ -84,6 +95,7 @@ struct Plan {
     uint32_t k, t, u, G;
     uint32_t total_words;      // sum of W over the base (words per gadget per LabelTensor)
     uint32_t work_words;       // evaluator working words per gadget: sum of W over R[1..u-1]
+    uint32_t ntab;             // gates 0..ntab-1 have a free-operation table slot
     uint32_t S[kMaxK];         // scaling modulus indices, ascending
     uint32_t R[kMaxK];         // remaining modulus indices, ascending
     uint32_t is_scale_mask;    // bit i set when modulus i is a scaling modulus

@@ -24,12 +24,17 @@ struct SeedKey {
 // Evaluator: the hot path (Sec. 3.4 gadget, Sec. 2.3 projection gates).
 //
 // LDS of a workgroup (addresses from 0: the kernel declares no static LDS):
-// the 64 KiB two-table image, then the 88 round-key words.  The working labels stay in global memory, mostly in L2: the
+// the 64 KiB two-table image, the 88 round-key words, then one 128-byte
+// free-operation table per gate (up to kMaxTables).  The working labels stay in global memory, mostly in L2: the
 // output tensor (and the working storage for Phase-B copies) holds every
 // intermediate label, each gate reads its destination label and its table
 // row before the AES runs and writes the destination back after it.
 // ---------------------------------------------------------------------------
-constexpr uint32_t kEvalLdsBytes = kTableRegionBytes + kLdsKeyWords * 4;
+constexpr uint32_t kEvalTableBase = kTableRegionBytes + 384;  // after the 352 key bytes
+// LDS bytes of an evaluator workgroup with ntab free-operation tables.
+constexpr uint32_t eval_lds_bytes(uint32_t ntab) { return kEvalTableBase + ntab * kTableBytes; }
+static_assert(kLdsKeyWords * 4 <= 384, "round keys overlap the free-operation tables");
+static_assert(2 * (kEvalTableBase + kMaxTables * kTableBytes) <= 160 * 1024, "two workgroups per CU");
 // Two workgroups of 768 threads share a CU (2 x 64.3 KiB of LDS): six waves
 // per SIMD, which caps the kernel at 80 VGPRs.
 constexpr int kEvalBlock = 768;
@@ -97,42 +102,73 @@ __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &
     }
 }
 
-// Applies one gate's free operation to its destination label (in tgt):
+// The fast path over all words of the destination label: full words in a
+// loop, the last word peeled, each with its own constants.
+template <bool TAB>
+__device__ __forceinline__ void eval_fast(uint32_t d, const ModConst &mm, uint32_t (&V)[8], uint32_t (&row)[kMaxW],
+                                          uint32_t (&tgt)[kMaxW], uint32_t *dst, const LabelBufs &LB, uint32_t tk) {
+    const uint32_t coeff = gate_coeff(d);
+    const bool acc = gate_kind(d) != 0;
+#pragma unroll 1
+    for (uint32_t w = 0; w + 1 < mm.W; ++w) {
+        const uint32_t l = next_word(tgt);
+        const uint32_t D = frac_mul_carry(V, mm.pw_g);
+        const uint32_t rw = next_word(row);
+        LB.put(dst, w,
+               acc ? fast_word_any<true, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm, tk)
+                   : fast_word_any<false, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm,
+                                               tk));
+    }
+    const uint32_t l = tgt[0];
+    const uint32_t D = frac_mul_carry(V, mm.pw_last);
+    const uint32_t rw = row[0];
+    LB.put(dst, mm.W - 1,
+           acc ? fast_word_any<true, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm, tk)
+               : fast_word_any<false, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm,
+                                           tk));
+}
+
+// Applies gate g's free operation to its destination label (in tgt):
 // E = row + pad, then L <- c (L - E) (sub: division step and the recursion
 // of Eq. rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination
 // onto a scaling modulus), and stores the new label.
-__device__ __forceinline__ void eval_update(uint32_t d, const ModConst &mm, uint32_t (&V)[8], uint32_t (&row)[kMaxW],
-                                            uint32_t (&tgt)[kMaxW], const LabelBufs &LB) {
-    const uint32_t coeff = gate_coeff(d);
+__device__ __forceinline__ void eval_update(uint32_t g, uint32_t d, const ModConst &mm, uint32_t (&V)[8],
+                                            uint32_t (&row)[kMaxW], uint32_t (&tgt)[kMaxW], const LabelBufs &LB) {
     uint32_t *dst = LB.dest(gate_tdst(d), mm);
     if (mm.m == 2) {
-        const bool flip = gate_kind(d) == 0 || (coeff & 1u);  // sub: q^{-1} = 1 mod 2
+        const bool flip = gate_kind(d) == 0 || (gate_coeff(d) & 1u);  // sub: q^{-1} = 1 mod 2
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const uint32_t E = bits_word(V, w) ^ row[w];
             LB.put(dst, w, flip ? tgt[w] ^ E : tgt[w]);
         }
+    } else if (gate_tab(d)) {
+        // table address, plus 2m for a sub gate (its index is l + 2m - p - r)
+        const uint32_t tk = kEvalTableBase + g * kTableBytes + (gate_kind(d) ? 0u : mm.two_m);
+        eval_fast<true>(d, mm, V, row, tgt, dst, LB, tk);
     } else if (mm.fast) {
-        // full words in a loop, the last word peeled: each with its own
-        // constants, so no per-word selection
-        const bool acc = gate_kind(d) != 0;
-#pragma unroll 1
-        for (uint32_t w = 0; w + 1 < mm.W; ++w) {
-            const uint32_t l = next_word(tgt);
-            const uint32_t D = frac_mul_carry(V, mm.pw_g);
-            const uint32_t rw = next_word(row);
-            LB.put(dst, w,
-                   acc ? fast_word_any<true>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm)
-                       : fast_word_any<false>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm));
-        }
-        const uint32_t l = tgt[0];
-        const uint32_t D = frac_mul_carry(V, mm.pw_last);
-        const uint32_t rw = row[0];
-        LB.put(dst, mm.W - 1,
-               acc ? fast_word_any<true>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm)
-                   : fast_word_any<false>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm));
+        eval_fast<false>(d, mm, V, row, tgt, dst, LB, 0);
     } else {
         eval_update_generic(d, mm, V, row, tgt, LB);
+    }
+}
+
+// Fills the free-operation tables (gates 0..ntab-1 that have one): byte v of
+// gate g's table is c (v mod m) mod m.  Wave w fills gates w, w + waves, ...
+template <int BLOCK>
+__device__ __forceinline__ void stage_free_op_tables(const Plan &P, uint32_t *lds, int tid) {
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
+    const uint32_t lane = static_cast<uint32_t>(tid) % 64u;
+    for (uint32_t g = wave; g < P.ntab; g += BLOCK / 64) {
+        const uint32_t d = P.gate[g];
+        if (!gate_tab(d) || lane >= kTableBytes / 4) continue;
+        const uint32_t m = P.mod[gate_dst(d)].m, c = gate_coeff(d);
+        uint32_t w = 0;
+        for (uint32_t k = 0; k < 4; ++k) {
+            const uint32_t v = 4 * lane + k;
+            w |= ((c * (v % m)) % m) << (8 * k);
+        }
+        lds[(kEvalTableBase + g * kTableBytes) / 4 + lane] = w;
     }
 }
 
@@ -197,6 +233,7 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
     const int tid = threadIdx.x;
     stage_perm_te02(lds, tid, BLOCK);
     stage_hash_key(K, tid, BLOCK);
+    stage_free_op_tables<BLOCK>(P, lds, tid);
     __syncthreads();
     const PermTE02 TT = perm_te02();
     const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
@@ -221,7 +258,7 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
         for (uint32_t j = 0; j < len; ++j) {
             const uint32_t dj = P.gate[g + j];
             const ModConst mm = P.mod[gate_dst(dj)];
-            eval_update(dj, mm, V[0], row[0], tgt[0], LB);
+            eval_update(g + j, dj, mm, V[0], row[0], tgt[0], LB);
             static_for<kMaxChunk - 1>([&](auto k) {
                 static_for<8>([&](auto l) { V[k][l] = V[k + 1][l]; });
                 static_for<kMaxW>([&](auto w) {
@@ -635,10 +672,11 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     if (!d_in_labels || !d_tables || !d_out_labels || (P.work_words && !d_work)) return REDASH_E_NULL;
     size_t max_lds = 0;
     if ((rc = max_lds_bytes(&max_lds))) return rc;
-    if (kEvalLdsBytes > max_lds) return REDASH_E_HIP;
-    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), kEvalLdsBytes))) return rc;
-    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, kEvalBlock)), dim3(kEvalBlock), kEvalLdsBytes, stream,
-                       P, d_in_labels, d_tables, d_out_labels, d_work);
+    const uint32_t lds = eval_lds_bytes(P.ntab);
+    if (lds > max_lds) return REDASH_E_HIP;
+    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds))) return rc;
+    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, kEvalBlock)), dim3(kEvalBlock), lds, stream, P,
+                       d_in_labels, d_tables, d_out_labels, d_work);
     return launched();
 }
 
