@@ -27,9 +27,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 11810928.5,  # mean of two dispatches: 11,811,062 and 11,810,795
-        "write_kib": 790272.0,
-        "sources_sha256": "4acf219d57950bf14796bbd02330e74a17980c793ea965ce0cb9fee36b3b0f1b",
+        "fetch_kib": 15209159.5,  # mean of two dispatches: 15,208,225 and 15,210,094
+        "write_kib": 5048483.0,  # mean of 5,048,521 and 5,048,445
+        "sources_sha256": "0bbe7d589da7d044e13c47826824635ff90064e1a8d43fb1c1f54880f08fb588",
     },
 }
 
