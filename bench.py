@@ -74,6 +74,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decode check after timing")
+    ap.add_argument("--garble-steps", type=int, default=3,
+                    help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -114,12 +116,41 @@ def main():
     buf = B.Buffers(params, dev)
     stream = torch.cuda.current_stream()
     t0 = time.time()
-    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, stream)
+    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work, stream)
     xd = torch.from_numpy(x).to(dev)
     B.redash_encode(params, xd, buf.in_zero, buf.offsets, buf.in_labels, stream)
     torch.cuda.synchronize()
     log(f"garbled and encoded on the GPU in {time.time() - t0:.1f} s "
         f"({buf.sizes['table_words'] * 4 / 1e9:.1f} GB of tables)")
+
+    garble = None
+    if args.garble_steps > 0:
+        # The offline phase on the same buffers (deterministic: rewrites the same tables).
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(args.garble_steps):
+            B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work, stream)
+        g1.record(stream)
+        torch.cuda.synchronize()
+        g_ms = g0.elapsed_time(g1) / args.garble_steps
+        g_aes = cost.garble_aes_blocks_per_gadget(w.moduli, w.scale_idx)
+        g_ops = cost.garble_ops_per_gadget(w.moduli, w.scale_idx)
+        g_bytes = cost.garble_bytes_per_gadget(w.moduli, w.scale_idx)
+        g_tops = g_ops * n / (g_ms / 1e3) / 1e12
+        garble = {
+            "ms_per_call": round(g_ms, 3),
+            "gadgets_per_s": round(n / (g_ms / 1e3), 1),
+            "aes_blocks_per_s": round(g_aes * n / (g_ms / 1e3), 1),
+            "table_write_gbs": round(buf.sizes["table_words"] * 4 / (g_ms / 1e3) / 1e9, 1),
+            "roofline": {"bound": "alu", "achieved": round(g_tops, 3), "peak": round(ALU_PEAK_TOPS, 2),
+                         "unit": "TOP/s", "frac": round(g_tops / ALU_PEAK_TOPS, 4), "ops_per_gadget": g_ops,
+                         "kernel": "k_garble"},
+            "hbm": {"achieved": round(g_bytes * n / (g_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "bytes_per_gadget": g_bytes},
+            "steps": args.garble_steps,
+        }
+        log(f"garble: {g_ms:.3f} ms per call")
 
     for _ in range(args.warmup):
         B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
@@ -206,6 +237,7 @@ def main():
         },
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
         "check": check,
+        "garble": garble,
     }
     del buf
     torch.cuda.empty_cache()

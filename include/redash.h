@@ -126,12 +126,16 @@ int redash_plan(const redash_params *p, redash_sizes *out);
  *   d_offsets   offset_words: R_m for every modulus (R_m[0] != 0, so the k
  *               colours of a wire are distinct).
  *   d_in_zero   label_words: input zero-labels Z of gadgets a0..a0+n-1.
- *   d_out_zero  label_words: output zero-labels (value 0 after ShiftDown).
+ *   d_out_zero  label_words: output zero-labels (value 0 after ShiftDown);
+ *               also holds intermediate zero-labels while the call runs.
  *   d_tables    table_words: every garbled row (may be NULL when n = 0).
+ *   d_work      work_words of working storage, as for redash_eval_scale
+ *               (may be NULL when n = 0 or work_words = 0).
  * Deterministic in (moduli, scale set, seed, global gadget index).
+ * REDASH_E_PARAM also when n >= 2^30.
  */
 int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero,
-                        uint32_t *d_out_zero, uint32_t *d_tables, hipStream_t stream);
+                        uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work, hipStream_t stream);
 
 /*
  * Stand-in for the oblivious transfer of input labels (Sec. 2.1):

@@ -87,7 +87,7 @@ def lib() -> ctypes.CDLL:
         vp = ctypes.c_void_p
         pp = ctypes.POINTER(Params)
         L.redash_plan.argtypes = [pp, ctypes.POINTER(Sizes)]
-        L.redash_garble_scale.argtypes = [pp, vp, vp, vp, vp, vp]
+        L.redash_garble_scale.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_encode.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_eval_scale.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_decode.argtypes = [pp, vp, vp, vp, vp, vp, vp]
@@ -156,7 +156,7 @@ def plan_rc(params: Params) -> int:
     return lib().redash_plan(ctypes.byref(params), ctypes.byref(s))
 
 
-def redash_garble_scale(params, offsets, in_zero, out_zero, tables, stream=None):
+def redash_garble_scale(params, offsets, in_zero, out_zero, tables, work, stream=None):
     import torch
 
     sz = redash_plan(params)
@@ -164,7 +164,8 @@ def redash_garble_scale(params, offsets, in_zero, out_zero, tables, stream=None)
         ctypes.byref(params), _ptr(offsets, torch.int32, sz["offset_words"], "offsets"),
         _ptr(in_zero, torch.int32, sz["label_words"], "in_zero"),
         _ptr(out_zero, torch.int32, sz["label_words"], "out_zero"),
-        _ptr(tables, torch.int32, sz["table_words"], "tables"), _stream(stream)), "redash_garble_scale")
+        _ptr(tables, torch.int32, sz["table_words"], "tables"),
+        _ptr(work, torch.int32, sz["work_words"], "work"), _stream(stream)), "redash_garble_scale")
 
 
 def redash_encode(params, x, in_zero, offsets, in_labels, stream=None):

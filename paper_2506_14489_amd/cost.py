@@ -85,3 +85,38 @@ def lds_bytes_per_gadget(moduli, scale_idx) -> int:
 
 def table_bytes_per_gadget(moduli, scale_idx) -> int:
     return sum((q - 1) * 4 * words(m) for (q, m) in gates(moduli, scale_idx))
+
+
+# ---------------------------------------------------------------------------
+# Garbler (offline phase), per gadget instance:
+#   * AES-128 blocks: 2 per modulus for the input zero-label (PRG), and per
+#     gate q -> m one hash of each of the q input values (2 blocks, or 1 when
+#     m = 2);
+#   * HBM bytes written: the garbled rows, (q-1) W_m words per gate, plus
+#     the input and output zero-labels;
+#   * 32-bit vector-ALU operations: the AES work, per hash the fold and
+#     sigma (W_q + 1), per hashed value the pad (32 per output word for the
+#     limb multiply-adds when m > 2, 3 per word when m = 2) and the row or
+#     zero-label residues (OPS_PER_RESIDUE each), per value the step
+#     A_v -> A_v + R_q of the input label (3 per input residue), and per
+#     modulus the zero-label digits (32 per word + 3 per residue).
+# ---------------------------------------------------------------------------
+def garble_aes_blocks_per_gadget(moduli, scale_idx) -> int:
+    return 2 * len(moduli) + sum(q * (1 if m == 2 else 2) for (q, m) in gates(moduli, scale_idx))
+
+
+def garble_bytes_per_gadget(moduli, scale_idx) -> int:
+    return table_bytes_per_gadget(moduli, scale_idx) + 2 * sum(4 * words(m) for m in moduli)
+
+
+def garble_ops_per_gadget(moduli, scale_idx) -> int:
+    total = 2 * len(moduli) * AES_OPS_PER_BLOCK
+    total += sum(LIMB_OPS_PER_WORD * words(m) + 3 * lam(m) for m in moduli)
+    for (q, m) in gates(moduli, scale_idx):
+        per_value = (1 if m == 2 else 2) * AES_OPS_PER_BLOCK + words(q) + 1 + 3 * lam(q)
+        if m == 2:
+            per_value += 3 * words(m)
+        else:
+            per_value += LIMB_OPS_PER_WORD * words(m) + OPS_PER_RESIDUE * lam(m)
+        total += q * per_value
+    return total

@@ -496,6 +496,87 @@ __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uin
     }
 }
 
+// Garbler rows: for one packed word over Z_m (m > 2, fast constants), the
+// residues (b_j - p_j) mod m, where p_j are the word's pad digits held in D
+// as a base-m number (residue 0 the most significant digit) and b_j the
+// residues of the packed word bw.
+template <int NRES, int B>
+__device__ __forceinline__ uint32_t row_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo, uint32_t bw,
+                                               const ModConst &mc) {
+    constexpr int NLO = NRES / 2, NHI = NRES - NLO;
+    constexpr uint32_t MASK = (1u << B) - 1u;
+    const uint32_t m = uniform24(mc.m);
+    uint32_t hi = D, lo = 0;
+    if constexpr (NLO > 0) {
+        hi = __umulhi(D, lo_M) >> lo_s;
+        lo = D - mul24(hi, pw_lo);
+    }
+    uint32_t res = 0;
+    auto residue = [&](uint32_t p, auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const uint32_t d = ((bw >> (B * j)) & MASK) - p;
+        res |= umin(d, d + m) << (B * j);
+    };
+    uint32_t x = lo;
+    static_for<NLO>([&](auto k) {
+        constexpr int j = NRES - 1 - decltype(k)::value;
+        if constexpr (j > NHI) {
+            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
+            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
+            x = q;
+        } else {
+            residue(x, std::integral_constant<int, j>{});
+        }
+    });
+    x = hi;
+    static_for<NHI>([&](auto k) {
+        constexpr int j = NHI - 1 - decltype(k)::value;
+        if constexpr (j > 0) {
+            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
+            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
+            x = q;
+        } else {
+            residue(x, std::integral_constant<int, 0>{});
+        }
+    });
+    return res;
+}
+
+// row_word_c for any word shape; shapes outside the primes up to 37 take the
+// generic digit loop.
+__device__ __forceinline__ uint32_t row_word_any(uint32_t D, uint32_t nres, uint32_t lo_M, uint32_t lo_s,
+                                                 uint32_t pw_lo, uint32_t bw, const ModConst &mc) {
+    switch (nres | (mc.b << 8)) {
+#define REDASH_RW(NR, BB) \
+    case (NR) | ((BB) << 8): return row_word_c<NR, BB>(D, lo_M, lo_s, pw_lo, bw, mc);
+        REDASH_RW(16, 2) REDASH_RW(1, 2) REDASH_RW(10, 3) REDASH_RW(6, 3) REDASH_RW(8, 4) REDASH_RW(6, 4)
+        REDASH_RW(3, 4) REDASH_RW(6, 5) REDASH_RW(5, 5) REDASH_RW(3, 5) REDASH_RW(2, 5) REDASH_RW(1, 5)
+        REDASH_RW(5, 6)
+#undef REDASH_RW
+        default: {
+            uint32_t res = 0;
+            for (uint32_t j = nres; j-- > 0;) {
+                uint32_t p = D;
+                if (j) {
+                    const uint32_t q = div_m(D, mc);
+                    p = D - q * mc.m;
+                    D = q;
+                }
+                res |= sub_mod(field(bw, j, mc), p, mc.m) << (mc.b * j);
+            }
+            return res;
+        }
+    }
+}
+
+// (x + u) mod m residue by residue for one packed word (any m; m = 2 is XOR).
+__device__ __forceinline__ uint32_t word_add(uint32_t x, uint32_t u, uint32_t nres, const ModConst &mc) {
+    if (mc.m == 2) return x ^ u;
+    uint32_t out = 0;
+    for (uint32_t j = 0; j < nres; ++j) out |= add_mod(field(x, j, mc), field(u, j, mc), mc.m) << (mc.b * j);
+    return out;
+}
+
 // For m = 2 (128-bit fraction in V[0..3]) digit r is bit 127 - r of V, so
 // word w is the bit reversal of limb 3 - w.
 __device__ __forceinline__ uint32_t bits_word(const uint32_t (&V)[8], uint32_t w) {

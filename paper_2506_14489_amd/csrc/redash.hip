@@ -39,6 +39,10 @@ static_assert(2 * (kEvalTableBase + kMaxTables * kTableBytes) <= 160 * 1024, "tw
 // per SIMD, which caps the kernel at 80 VGPRs.
 constexpr int kEvalBlock = 768;
 constexpr int kEvalWaves = 6;
+// The garbler: the same LDS image without the free-operation tables; two
+// workgroups of 512 per CU, four waves per SIMD (up to 128 VGPRs).
+constexpr int kGarbleBlock = 512;
+constexpr int kGarbleWaves = 4;
 
 // The four places a label can be (kLocIn, kLocOut, kLocWork, kLocZero) for
 // one thread: word w of a label starts at base + (offset + w) n, and the
@@ -314,137 +318,261 @@ __device__ __forceinline__ uint32_t inverse_unit(uint32_t r, const ModConst &mc)
     return acc;
 }
 
+// The garbler's label access: like the evaluator's, except that a label read
+// from the input tensor (the input zero-labels Z) is taken as Z - (P/2 mod m) R,
+// the ShiftUp of Sec. 3.4 applied as a free constant addition.
+__device__ __forceinline__ void load_zero_label(const LabelBufs &LB, uint32_t loc, const ModConst &mc,
+                                                const uint32_t *__restrict__ offsets, uint32_t (&L)[kMaxW]) {
+    static_for<kMaxW>([&](auto w) { L[w] = 0; });
+    if (loc == kLocZero) return;
+    const uint32_t *p = LB.base(loc, mc);
+    const uint32_t neg_up = (mc.m - mc.up) % mc.m;
+    static_for<kMaxW>([&](auto w) {
+        if (w < static_cast<int>(mc.W)) {
+            L[w] = LB.get(p, w);
+            if (loc == kLocIn) L[w] = label_axpy(L[w], offsets[mc.woff + w], neg_up, w, mc);
+        }
+    });
+}
+
+// One garbled row over Z_m: (B - pad) word by word, pad the first lambda_m
+// base-m digits of the hash fraction V (consumed), stored at rp.
+__device__ __forceinline__ void store_row(uint32_t (&V)[8], const uint32_t (&B)[kMaxW], const ModConst &mm,
+                                          uint32_t *rp) {
+    if (mm.m == 2) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) rp[w] = B[w] ^ bits_word(V, w);
+        return;
+    }
+    uint32_t b[kMaxW];
+    static_for<kMaxW>([&](auto w) { b[w] = B[w]; });
+    if (mm.fast) {
+#pragma unroll 1
+        for (uint32_t w = 0; w + 1 < mm.W; ++w) {
+            const uint32_t D = frac_mul_carry(V, mm.pw_g);
+            rp[w] = row_word_any(D, mm.g, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, next_word(b), mm);
+        }
+        const uint32_t D = frac_mul_carry(V, mm.pw_last);
+        rp[mm.W - 1] = row_word_any(D, mm.glast, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, b[0], mm);
+    } else {
+#pragma unroll 1
+        for (uint32_t w = 0; w < mm.W; ++w) rp[w] = label_sub(next_word(b), pad_word(V, w, mm), w, mm);
+    }
+}
+
+// Hash fractions of two labels (folded into xa, xb) under the same tweak tau:
+// the four AES blocks run interleaved.
+__device__ __forceinline__ void hash_fraction_two(const PermTE02 &T, const LdsKey &rk, const uint32_t (&xa)[4],
+                                                  const uint32_t (&xb)[4], uint64_t tau, uint32_t gid,
+                                                  uint32_t (&Va)[8], uint32_t (&Vb)[8]) {
+    uint32_t u[2][4], s[4][4], k0[2], k1[2];
+    static_for<2>([&](auto j) {
+        const uint32_t(&x)[4] = j ? xb : xa;
+        u[j][0] = x[2];
+        u[j][1] = x[3];
+        u[j][2] = x[2] ^ x[0];
+        u[j][3] = x[3] ^ x[1];
+    });
+    static_for<2>([&](auto h) {
+        const uint64_t tw = tau * 4u + static_cast<uint64_t>(h);
+        k0[h] = static_cast<uint32_t>(tw);
+        k1[h] = static_cast<uint32_t>(tw >> 32);
+    });
+    static_for<2>([&](auto j) {
+        static_for<2>([&](auto h) {
+            s[2 * j + h][0] = u[j][0] ^ k0[h];
+            s[2 * j + h][1] = u[j][1] ^ k1[h];
+            s[2 * j + h][2] = u[j][2];
+            s[2 * j + h][3] = u[j][3] ^ gid;
+        });
+    });
+    aes128_encrypt_n<4>(T, s, rk);
+    static_for<2>([&](auto h) {
+        Va[4 * h + 0] = s[h][0] ^ u[0][0] ^ k0[h];
+        Va[4 * h + 1] = s[h][1] ^ u[0][1] ^ k1[h];
+        Va[4 * h + 2] = s[h][2] ^ u[0][2];
+        Va[4 * h + 3] = s[h][3] ^ u[0][3] ^ gid;
+        Vb[4 * h + 0] = s[2 + h][0] ^ u[1][0] ^ k0[h];
+        Vb[4 * h + 1] = s[2 + h][1] ^ u[1][1] ^ k1[h];
+        Vb[4 * h + 2] = s[2 + h][2] ^ u[1][2];
+        Vb[4 * h + 3] = s[2 + h][3] ^ u[1][3] ^ gid;
+    });
+}
+
+__device__ __forceinline__ void fold_label(const uint32_t (&A)[kMaxW], const ModConst &mq, uint32_t (&x)[4]) {
+    x[0] = A[0];
+    x[1] = x[2] = x[3] = 0;
+    static_for<kMaxW - 1>([&](auto w1) {
+        constexpr int w = decltype(w1)::value + 1;
+        if (w < static_cast<int>(mq.W)) x[w & 3] ^= A[w];
+    });
+}
+
+// A <- A + U residue by residue (U uniform).
+__device__ __forceinline__ void label_add(uint32_t (&A)[kMaxW], const uint32_t (&U)[kMaxW], const ModConst &mc) {
+    static_for<kMaxW>([&](auto w) {
+        if (w < static_cast<int>(mc.W)) A[w] = word_add(A[w], U[w], residues_in_word(w, mc), mc);
+    });
+}
+
+// Garbler (Sec. 2.3 projection gates with row reduction, the gadget of
+// Sec. 3.4 applied to zero-labels).  One thread per gadget; labels live
+// where the evaluator keeps them (zin read with the ShiftUp, zout, work).
+// Per gate q -> m the q labels of the digit wire are walked by colour:
+// colour c holds the value v_c = (c - c_0) R_q[0]^{-1} mod q, so the label
+// steps by the uniform label R_q[0]^{-1} R_q.  Colour 0 gives
+// B0 = H(A_{v_0}) - (v_0 mod m) R_m; colour c >= 1 gives the row
+// B0 + (v_c mod m) R_m - H(A_{v_c}), two colours per AES batch.  The walk
+// keeps B_c = B0 + (v_c mod m) R_m, starting from B_0 = H(A_{v_0}).
 template <int BLOCK>
-__global__ void __launch_bounds__(BLOCK) k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets,
-                                                  uint32_t *__restrict__ zin, uint32_t *__restrict__ zout,
-                                                  uint32_t *__restrict__ tab) {
+__global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kGarbleWaves, kGarbleWaves)))
+k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, uint32_t *zin, uint32_t *zout,
+         uint32_t *__restrict__ tab, uint32_t *work) {
     extern __shared__ uint32_t lds[];
-    uint32_t *TT = lds;
-    uint32_t *Rl = lds + kTableWords;                   // offsets, P.total_words
-    uint32_t *L = lds + kTableWords + P.total_words;    // [word][BLOCK]
+    uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    stage_round_tables(TT, tid, BLOCK);
-    for (uint32_t i = tid; i < P.total_words; i += BLOCK) Rl[i] = offsets[i];
+    stage_perm_te02(lds, tid, BLOCK);
+    stage_hash_key(K, tid, BLOCK);
     __syncthreads();
+    const PermTE02 TT = perm_te02();
+    const LdsKey HK{K};
     const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
     if (a >= P.n) return;  // no barrier follows
     const uint64_t n = P.n;
     const uint64_t ga = P.a0 + a;
+    const LabelBufs LB{zin, zout, work, n, static_cast<uint32_t>(a) * 4u};
 
-    // Input zero-labels Z (digits of rho(2, ga k + i)); the working labels
-    // start at Z - (P/2 mod m) R: the ShiftUp of Sec. 3.4 as a free constant
-    // addition on the garbler side.
+    // Input zero-labels Z: digits of rho(2, ga k + i) (Sec. 2.3 label sampling).
     for (uint32_t i = 0; i < P.k; ++i) {
-        const ModConst &mc = P.mod[i];
+        const ModConst mc = P.mod[i];
+        uint32_t s[1][4];
         uint32_t V[8];
-        prg_fraction(TT, key.w, 2u, ga * P.k + i, V);
-        uint32_t *dst = zin + static_cast<uint64_t>(mc.woff) * n + a;
-        const uint32_t neg_up = (mc.m - mc.up) % mc.m;
-        for (uint32_t w = 0; w < mc.W; ++w) {
-            const uint32_t z = prg_word(V, w, mc);
-            dst[static_cast<uint64_t>(w) * n] = z;
-            L[(mc.woff + w) * BLOCK + tid] = label_axpy(z, Rl[mc.woff + w], neg_up, w, mc);
-        }
+        static_for<2>([&](auto h) {
+            const uint64_t c = (ga * P.k + i) * 2u + static_cast<uint64_t>(h);
+            s[0][0] = static_cast<uint32_t>(c);
+            s[0][1] = static_cast<uint32_t>(c >> 32);
+            s[0][2] = 0;
+            s[0][3] = 2u << 24;
+            aes128_encrypt_n<1>(TT, s, ArgKey{key.w});
+            static_for<4>([&](auto l) { V[4 * h + l] = s[0][l]; });
+        });
+        uint32_t *dst = zin + static_cast<uint64_t>(mc.woff) * n;
+        for (uint32_t w = 0; w < mc.W; ++w) LB.put(dst, w, prg_word(V, w, mc));
     }
 
     const uint64_t tau0 = ga * P.G;
     uint64_t toff = 0;
-    bool phaseB = false;
     for (uint32_t g = 0; g < P.G; ++g) {
         const uint32_t d = P.gate[g];
-        if (gate_phase(d) && !phaseB) {
-            phaseB = true;
-            for (uint32_t b = 0; b < P.u; ++b) {  // R outputs, plus the ShiftDown constant
-                const ModConst &mc = P.mod[P.R[b]];
-                uint32_t *dst = zout + static_cast<uint64_t>(mc.woff) * n + a;
-                for (uint32_t w = 0; w < mc.W; ++w)
-                    dst[static_cast<uint64_t>(w) * n] =
-                        label_axpy(L[(mc.woff + w) * BLOCK + tid], Rl[mc.woff + w], mc.down, w, mc);
-            }
-            for (uint32_t s = 0; s < P.t; ++s) {
-                const ModConst &mc = P.mod[P.S[s]];
-                for (uint32_t w = 0; w < mc.W; ++w) L[(mc.woff + w) * BLOCK + tid] = 0;
-            }
-        }
-        const ModConst &mq = P.mod[gate_src(d)];
-        const ModConst &mm = P.mod[gate_dst(d)];
-        const uint32_t q = mq.m;
-        const uint32_t *Rq = Rl + mq.woff;
-        const uint32_t *Rm = Rl + mm.woff;
-        uint32_t A0[kMaxW];
-#pragma unroll
-        for (int w = 0; w < kMaxW; ++w) A0[w] = (w < static_cast<int>(mq.W)) ? L[(mq.woff + w) * BLOCK + tid] : 0u;
-        const uint32_t c0 = A0[0] & mq.mask;
-        const uint32_t rq0 = Rq[0] & mq.mask;
-        const uint32_t rinv = inverse_unit(rq0, mq);
-        // v0: the value whose label has colour 0.
-        const uint32_t v0 = mul_mod((q - c0) % q, rinv, mq);
+        const ModConst mq = P.mod[gate_src(d)];
+        const ModConst mm = P.mod[gate_dst(d)];
+        const uint32_t q = mq.m, m = mm.m;
+        uint32_t Rq[kMaxW], Rm[kMaxW];
+        static_for<kMaxW>([&](auto w) {
+            Rq[w] = w < static_cast<int>(mq.W) ? offsets[mq.woff + w] : 0u;
+            Rm[w] = w < static_cast<int>(mm.W) ? offsets[mm.woff + w] : 0u;
+        });
+        uint32_t A[kMaxW], T[kMaxW];
+        load_zero_label(LB, gate_dsrc(d), mq, offsets, A);
+        load_zero_label(LB, gate_tsrc(d), mm, offsets, T);
+        const uint32_t rinv = inverse_unit(Rq[0] & mq.mask, mq);
+        // v: the value of colour 0; A <- A0 + v R_q
+        uint32_t v = mul_mod((q - (A[0] & mq.mask)) % q, rinv, mq);
+        static_for<kMaxW>([&](auto w) {
+            if (w < static_cast<int>(mq.W)) A[w] = label_axpy(A[w], Rq[w], v, w, mq);
+        });
+        // uniform steps: the input label by rinv R_q, the output label by
+        // (rinv mod m) R_m, or ((rinv - q) mod m) R_m when v wraps past q
+        const uint32_t s1 = rinv % m, s2 = (rinv % m + m - q % m) % m;
+        uint32_t Rs[kMaxW], U1[kMaxW], U2[kMaxW];
+        static_for<kMaxW>([&](auto w) {
+            Rs[w] = w < static_cast<int>(mq.W) ? label_axpy(0u, Rq[w], rinv, w, mq) : 0u;
+            U1[w] = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s1, w, mm) : 0u;
+            U2[w] = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s2, w, mm) : 0u;
+        });
         const uint64_t tau = tau0 + g;
 
-        // B0 = H(A0 + v0 Rq) - (v0 mod m) Rm   (row reduction)
-        uint32_t B0[kMaxW];
+        // colour 0: the pad H(A_v0) starts the walk B_c = B0 + (v_c mod m) R_m,
+        // with B0 = H(A_v0) - (v0 mod m) R_m (row reduction: no row stored)
+        uint32_t B[kMaxW];
         {
-            uint32_t Av[kMaxW];
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w)
-                Av[w] = (w < static_cast<int>(mq.W)) ? label_axpy(A0[w], Rq[w], v0, w, mq) : 0u;
-            uint32_t x[4] = {0, 0, 0, 0};
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w) x[w & 3] ^= Av[w];
-            uint32_t V[8];
-            hash_fraction(TT, x[0], x[1], x[2], x[3], tau, P.gid, mm.m != 2, V);
-            const uint32_t negv = (mm.m - v0 % mm.m) % mm.m;
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w)
-                B0[w] = (w < static_cast<int>(mm.W)) ? label_axpy(pad_word(V, w, mm), Rm[w], negv, w, mm) : 0u;
-        }
-        // Rows: for every v != v0, row[colour(A0 + v Rq)] = B0 + (v mod m) Rm - H(A0 + v Rq).
-        uint32_t Av[kMaxW];
-#pragma unroll
-        for (int w = 0; w < kMaxW; ++w) Av[w] = A0[w];
-        const uint64_t gate_base = toff + a * (q - 1) * mm.W;
-        for (uint32_t v = 0; v < q; ++v) {
-            const uint32_t c = Av[0] & mq.mask;
-            if (v != v0 && c != 0) {  // c != 0 holds for every v != v0 since R_q[0] is a unit
-                uint32_t x[4] = {0, 0, 0, 0};
-#pragma unroll
-                for (int w = 0; w < kMaxW; ++w) x[w & 3] ^= Av[w];
-                uint32_t V[8];
-                hash_fraction(TT, x[0], x[1], x[2], x[3], tau, P.gid, mm.m != 2, V);
-                uint32_t *rp = tab + gate_base + static_cast<uint64_t>(c - 1) * mm.W;
-                const uint32_t vm = v % mm.m;
-#pragma unroll
-                for (int w = 0; w < kMaxW; ++w) {
-                    if (w < static_cast<int>(mm.W)) {
-                        const uint32_t h = pad_word(V, w, mm);
-                        rp[w] = label_sub(label_axpy(B0[w], Rm[w], vm, w, mm), h, w, mm);
-                    }
-                }
+            uint32_t x[4], V0[1][8];
+            fold_label(A, mq, x);
+            hash_fraction_n<1>(TT, HK, x[0], x[1], x[2], x[3], tau, P.gid, V0);
+            static_for<kMaxW>([&](auto w) { B[w] = 0; });
+#pragma unroll 1
+            for (uint32_t w = 0; w < mm.W; ++w) {
+                const uint32_t pw = pad_word(V0[0], w, mm);
+                static_for<kMaxW>([&](auto ww) {
+                    if (ww == static_cast<int>(w)) B[ww] = pw;
+                });
             }
-#pragma unroll
-            for (int w = 0; w < kMaxW; ++w)
-                if (w < static_cast<int>(mq.W)) Av[w] = label_axpy(Av[w], Rq[w], 1u, w, mq);
+        }
+        // The free operation on the destination zero-label, as the evaluator
+        // applies it to labels (E replaced by B0).
+        {
+            const uint32_t coeff = gate_coeff(d);
+            const uint32_t negv = (m - v % m) % m;
+            uint32_t *dst = LB.dest(gate_tdst(d), mm);
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(mm.W)) {
+                    const uint32_t b0 = label_axpy(B[w], Rm[w], negv, w, mm);
+                    LB.put(dst, w,
+                           gate_kind(d) == 0 ? label_scaled_sub(T[w], b0, coeff, w, mm)
+                                             : label_axpy(T[w], b0, coeff, w, mm));
+                }
+            });
+        }
+        // colours 1..q-1, two per AES batch
+        uint32_t *gate_rows = tab + toff + a * (q - 1) * mm.W;
+        auto step = [&](uint32_t(&Ax)[kMaxW], uint32_t(&Bx)[kMaxW], uint32_t &vx) {
+            label_add(Ax, Rs, mq);
+            const uint32_t vn = vx + rinv;
+            const bool wrap = vn >= q;
+            vx = wrap ? vn - q : vn;
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(mm.W))
+                    Bx[w] = word_add(Bx[w], wrap ? U2[w] : U1[w], residues_in_word(w, mm), mm);
+            });
+        };
+#pragma unroll 1
+        for (uint32_t c = 1; c < q; c += 2) {
+            step(A, B, v);
+            if (c + 1 < q) {
+                uint32_t A2[kMaxW], B2[kMaxW];
+                uint32_t v2 = v;
+                static_for<kMaxW>([&](auto w) {
+                    A2[w] = A[w];
+                    B2[w] = B[w];
+                });
+                step(A2, B2, v2);
+                uint32_t xa[4], xb[4], Va[8], Vb[8];
+                fold_label(A, mq, xa);
+                fold_label(A2, mq, xb);
+                hash_fraction_two(TT, HK, xa, xb, tau, P.gid, Va, Vb);
+                store_row(Va, B, mm, gate_rows + (c - 1) * mm.W);
+                store_row(Vb, B2, mm, gate_rows + c * mm.W);
+                static_for<kMaxW>([&](auto w) {
+                    A[w] = A2[w];
+                    B[w] = B2[w];
+                });
+                v = v2;
+            } else {
+                uint32_t x[4], V1[1][8];
+                fold_label(A, mq, x);
+                hash_fraction_n<1>(TT, HK, x[0], x[1], x[2], x[3], tau, P.gid, V1);
+                store_row(V1[0], B, mm, gate_rows + (c - 1) * mm.W);
+            }
         }
         toff += n * (q - 1) * mm.W;
-
-        // The same free operation on zero-labels that the evaluator applies.
-        const uint32_t coeff = gate_coeff(d);
-        for (uint32_t w = 0; w < mm.W; ++w) {
-            uint32_t l = L[(mm.woff + w) * BLOCK + tid];
-            uint32_t b0 = 0;
-#pragma unroll
-            for (int ww = 0; ww < kMaxW; ++ww)
-                if (ww == static_cast<int>(w)) b0 = B0[ww];
-            l = gate_kind(d) == 0 ? label_scaled_sub(l, b0, coeff, w, mm) : label_axpy(l, b0, coeff, w, mm);
-            L[(mm.woff + w) * BLOCK + tid] = l;
-        }
     }
-    for (uint32_t s = 0; s < P.t; ++s) {  // S outputs, plus the ShiftDown constant
-        const ModConst &mc = P.mod[P.S[s]];
-        uint32_t *dst = zout + static_cast<uint64_t>(mc.woff) * n + a;
+    // Output zero-labels: the working labels plus (P/(2s) mod m) R, the
+    // ShiftDown of Sec. 3.4.
+    for (uint32_t i = 0; i < P.k; ++i) {
+        const ModConst mc = P.mod[i];
+        uint32_t *p = zout + static_cast<uint64_t>(mc.woff) * n;
         for (uint32_t w = 0; w < mc.W; ++w)
-            dst[static_cast<uint64_t>(w) * n] =
-                label_axpy(L[(mc.woff + w) * BLOCK + tid], Rl[mc.woff + w], mc.down, w, mc);
+            LB.put(p, w, label_axpy(LB.get(p, w), offsets[mc.woff + w], mc.down, w, mc));
     }
 }
 
@@ -555,10 +683,6 @@ __global__ void __launch_bounds__(BLOCK) k_hash(const ModConst mq, const ModCons
 // ---------------------------------------------------------------------------
 namespace {
 
-size_t garble_lds_bytes(const Plan &P, int block) {
-    return (static_cast<size_t>(kTableWords) + P.total_words + static_cast<size_t>(P.total_words) * block) * 4;
-}
-
 // Largest LDS allocation a block may request on the current device.
 int max_lds_bytes(size_t *out) {
     int dev = 0, v = 0;
@@ -581,19 +705,6 @@ unsigned grid_for(uint64_t n, int block) { return static_cast<unsigned>((n + blo
 
 int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
-}
-
-template <int BLOCK>
-int try_garble(const Plan &P, size_t max_lds, const SeedKey &key, const uint32_t *offsets, uint32_t *zin,
-               uint32_t *zout, uint32_t *tab, hipStream_t stream, bool *done) {
-    const size_t lds = garble_lds_bytes(P, BLOCK);
-    if (*done || lds > max_lds) return REDASH_OK;
-    *done = true;
-    int rc = allow_lds(reinterpret_cast<const void *>(&k_garble<BLOCK>), lds);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_garble<BLOCK>, dim3(grid_for(P.n, BLOCK)), dim3(BLOCK), lds, stream, P, key, offsets, zin,
-                       zout, tab);
-    return launched();
 }
 
 SeedKey seed_key(uint64_t seed) {
@@ -630,23 +741,25 @@ int redash_plan(const redash_params *p, redash_sizes *out) {
 }
 
 int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero, uint32_t *d_out_zero,
-                        uint32_t *d_tables, hipStream_t stream) {
+                        uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
     Plan P;
     int rc = build_plan(p, &P);
     if (rc) return rc;
+    if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
     if (!d_offsets) return REDASH_E_NULL;
-    if (P.n > 0 && (!d_in_zero || !d_out_zero || !d_tables)) return REDASH_E_NULL;
+    if (P.n > 0 && (!d_in_zero || !d_out_zero || !d_tables || (P.work_words && !d_work))) return REDASH_E_NULL;
     const SeedKey key = seed_key(P.seed);
     hipLaunchKernelGGL(k_offsets, dim3(1), dim3(64), 0, stream, P, key, d_offsets);
     if ((rc = launched())) return rc;
     if (P.n == 0) return REDASH_OK;
     size_t max_lds = 0;
     if ((rc = max_lds_bytes(&max_lds))) return rc;
-    bool done = false;
-    if ((rc = try_garble<256>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
-    if ((rc = try_garble<128>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
-    if ((rc = try_garble<64>(P, max_lds, key, d_offsets, d_in_zero, d_out_zero, d_tables, stream, &done))) return rc;
-    return done ? REDASH_OK : REDASH_E_PARAM;
+    const uint32_t lds = kEvalTableBase;  // the AES image and the round keys
+    if (lds > max_lds) return REDASH_E_HIP;
+    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_garble<kGarbleBlock>), lds))) return rc;
+    hipLaunchKernelGGL(k_garble<kGarbleBlock>, dim3(grid_for(P.n, kGarbleBlock)), dim3(kGarbleBlock), lds, stream, P,
+                       key, d_offsets, d_in_zero, d_out_zero, d_tables, d_work);
+    return launched();
 }
 
 int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_in_zero, const uint32_t *d_offsets,

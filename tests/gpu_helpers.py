@@ -72,7 +72,7 @@ def to_dev(a: np.ndarray, device="cuda") -> torch.Tensor:
 def gpu_pipeline(params, x: np.ndarray, device="cuda"):
     """Garble, encode, evaluate and decode on the GPU.  Returns the Buffers."""
     buf = B.Buffers(params, device)
-    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables)
+    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work)
     xd = torch.from_numpy(np.ascontiguousarray(x, dtype=np.int64)).to(device)
     B.redash_encode(params, xd, buf.in_zero, buf.offsets, buf.in_labels)
     B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work)

@@ -128,7 +128,7 @@ def test_entry_points_validate_before_any_device_work():
     good = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 4, 0)
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below returns early
     assert L.redash_eval_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
-    assert L.redash_garble_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_garble_scale(ctypes.byref(bad), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_encode(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_decode(ctypes.byref(bad), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_eval_scale(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
@@ -137,8 +137,10 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_eval_scale(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
     huge = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 1 << 30, 0)
     assert L.redash_eval_scale(ctypes.byref(huge), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
-    assert L.redash_garble_scale(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
-    assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(good), None, fake, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale(ctypes.byref(huge), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_encode(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_decode(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
     assert L.redash_hash_labels(4, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM

@@ -98,7 +98,7 @@ def test_garble_matches_oracle(case):
     name, moduli, S, n, seed, a0 = case
     bp, op = _params_pair(moduli, S, n, seed, a0)
     buf = B.Buffers(bp)
-    B.redash_garble_scale(bp, buf.offsets, buf.in_zero, buf.out_zero, buf.tables)
+    B.redash_garble_scale(bp, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work)
     torch.cuda.synchronize()
     offs, zin, zout, tab = O.garble(op, a0, n)
     assert np.array_equal(H.to_u32(buf.offsets), offs)
@@ -189,7 +189,7 @@ def test_empty_calls_are_noops():
     assert sz["label_words"] == 0 and sz["table_words"] == 0
     offs = torch.empty(sz["offset_words"], dtype=torch.int32, device="cuda")
     e = torch.empty(1, dtype=torch.int32, device="cuda")
-    B.redash_garble_scale(bp, offs, e, e, e)
+    B.redash_garble_scale(bp, offs, e, e, e, e)
     B.redash_eval_scale(bp, e, e, e, e)
     bad = torch.full((1,), 7, dtype=torch.int64, device="cuda")
     B.redash_decode(bp, e, e, offs, torch.empty(1, dtype=torch.int64, device="cuda"), bad)
