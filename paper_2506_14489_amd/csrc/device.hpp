@@ -569,6 +569,19 @@ __device__ __forceinline__ uint32_t row_word_any(uint32_t D, uint32_t nres, uint
     }
 }
 
+// (x + u) mod m in every field of one packed word (m > 2) at once, with u
+// given as its even fields ue and its odd fields shifted down, uo (see
+// ModConst::sw_even): sums of two residues stay below 2m <= 2^(b+1) in a
+// field with b free bits above it, adding 2^b - m sets bit b exactly where
+// the sum is at least m, and m times that bit is subtracted.
+__device__ __forceinline__ uint32_t swar_add(uint32_t x, uint32_t ue, uint32_t uo, const ModConst &mc) {
+    const uint32_t se = (x & mc.sw_even) + ue;
+    const uint32_t so = ((x >> mc.b) & mc.sw_even) + uo;
+    const uint32_t ce = ((se + mc.sw_k) >> mc.b) & mc.sw_ones;
+    const uint32_t co = ((so + mc.sw_k) >> mc.b) & mc.sw_ones;
+    return (se - ce * mc.m) | ((so - co * mc.m) << mc.b);
+}
+
 // (x + u) mod m residue by residue for one packed word (any m; m = 2 is XOR).
 __device__ __forceinline__ uint32_t word_add(uint32_t x, uint32_t u, uint32_t nres, const ModConst &mc) {
     if (mc.m == 2) return x ^ u;

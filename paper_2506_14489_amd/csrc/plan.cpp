@@ -126,6 +126,11 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     division_constants(m, bound, &mc->divM, &mc->divS, &mc->div_fix);
 
     if (m == 2) return;  // labels over Z_2 are bit vectors; no fast path needed
+    for (uint32_t f = 0; f < mc->g; f += 2) {
+        mc->sw_even |= mc->mask << (mc->b * f);
+        mc->sw_ones |= 1u << (mc->b * f);
+        mc->sw_k |= ((1u << mc->b) - m) << (mc->b * f);
+    }
     mc->two_m = 2 * m;
     bool ok = mul24_constants(m, 3 * sq, &mc->red_M, &mc->red_s);
     uint64_t part = 1;

@@ -52,6 +52,11 @@ struct ModConst {
     // Word offset of this modulus in the evaluator's working storage (only
     // the remaining moduli R[1..u-1] have one: their Phase-B copies).
     uint32_t wkoff;
+    // Packed addition mod m in one word (m > 2): the even fields (0, 2, 4,
+    // ...) of x, in place, and the odd fields shifted down by b, each have
+    // b free bits above them.  sw_even masks the even fields, sw_ones has
+    // bit 0 of each even field, sw_k holds 2^b - m in each even field.
+    uint32_t sw_even, sw_ones, sw_k;
 };
 
 // Gate descriptor packed in one word:

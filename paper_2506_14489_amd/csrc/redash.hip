@@ -408,13 +408,6 @@ __device__ __forceinline__ void fold_label(const uint32_t (&A)[kMaxW], const Mod
     });
 }
 
-// A <- A + U residue by residue (U uniform).
-__device__ __forceinline__ void label_add(uint32_t (&A)[kMaxW], const uint32_t (&U)[kMaxW], const ModConst &mc) {
-    static_for<kMaxW>([&](auto w) {
-        if (w < static_cast<int>(mc.W)) A[w] = word_add(A[w], U[w], residues_in_word(w, mc), mc);
-    });
-}
-
 // Garbler (Sec. 2.3 projection gates with row reduction, the gadget of
 // Sec. 3.4 applied to zero-labels).  One thread per gadget; labels live
 // where the evaluator keeps them (zin read with the ShiftUp, zout, work).
@@ -483,12 +476,19 @@ k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, 
         });
         // uniform steps: the input label by rinv R_q, the output label by
         // (rinv mod m) R_m, or ((rinv - q) mod m) R_m when v wraps past q
+        // (split into even and odd fields for swar_add; m = 2 steps by XOR)
         const uint32_t s1 = rinv % m, s2 = (rinv % m + m - q % m) % m;
-        uint32_t Rs[kMaxW], U1[kMaxW], U2[kMaxW];
+        uint32_t Rse[kMaxW], Rso[kMaxW], U1e[kMaxW], U1o[kMaxW], U2e[kMaxW], U2o[kMaxW];
         static_for<kMaxW>([&](auto w) {
-            Rs[w] = w < static_cast<int>(mq.W) ? label_axpy(0u, Rq[w], rinv, w, mq) : 0u;
-            U1[w] = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s1, w, mm) : 0u;
-            U2[w] = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s2, w, mm) : 0u;
+            const uint32_t rs = w < static_cast<int>(mq.W) ? label_axpy(0u, Rq[w], rinv, w, mq) : 0u;
+            const uint32_t u1 = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s1, w, mm) : 0u;
+            const uint32_t u2 = w < static_cast<int>(mm.W) ? label_axpy(0u, Rm[w], s2, w, mm) : 0u;
+            Rse[w] = q == 2 ? rs : rs & mq.sw_even;
+            Rso[w] = (rs >> mq.b) & mq.sw_even;
+            U1e[w] = m == 2 ? u1 : u1 & mm.sw_even;
+            U1o[w] = (u1 >> mm.b) & mm.sw_even;
+            U2e[w] = m == 2 ? u2 : u2 & mm.sw_even;
+            U2o[w] = (u2 >> mm.b) & mm.sw_even;
         });
         const uint64_t tau = tau0 + g;
 
@@ -526,13 +526,16 @@ k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, 
         // colours 1..q-1, two per AES batch
         uint32_t *gate_rows = tab + toff + a * (q - 1) * mm.W;
         auto step = [&](uint32_t(&Ax)[kMaxW], uint32_t(&Bx)[kMaxW], uint32_t &vx) {
-            label_add(Ax, Rs, mq);
+            static_for<kMaxW>([&](auto w) {
+                if (w < static_cast<int>(mq.W)) Ax[w] = q == 2 ? Ax[w] ^ Rse[w] : swar_add(Ax[w], Rse[w], Rso[w], mq);
+            });
             const uint32_t vn = vx + rinv;
             const bool wrap = vn >= q;
             vx = wrap ? vn - q : vn;
             static_for<kMaxW>([&](auto w) {
                 if (w < static_cast<int>(mm.W))
-                    Bx[w] = word_add(Bx[w], wrap ? U2[w] : U1[w], residues_in_word(w, mm), mm);
+                    Bx[w] = m == 2 ? Bx[w] ^ (wrap ? U2e[w] : U1e[w])
+                                   : swar_add(Bx[w], wrap ? U2e[w] : U1e[w], wrap ? U2o[w] : U1o[w], mm);
             });
         };
 #pragma unroll 1
