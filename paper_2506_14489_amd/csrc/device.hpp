@@ -410,16 +410,36 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_
     return res;
 }
 
+// The ND base-m digits of x < m^ND (with (m^ND)^2 < 2^32), most significant
+// first, handed to f(digit, integral_constant<J0 + k>) for k = 0..ND-1:
+// F = x C mod 2^32 with C = floor(2^32 / m^ND) + 1 approximates the fraction
+// x / m^ND from above by less than 2^-32 x, so each umulhi(F, m) is the next
+// digit exactly, and F m mod 2^32 the remaining fraction.
+template <int ND, int J0, typename Fn>
+__device__ __forceinline__ void frac_digits(uint32_t x, uint32_t C, uint32_t m, Fn &&f) {
+    if constexpr (ND > 0) {
+        uint32_t F = x * C;
+        static_for<ND>([&](auto k) {
+            constexpr int kk = decltype(k)::value;
+            f(__umulhi(F, m), std::integral_constant<int, J0 + kk>{});
+            if constexpr (kk + 1 < ND) F *= m;
+        });
+    }
+}
+
 // fast_word with the residue count and field width known at compile time:
 // every loop unrolled, every shift an immediate.
 //
 // With TAB, the product c (v mod m) mod m comes from the gate's byte table in
 // LDS (v < 3m, see free_op_table): tk is the table's LDS address, plus 2m for
 // a sub gate, so the sub gate's byte address is lj + tk - p - r.
+//
+// The digits of each part come from fraction multiplication (ModConst::fd):
+// two full-rate multiplies per digit instead of a division step.
 template <bool ACC, int NRES, int B, bool TAB>
 __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo,
-                                                uint32_t rw, uint32_t l, uint32_t c, const ModConst &mc,
-                                                uint32_t tk) {
+                                                uint32_t c_hi, uint32_t c_lo, uint32_t rw, uint32_t l, uint32_t c,
+                                                const ModConst &mc, uint32_t tk) {
     constexpr int NLO = NRES / 2, NHI = NRES - NLO;
     constexpr uint32_t MASK = (1u << B) - 1u;
     const uint32_t m = uniform24(mc.m);
@@ -453,29 +473,9 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
             res |= opaque(v - mul24(q, m)) << (B * j);
         }
     };
-    // low part: positions NRES-1 down to NHI; high part: NHI-1 down to 0
-    uint32_t x = lo;
-    static_for<NLO>([&](auto k) {
-        constexpr int j = NRES - 1 - decltype(k)::value;
-        if constexpr (j > NHI) {
-            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
-            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
-            x = q;
-        } else {
-            residue(x, std::integral_constant<int, j>{});
-        }
-    });
-    x = hi;
-    static_for<NHI>([&](auto k) {
-        constexpr int j = NHI - 1 - decltype(k)::value;
-        if constexpr (j > 0) {
-            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
-            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
-            x = q;
-        } else {
-            residue(x, std::integral_constant<int, 0>{});
-        }
-    });
+    // high part: residues 0..NHI-1; low part: NHI..NRES-1 (most significant first)
+    frac_digits<NHI, 0>(hi, c_hi, mc.m, residue);
+    frac_digits<NLO, NHI>(lo, c_lo, mc.m, residue);
     return res;
 }
 
@@ -483,11 +483,14 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
 // of the primes up to 37 are unrolled, anything else takes the loops.
 template <bool ACC, bool TAB>
 __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uint32_t nlo, uint32_t lo_M,
-                                                  uint32_t lo_s, uint32_t pw_lo, uint32_t rw, uint32_t l, uint32_t c,
-                                                  const ModConst &mc, uint32_t tk) {
+                                                  uint32_t lo_s, uint32_t pw_lo, uint32_t c_hi, uint32_t c_lo,
+                                                  uint32_t rw, uint32_t l, uint32_t c, const ModConst &mc,
+                                                  uint32_t tk) {
+    if (!mc.fd) return fast_word<ACC>(D, nres, nlo, lo_M, lo_s, pw_lo, rw, l, c, mc);
     switch (nres | (mc.b << 8)) {
-#define REDASH_FW(NR, BB) \
-    case (NR) | ((BB) << 8): return fast_word_c<ACC, NR, BB, TAB>(D, lo_M, lo_s, pw_lo, rw, l, c, mc, tk);
+#define REDASH_FW(NR, BB)        \
+    case (NR) | ((BB) << 8): \
+        return fast_word_c<ACC, NR, BB, TAB>(D, lo_M, lo_s, pw_lo, c_hi, c_lo, rw, l, c, mc, tk);
         REDASH_FW(16, 2) REDASH_FW(1, 2) REDASH_FW(10, 3) REDASH_FW(6, 3) REDASH_FW(8, 4) REDASH_FW(6, 4)
         REDASH_FW(3, 4) REDASH_FW(6, 5) REDASH_FW(5, 5) REDASH_FW(3, 5) REDASH_FW(2, 5) REDASH_FW(1, 5)
         REDASH_FW(5, 6)
@@ -501,8 +504,8 @@ __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uin
 // as a base-m number (residue 0 the most significant digit) and b_j the
 // residues of the packed word bw.
 template <int NRES, int B>
-__device__ __forceinline__ uint32_t row_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo, uint32_t bw,
-                                               const ModConst &mc) {
+__device__ __forceinline__ uint32_t row_word_c(uint32_t D, uint32_t lo_M, uint32_t lo_s, uint32_t pw_lo, uint32_t c_hi,
+                                               uint32_t c_lo, uint32_t bw, const ModConst &mc) {
     constexpr int NLO = NRES / 2, NHI = NRES - NLO;
     constexpr uint32_t MASK = (1u << B) - 1u;
     const uint32_t m = uniform24(mc.m);
@@ -517,38 +520,19 @@ __device__ __forceinline__ uint32_t row_word_c(uint32_t D, uint32_t lo_M, uint32
         const uint32_t d = ((bw >> (B * j)) & MASK) - p;
         res |= umin(d, d + m) << (B * j);
     };
-    uint32_t x = lo;
-    static_for<NLO>([&](auto k) {
-        constexpr int j = NRES - 1 - decltype(k)::value;
-        if constexpr (j > NHI) {
-            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
-            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
-            x = q;
-        } else {
-            residue(x, std::integral_constant<int, j>{});
-        }
-    });
-    x = hi;
-    static_for<NHI>([&](auto k) {
-        constexpr int j = NHI - 1 - decltype(k)::value;
-        if constexpr (j > 0) {
-            const uint32_t q = __builtin_amdgcn_ubfe(mul24(x, mc.sd_M), mc.sd_s, 24);
-            residue(opaque(x - mul24(q, m)), std::integral_constant<int, j>{});
-            x = q;
-        } else {
-            residue(x, std::integral_constant<int, 0>{});
-        }
-    });
+    frac_digits<NHI, 0>(hi, c_hi, mc.m, residue);
+    frac_digits<NLO, NHI>(lo, c_lo, mc.m, residue);
     return res;
 }
 
 // row_word_c for any word shape; shapes outside the primes up to 37 take the
 // generic digit loop.
 __device__ __forceinline__ uint32_t row_word_any(uint32_t D, uint32_t nres, uint32_t lo_M, uint32_t lo_s,
-                                                 uint32_t pw_lo, uint32_t bw, const ModConst &mc) {
-    switch (nres | (mc.b << 8)) {
+                                                 uint32_t pw_lo, uint32_t c_hi, uint32_t c_lo, uint32_t bw,
+                                                 const ModConst &mc) {
+    switch (mc.fd ? nres | (mc.b << 8) : 0u) {
 #define REDASH_RW(NR, BB) \
-    case (NR) | ((BB) << 8): return row_word_c<NR, BB>(D, lo_M, lo_s, pw_lo, bw, mc);
+    case (NR) | ((BB) << 8): return row_word_c<NR, BB>(D, lo_M, lo_s, pw_lo, c_hi, c_lo, bw, mc);
         REDASH_RW(16, 2) REDASH_RW(1, 2) REDASH_RW(10, 3) REDASH_RW(6, 3) REDASH_RW(8, 4) REDASH_RW(6, 4)
         REDASH_RW(3, 4) REDASH_RW(6, 5) REDASH_RW(5, 5) REDASH_RW(3, 5) REDASH_RW(2, 5) REDASH_RW(1, 5)
         REDASH_RW(5, 6)

@@ -158,6 +158,21 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     // (the split's parts also feed signed 24-bit multiply-adds: below 2^23)
     ok = ok && mul24_constants(m, part, &mc->sd_M, &mc->sd_s) && part < (1u << 23);
     mc->fast = ok ? 1u : 0u;
+    // fraction-multiplication digits: exact while (m^n)^2 < 2^32
+    mc->fd = (static_cast<uint64_t>(part) * part < (1ull << 32)) ? 1u : 0u;
+    auto frac_mult = [](uint64_t M) { return M > 1 ? static_cast<uint32_t>((1ull << 32) / M + 1) : 0u; };
+    for (int k = 0; k < 2; ++k) {
+        const uint32_t nres = k ? mc->glast : mc->g;
+        const uint32_t nlo = nres / 2, nhi = nres - nlo;
+        const uint32_t chi = frac_mult(ipow(m, nhi)), clo = frac_mult(ipow(m, nlo));
+        if (k) {
+            mc->fc_hi_l = chi;
+            mc->fc_lo_l = clo;
+        } else {
+            mc->fc_hi_f = chi;
+            mc->fc_lo_f = clo;
+        }
+    }
 }
 
 int build_plan(const redash_params *p, Plan *pl) {

@@ -49,6 +49,13 @@ struct ModConst {
     uint32_t red_M, red_s, sd_M, sd_s;
     uint32_t nlo_f, pw_lo_f, lo_M_f, lo_s_f;
     uint32_t nlo_l, pw_lo_l, lo_M_l, lo_s_l;
+    // Digits by fraction multiplication (fd == 1 when m^(2 nhi) < 2^32 for
+    // both word kinds, nhi = nres - nlo the larger part): for x < m^n,
+    // F = x * (floor(2^32 / m^n) + 1) mod 2^32, then each digit, most
+    // significant first, is umulhi(F, m) and F <- F m mod 2^32.  fc_hi_* and
+    // fc_lo_* are those multipliers for the high and low parts of a word.
+    uint32_t fd;
+    uint32_t fc_hi_f, fc_lo_f, fc_hi_l, fc_lo_l;
     // Word offset of this modulus in the evaluator's working storage (only
     // the remaining moduli R[1..u-1] have one: their Phase-B copies).
     uint32_t wkoff;

@@ -119,17 +119,19 @@ __device__ __forceinline__ void eval_fast(uint32_t d, const ModConst &mm, uint32
         const uint32_t D = frac_mul_carry(V, mm.pw_g);
         const uint32_t rw = next_word(row);
         LB.put(dst, w,
-               acc ? fast_word_any<true, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm, tk)
-                   : fast_word_any<false, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, rw, l, coeff, mm,
-                                               tk));
+               acc ? fast_word_any<true, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f,
+                                              mm.fc_lo_f, rw, l, coeff, mm, tk)
+                   : fast_word_any<false, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f,
+                                               mm.fc_lo_f, rw, l, coeff, mm, tk));
     }
     const uint32_t l = tgt[0];
     const uint32_t D = frac_mul_carry(V, mm.pw_last);
     const uint32_t rw = row[0];
     LB.put(dst, mm.W - 1,
-           acc ? fast_word_any<true, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm, tk)
-               : fast_word_any<false, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, rw, l, coeff, mm,
-                                           tk));
+           acc ? fast_word_any<true, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l,
+                                          mm.fc_lo_l, rw, l, coeff, mm, tk)
+               : fast_word_any<false, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l,
+                                           mm.fc_lo_l, rw, l, coeff, mm, tk));
 }
 
 // Applies gate g's free operation to its destination label (in tgt):
@@ -350,10 +352,10 @@ __device__ __forceinline__ void store_row(uint32_t (&V)[8], const uint32_t (&B)[
 #pragma unroll 1
         for (uint32_t w = 0; w + 1 < mm.W; ++w) {
             const uint32_t D = frac_mul_carry(V, mm.pw_g);
-            rp[w] = row_word_any(D, mm.g, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, next_word(b), mm);
+            rp[w] = row_word_any(D, mm.g, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f, mm.fc_lo_f, next_word(b), mm);
         }
         const uint32_t D = frac_mul_carry(V, mm.pw_last);
-        rp[mm.W - 1] = row_word_any(D, mm.glast, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, b[0], mm);
+        rp[mm.W - 1] = row_word_any(D, mm.glast, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l, mm.fc_lo_l, b[0], mm);
     } else {
 #pragma unroll 1
         for (uint32_t w = 0; w < mm.W; ++w) rp[w] = label_sub(next_word(b), pad_word(V, w, mm), w, mm);
