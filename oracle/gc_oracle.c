@@ -14,6 +14,13 @@
  *   - ShiftUp by P/2, division by s (Sec. 3.2), generalized base
  *     extension (Sec. 3.3, Eq. rns_to_mrs with the corrected missing-residue
  *     formula), ShiftDown by P/(2s)                             (Sec. 3.4)
+ *     READING where P/2 or P/(2s) is not an integer (odd P, or a power-of-two
+ *     modulus that is also scaled by, Sec. 4's 2^l bases): ShiftUp by
+ *     U = floor(P/2), ShiftDown by floor(U/s); the gadget then returns
+ *     floor((x + (U mod s)) / s), which is floor(x/s) whenever P/(2s) is an
+ *     integer.
+ *   - moduli: primes, or one power of two (the 2^l moduli of Sec. 4),
+ *     pairwise coprime
  *   - garbler offline / evaluator online roles                 (Sec. 2.1)
  *
  * The paper does not fix the label hash, the label length, the PRG, the
@@ -154,6 +161,22 @@ static int is_prime_u32(uint32_t n) {
     return 1;
 }
 
+static int is_pow2_u32(uint32_t n) { return n >= 2 && (n & (n - 1)) == 0; }
+
+static uint32_t gcd_u32(uint32_t a, uint32_t b) {
+    while (b) {
+        uint32_t t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+/* Radix of the first offset digit: R_m[0] is drawn from it and mapped to a
+ * unit of Z_m (d + 1 for a prime m, 2d + 1 for m = 2^l, l >= 2). */
+static uint32_t offset_first_radix(uint32_t m) { return (is_pow2_u32(m) && m > 2) ? m / 2 : m - 1; }
+static uint32_t offset_first_unit(uint32_t m, uint32_t d) { return (is_pow2_u32(m) && m > 2) ? 2 * d + 1 : d + 1; }
+
 static uint32_t inv_mod(uint32_t a, uint32_t m) {
     a %= m;
     for (uint32_t x = 1; x < m; ++x)
@@ -260,7 +283,8 @@ static void hash_label(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadge
 /* Garbler PRG: K_seed = seed as 16 little-endian bytes;
  * rho(stream, idx) = AES_{K_seed}(C_0) + 2^128 AES_{K_seed}(C_1),
  * C_h = stream * 2^120 + idx * 2 + h.  A label is read off rho as fraction
- * digits; the first radix is m-1 when first_minus_one is set (offsets). */
+ * digits; the first radix is offset_first_radix(m) when first_minus_one is
+ * set (offsets). */
 static void prg_label(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx, uint32_t m,
                       int first_minus_one, uint32_t *out) {
     uint32_t V[8];
@@ -277,7 +301,7 @@ static void prg_label(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx,
     uint32_t lam = lambda_of(m);
     uint32_t radix[ORC_MAXLAMBDA];
     for (uint32_t i = 0; i < lam; ++i) radix[i] = m;
-    if (first_minus_one) radix[0] = m - 1;
+    if (first_minus_one) radix[0] = offset_first_radix(m);
     frac_digits(V, 8, radix, (int)lam, out);
 }
 
@@ -317,8 +341,10 @@ static int make_plan(const orc_params *p, orc_plan *pl) {
     unsigned __int128 P = 1;
     for (uint32_t i = 0; i < p->k; ++i) {
         uint32_t m = p->moduli[i];
-        if (m < 2 || m > 255 || !is_prime_u32(m)) return ORC_EPARAM;
+        if (m < 2 || m > 255 || !(is_prime_u32(m) || is_pow2_u32(m))) return ORC_EPARAM;
         if (i > 0 && m <= p->moduli[i - 1]) return ORC_EPARAM;
+        for (uint32_t j = 0; j < i; ++j)
+            if (gcd_u32(m, p->moduli[j]) != 1) return ORC_EPARAM;
         pl->m[i] = m;
         pl->lam[i] = lambda_of(m);
         pl->W[i] = words_of(m);
@@ -336,7 +362,6 @@ static int make_plan(const orc_params *p, orc_plan *pl) {
     }
     pl->P = (uint64_t)P;
     pl->s = s;
-    if (pl->P % (2 * s) != 0) return ORC_EPARAM; /* ShiftDown P/(2s) must be an integer */
     pl->u = 0;
     for (uint32_t i = 0; i < p->k; ++i)
         if (!pl->is_scale[i]) pl->R[pl->u++] = i;
@@ -492,12 +517,14 @@ void orc_prg_label(uint64_t seed, uint32_t stream, uint64_t idx, uint32_t m, int
     prg_label(rk, stream, idx, m, first_minus_one, out);
 }
 
-/* Offsets R_m: digits of rho(1, i) with radices (m-1, m, ..., m), then
- * R_m[0] += 1 so that R_m[0] is a unit of Z_m (m prime). */
+/* Offsets R_m: digits of rho(1, i) with radices (r0, m, ..., m), then R_m[0]
+ * mapped to a unit of Z_m so that the m colours of a wire are distinct:
+ * r0 = m-1 and R_m[0] = d+1 for a prime m; r0 = m/2 and R_m[0] = 2d+1 for
+ * m = 2^l, l >= 2. */
 static void make_offsets(const orc_plan *pl, const uint8_t rk_seed[176], uint32_t R[ORC_MAXK][ORC_MAXLAMBDA]) {
     for (uint32_t i = 0; i < pl->k; ++i) {
         prg_label(rk_seed, 1u, i, pl->m[i], 1, R[i]);
-        R[i][0] += 1;
+        R[i][0] = offset_first_unit(pl->m[i], R[i][0]);
     }
 }
 
@@ -519,8 +546,8 @@ static void garble_one(const orc_plan *pl, uint32_t gadget_id, uint64_t a, uint3
     const uint32_t k = pl->k;
     uint32_t Wl[ORC_MAXK][ORC_MAXLAMBDA];
     uint32_t outR[ORC_MAXK][ORC_MAXLAMBDA];
-    uint64_t half = pl->P / 2, down = pl->P / (2 * pl->s);
-    /* ShiftUp: G^0_i = Z_i - (P/2 mod m_i) R_i. */
+    uint64_t half = pl->P / 2, down = half / pl->s; /* floor(P/2), floor(floor(P/2)/s) */
+    /* ShiftUp: G^0_i = Z_i - (floor(P/2) mod m_i) R_i. */
     for (uint32_t i = 0; i < k; ++i) {
         uint32_t m = pl->m[i];
         uint32_t c = (uint32_t)((m - half % m) % m);

@@ -250,13 +250,21 @@ def gate_list(base, scale_idx):
 
 
 def shift_constants(base, scale_idx):
-    """ShiftUp by P/2 and ShiftDown by P/(2s) (Sec. 3.4).  READING: both must be
-    integers, i.e. P even and 2 not among the scaling moduli."""
+    """ShiftUp by P/2 and ShiftDown by P/(2s) (Sec. 3.4).  READING where they
+    are not integers (odd P; a 2^l modulus scaled by, the bases of Sec. 4):
+    ShiftUp by U = floor(P/2) and ShiftDown by floor(U/s).  The gadget then
+    returns floor((x + (U mod s)) / s), equal to floor(x/s) whenever P/(2s)
+    is an integer."""
     P = cardinality(base)
     s = cardinality([base[i] for i in scale_idx])
-    if P % (2 * s) != 0:
-        raise ValueError("P/(2s) is not an integer")
-    return P // 2, P // (2 * s)
+    return P // 2, (P // 2) // s
+
+
+def rounding_offset(base, scale_idx) -> int:
+    """r = floor(P/2) mod s: the gadget computes floor((x + r)/s) (0 when
+    P/(2s) is an integer)."""
+    s = cardinality([base[i] for i in scale_idx])
+    return (cardinality(base) // 2) % s
 
 
 def gadget_trace(base, scale_idx, x: int):
@@ -314,7 +322,8 @@ def gadget_trace(base, scale_idx, x: int):
 
 
 def plain_scale(x: int, base, scale_idx) -> int:
-    """floor(x/s) computed through the gadget's residue steps (value level)."""
+    """floor((x + r)/s), r = rounding_offset(base, scale_idx) (floor(x/s) when
+    P/(2s) is an integer), computed through the gadget's residue steps."""
     return gadget_trace(base, scale_idx, x)["y"]
 
 

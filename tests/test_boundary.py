@@ -76,8 +76,9 @@ def test_label_words_match_oracle(m):
 
 
 BAD = [
-    ([3, 5, 7], [2]),
-    ([2, 3, 5], [0]),
+    ([3, 9, 11], [2]),
+    ([3, 5, 6], [2]),
+    ([4, 8, 11], [2]),
     ([2, 3, 4], [2]),
     ([3, 2, 5], [2]),
     ([2, 3, 5], [1, 1]),
@@ -124,7 +125,7 @@ def test_entry_points_validate_before_any_device_work():
     """Invalid parameters and NULL buffers are rejected on the host, before
     any HIP call, so this runs without a GPU."""
     L = B.lib()
-    bad = B.make_params([3, 5, 7], [2], 4, 0)  # P odd
+    bad = B.make_params([3, 9, 11], [2], 4, 0)  # 9 is neither prime nor a power of two
     good = B.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 4, 0)
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below returns early
     assert L.redash_eval_scale(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM

@@ -184,6 +184,25 @@ def test_prg_offsets_first_residue_nonzero():
             assert r.max() < m
 
 
+@pytest.mark.parametrize("m", [4, 8, 16, 32, 64, 128])
+def test_offsets_first_residue_is_a_unit_for_powers_of_two(m):
+    """For m = 2^l the first offset residue is drawn from m/2 values and mapped
+    to the odd residue 2d + 1 (a unit), so the m colours of a wire stay
+    distinct (point-and-permute)."""
+    seen = set()
+    w3 = O.words(3)
+    for seed in range(40):
+        d = O.prg_label(seed, 1, 1, m, True)  # the draw behind R_m of base (3, m)
+        assert d[0] < m // 2 and d.max() < m
+        offs = O.garble(O.make_params([3, m], [1], 1, seed), 0, 1, with_tables=False)[0]
+        R = O.pk32_unpack(m, offs[w3:w3 + O.words(m)])
+        assert int(R[0]) == 2 * int(d[0]) + 1
+        assert np.array_equal(R[1:], d[1:])
+        seen.add(int(R[0]))
+        assert sorted({(int(R[0]) * v) % m for v in range(m)}) == list(range(m))
+    assert len(seen) > 1
+
+
 # ----------------------------------------------------------------------------
 # garbling algebra
 # ----------------------------------------------------------------------------
@@ -195,6 +214,11 @@ TRACE_CASES = [
     (rns.first_primes(12), [11], 3),
     (rns.first_primes(12), [10, 11], 13),
     ([2, 3, 5, 7], [1, 2], 9),
+    # power-of-two moduli and odd P (Sec. 4's bases; rounding reading)
+    ([5, 7, 8], [2], 21),
+    ([3, 5, 7, 16], [0], 22),
+    ([3, 5, 7], [0, 1], 23),
+    ([32, 167, 173], [0], 24),
 ]
 
 
@@ -239,15 +263,15 @@ def test_every_wire_label_is_zero_plus_value_times_offset(base, S, seed):
             lam = O.lam(mi)
             assert np.array_equal(tr["ev_slots"][G][i][:lam],
                                   _lab(mi, tr["gb_slots"][G][i], R[i], pt["slots"][G][i]))
-        # outputs after ShiftDown carry floor(x/s)
+        # outputs after ShiftDown carry floor((x + r)/s), r = floor(P/2) mod s
         s = rns.cardinality([base[i] for i in S])
-        y = x // s
+        y = (x + rns.rounding_offset(base, S)) // s
         for i, mi in enumerate(base):
             lam = O.lam(mi)
             assert np.array_equal(tr["ev_final"][i][:lam], _lab(mi, tr["gb_final"][i], R[i], y % P % mi))
 
 
-@pytest.mark.parametrize("base,S,seed", TRACE_CASES[:4])
+@pytest.mark.parametrize("base,S,seed", TRACE_CASES[:4] + TRACE_CASES[6:8])
 def test_every_row_decrypts_for_every_input_value(base, S, seed):
     """For every gate and every v in Z_q: the row selected by the colour of
     A^0 + v R_q, plus the hash of that label, is B^0 + (v mod m) R_m, and the
@@ -307,6 +331,22 @@ def test_decode_all_inputs_product_scaling(base, S):
     Y = O.evaluate(p, 0, len(xs), O.encode(p, xs, zin, offs), tab)
     y, bad = O.decode(p, Y, zout, offs)
     assert bad.sum() == 0 and np.array_equal(y, xs // s)
+
+
+@pytest.mark.parametrize("base,S", [([3, 4, 5], [1]), ([5, 7, 8], [2]), ([3, 5, 7], [2]), ([2, 3, 5], [0]),
+                                     ([4, 5, 7, 11], [0, 2])])
+def test_decode_all_inputs_rounding_reading(base, S):
+    """Every input of small bases with a power-of-two modulus or odd P, one
+    gadget per input: decode(eval) = floor((x + r)/s), r = floor(P/2) mod s."""
+    P = rns.cardinality(base)
+    s = rns.cardinality([base[i] for i in S])
+    r = (P // 2) % s
+    xs = np.arange(-(P // 2), P - P // 2, dtype=np.int64)
+    p = O.make_params(base, S, len(xs), 7)
+    offs, zin, zout, tab = O.garble(p, 0, len(xs))
+    Y = O.evaluate(p, 0, len(xs), O.encode(p, xs, zin, offs), tab)
+    y, bad = O.decode(p, Y, zout, offs)
+    assert bad.sum() == 0 and np.array_equal(y, (xs + r) // s)
 
 
 def test_zero_label_path_matches_full_garbling():
@@ -381,9 +421,10 @@ def test_corrupted_row_breaks_only_its_gadget():
 
 
 @pytest.mark.parametrize("moduli,S", [
-    ([3, 5, 7], [2]),          # P odd: ShiftDown not an integer
-    ([2, 3, 5], [0]),          # 2 among the scaling moduli
-    ([2, 3, 4], [2]),          # not prime
+    ([2, 3, 4], [2]),          # 2 and 4 not coprime
+    ([3, 9, 11], [2]),         # 9: neither prime nor a power of two
+    ([3, 5, 6], [2]),          # 6: neither prime nor a power of two
+    ([4, 8, 11], [2]),         # two powers of two
     ([3, 2, 5], [2]),          # not ascending
     ([2, 3, 5], [1, 1]),       # scale set not strictly ascending
     ([2, 3, 5], [0, 1, 2]),    # t = k

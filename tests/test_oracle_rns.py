@@ -160,12 +160,59 @@ def test_gadget_floor_division_large_base_sampled():
             assert rns.plain_scale(x, base, S) == x // s
 
 
-def test_shift_requires_even_quotient():
-    """READING: ShiftDown by P/(2s) needs P/(2s) to be an integer."""
-    with pytest.raises(ValueError):
-        rns.shift_constants([3, 5, 7], [2])
-    with pytest.raises(ValueError):
-        rns.shift_constants([2, 3, 5], [0])
+def test_shift_constants_reading():
+    """Sec. 3.4 shifts by P/2 and P/(2s).  READING where they are not integers:
+    ShiftUp by U = floor(P/2), ShiftDown by floor(U/s).  Where they are
+    integers nothing changes (Table 1: up 3, down 1)."""
+    assert rns.shift_constants([2, 3], [1]) == (3, 1)
+    assert rns.rounding_offset([2, 3], [1]) == 0
+    assert rns.shift_constants([3, 5, 7], [2]) == (52, 7)   # P = 105 odd
+    assert rns.rounding_offset([3, 5, 7], [2]) == 3
+    Q = 167 * 173
+    assert rns.shift_constants([32, 167, 173], [0]) == (16 * Q, (16 * Q) // 32)
+    assert rns.rounding_offset([32, 167, 173], [0]) == 16  # s/2: round half up
+    for k in range(3, 13):
+        base = rns.first_primes(k)
+        for S in ([k - 1], [k - 2, k - 1]):
+            assert rns.rounding_offset(base, S) == 0
+
+
+# Bases the paper's Sec. 4 uses or that stress the reading: a power-of-two
+# modulus (scaled by, or among the remaining moduli) and odd P.
+ROUNDING_CASES = [
+    ([2, 3, 5], [0]),          # s = 2, 2 scaled by: U mod s = 1
+    ([3, 4, 5], [1]),          # s = 4
+    ([4, 5, 7], [0]),          # s = 4, 4 first
+    ([5, 7, 8], [2]),          # s = 8
+    ([3, 5, 8], [2]),          # s = 8
+    ([3, 5, 7, 16], [3]),      # s = 16
+    ([3, 5, 7, 16], [0]),      # s = 3, 16 among R
+    ([3, 5, 7], [2]),          # P odd, s = 7
+    ([3, 5, 7], [0, 1]),       # P odd, s = 15
+    ([8, 11, 13], [0]),        # s = 8, 2^l with odd primes
+]
+
+
+@pytest.mark.parametrize("base,S", ROUNDING_CASES)
+def test_gadget_rounding_brute_force(base, S):
+    """Every x of the signed range [-floor(P/2), ceil(P/2) - 1] (Sec. 2.4):
+    the residue-level gadget returns floor((x + r)/s), r = floor(P/2) mod s."""
+    P = rns.cardinality(base)
+    s = rns.cardinality([base[i] for i in S])
+    r = (P // 2) % s
+    assert r == rns.rounding_offset(base, S)
+    for x in range(-(P // 2), P - P // 2):
+        assert rns.plain_scale(x, base, S) == (x + r) // s, (x, base, S)
+
+
+def test_round_half_up_for_half_offset():
+    """With r = s/2 (a 2^l modulus scaled by, Sec. 4's bases) the gadget rounds
+    x/s to the nearest integer, halves upward."""
+    base, S = [5, 7, 8], [2]
+    assert rns.rounding_offset(base, S) == 4
+    for x in range(-140, 140):
+        want = (2 * x + 8) // 16  # nearest, ties up
+        assert rns.plain_scale(x, base, S) == want
 
 
 def test_gate_counts():
