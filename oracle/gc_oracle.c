@@ -740,7 +740,8 @@ int orc_eval(const orc_params *p, uint64_t a_begin, uint64_t count, const uint32
 
 /* Decode: v_i = (Y_i[0] - O_i[0]) R_i[0]^{-1} mod m_i; the label is valid iff
  * Y_i = O_i + v_i R_i componentwise; y = CRT(v) mapped to the signed range
- * [-P/2, P/2).  bad[a] = 1 for a gadget with any invalid residue label. */
+ * [-floor(P/2), ceil(P/2) - 1] (Sec. 2.4; [-P/2, P/2) for even P).  bad[a] = 1
+ * for a gadget with any invalid residue label. */
 int orc_decode(const orc_params *p, uint64_t count, const uint32_t *out_labels, const uint32_t *out_zero,
                const uint32_t *offsets, int64_t *y, uint8_t *bad) {
     orc_plan pl;
@@ -773,7 +774,7 @@ int orc_decode(const orc_params *p, uint64_t count, const uint32_t *out_labels, 
             M *= m;
         }
         int64_t val = (int64_t)acc;
-        if ((uint64_t)val >= pl.P / 2) val -= (int64_t)pl.P;
+        if ((uint64_t)val >= (pl.P + 1) / 2) val -= (int64_t)pl.P; /* [-floor(P/2), ceil(P/2) - 1] */
         y[a] = val;
         bad[a] = (uint8_t)!ok;
     }

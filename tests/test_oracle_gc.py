@@ -349,6 +349,19 @@ def test_decode_all_inputs_rounding_reading(base, S):
     assert bad.sum() == 0 and np.array_equal(y, (xs + r) // s)
 
 
+def test_decode_signed_range_odd_P():
+    """Sec. 2.4 signed encoding for odd P: labels of every value of Z_P decode
+    to [-floor(P/2), ceil(P/2) - 1] (P = 105: 52 stays 52, 53 becomes -52)."""
+    base, S = [3, 5, 7], [2]
+    P = 105
+    vals = np.arange(-(P // 2), P - P // 2, dtype=np.int64)
+    p = O.make_params(base, S, len(vals), 3)
+    offs, zin, zout, _ = O.garble(p, 0, len(vals), with_tables=False)
+    y, bad = O.decode(p, O.encode(p, vals, zout, offs), zout, offs)
+    assert bad.sum() == 0 and np.array_equal(y, vals)
+    assert y.max() == 52 and y.min() == -52
+
+
 def test_zero_label_path_matches_full_garbling():
     base = rns.first_primes(8)
     p = O.make_params(base, [7], 64, 1)
