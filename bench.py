@@ -52,7 +52,7 @@ def cpu_baseline(w, x, sample: int, target_s: float):
         elapsed += time.perf_counter() - t1
         reps += 1
     y, bad = O.decode(op, Y, zout, offs)
-    assert bad.sum() == 0 and np.array_equal(y, np.floor_divide(x[:sample], w.s))
+    assert bad.sum() == 0 and np.array_equal(y, expected_values(w, x[:sample]))
     return {
         "value": round(sample * reps / elapsed, 1),
         "unit": "gadgets/s",
@@ -61,6 +61,63 @@ def cpu_baseline(w, x, sample: int, target_s: float):
         "sample": f"oracle eval of the first {sample} gadgets of the {w.name} workload "
                   f"(oracle-garbled tables), {reps} passes, {elapsed:.1f} s timed; plain C, one thread; "
                   f"host has {len(os.sched_getaffinity(0))} cores available",
+    }
+
+
+def expected_values(w, x):
+    """What the gadget returns: floor((x + r)/s) with r = floor(P/2) mod s
+    (the shift constants floor(P/2) and floor(floor(P/2)/s) of Sec. 3.4;
+    r = 0, i.e. floor(x/s), whenever P/(2s) is an integer)."""
+    return np.floor_divide(x + (w.P // 2) % w.s, w.s)
+
+
+def time_short_base(w, steps: int, warmup: int, dev):
+    """Garble, encode and time the evaluator on one short-base workload;
+    decode and check every gadget afterwards.  Returns a summary dict."""
+    import torch
+
+    from paper_2506_14489_amd import binding as B
+    from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import workloads as WL
+
+    n = w.n
+    x = WL.make_inputs(w)
+    params = B.make_params(w.moduli, w.scale_idx, n, w.seed)
+    buf = B.Buffers(params, dev)
+    stream = torch.cuda.current_stream()
+    B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work, stream)
+    B.redash_encode(params, torch.from_numpy(x).to(dev), buf.in_zero, buf.offsets, buf.in_labels, stream)
+    for _ in range(warmup):
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
+    ev1.record(stream)
+    B.redash_decode(params, buf.out_labels, buf.out_zero, buf.offsets, buf.y, buf.bad, stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    ok = int(buf.bad.item()) == 0 and np.array_equal(buf.y.cpu().numpy()[:n], expected_values(w, x))
+    del buf
+    torch.cuda.empty_cache()
+    if not ok:
+        log(f"{w.name}: decode check FAILED")
+        sys.exit(1)
+    tops = cost.ops_per_gadget(w.moduli, w.scale_idx) * n / (ms / 1e3) / 1e12
+    gbs = cost.bytes_per_gadget(w.moduli, w.scale_idx) * n / (ms / 1e3) / 1e9
+    log(f"{w.name}: eval {ms:.3f} ms per call, {n / (ms / 1e3):.3e} gadgets/s")
+    return {
+        "workload": f"{w.name}: {n} gadgets, values uniform over the signed range",
+        "moduli": list(w.moduli),
+        "scale": w.s,
+        "gates_per_gadget": len(cost.gates(w.moduli, w.scale_idx)),
+        "ms_per_call": round(ms, 4),
+        "gadgets_per_s": round(n / (ms / 1e3), 1),
+        "alu_frac": round(tops / ALU_PEAK_TOPS, 4),
+        "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "check": "decode = floor((x + (floor(P/2) mod s))/s) with every label valid, all gadgets",
+        "steps": steps,
     }
 
 
@@ -76,6 +133,8 @@ def main():
     ap.add_argument("--no-check", action="store_true", help="skip the decode check after timing")
     ap.add_argument("--garble-steps", type=int, default=3,
                     help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
+    ap.add_argument("--no-short-bases", action="store_true",
+                    help="skip timing the evaluator on the short and power-of-two bases of Sec. 4")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -172,7 +231,7 @@ def main():
     if not args.no_check:
         B.redash_decode(params, buf.out_labels, buf.out_zero, buf.offsets, buf.y, buf.bad, stream)
         torch.cuda.synchronize()
-        ok = int(buf.bad.item()) == 0 and np.array_equal(buf.y.cpu().numpy()[:n], np.floor_divide(x, w.s))
+        ok = int(buf.bad.item()) == 0 and np.array_equal(buf.y.cpu().numpy()[:n], expected_values(w, x))
         if not ok:
             log("decode check FAILED")
             sys.exit(1)
@@ -241,6 +300,10 @@ def main():
     }
     del buf
     torch.cuda.empty_cache()
+    if not args.no_short_bases:
+        # the short and power-of-two bases of Sec. 4, at the batched map's gadget count
+        result["short_bases"] = [time_short_base(WL.at_size(sw, WL.BATCHED.n), max(args.steps // 2, 1),
+                                                 args.warmup, dev) for sw in WL.SHORT_BASES]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -79,14 +79,18 @@ extern "C" {
  * One gadget call: n independent gadget instances with the same base and
  * scaling factor.
  *   k           number of base moduli, 2..15.
- *   moduli      the RNS base (Sec. 2.2): primes, strictly ascending, 2..255,
- *               with P = prod(moduli) < 2^63.
+ *   moduli      the RNS base (Sec. 2.2): primes or powers of two (Sec. 4
+ *               uses one 2^l modulus), 2..255, strictly ascending, pairwise
+ *               coprime, with P = prod(moduli) < 2^63.
  *   t           number of scaling moduli, 1..k-1.
  *   scale_idx   indices into moduli of the scaling moduli S, strictly
  *               ascending; s = prod of those moduli (Sec. 3.4: s may be one
- *               base modulus or a product of several).  P/(2s) must be an
- *               integer (P even and 2 not in S), because ShiftUp and
- *               ShiftDown add the constants P/2 and P/(2s) (Sec. 3.4).
+ *               base modulus or a product of several).  ShiftUp adds
+ *               U = floor(P/2) and ShiftDown subtracts floor(U/s) (Sec. 3.4's
+ *               P/2 and P/(2s) where those are integers), so the gadget
+ *               returns floor((x + (U mod s)) / s): floor(x/s) whenever
+ *               P/(2s) is an integer, round-half-up of x/s for a base whose
+ *               only even modulus 2^l is scaled by.
  *   n           number of gadget instances held in the buffers (may be 0).
  *   seed        garbler seed: keys the garbling PRG; gadget_id = seed mod 2^32.
  *   a0          global index of the first gadget held in the buffers.  The
@@ -123,8 +127,8 @@ int redash_plan(const redash_params *p, redash_sizes *out);
  * Garbler, offline phase (Sec. 2.1; Sec. 2.3 projection gates with row
  * reduction; Sec. 3.4 free ShiftUp/ShiftDown applied to zero-labels).
  * Writes:
- *   d_offsets   offset_words: R_m for every modulus (R_m[0] != 0, so the k
- *               colours of a wire are distinct).
+ *   d_offsets   offset_words: R_m for every modulus (R_m[0] a unit of Z_m,
+ *               so the m colours of a wire are distinct).
  *   d_in_zero   label_words: input zero-labels Z of gadgets a0..a0+n-1.
  *   d_out_zero  label_words: output zero-labels (value 0 after ShiftDown);
  *               also holds intermediate zero-labels while the call runs.
@@ -141,7 +145,8 @@ int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d
  * Stand-in for the oblivious transfer of input labels (Sec. 2.1):
  * X_{a,i} = Z_{a,i} + ((x_a mod P) mod m_i) * R_{m_i}, residue-wise mod m_i.
  *   d_x         n signed activations (int64), any value (reduced mod P; the
- *               result is floor(x/s) for x in [-P/2, P/2), Sec. 3.2/3.4).
+ *               result is as stated under redash_params for x in the signed
+ *               range [-floor(P/2), ceil(P/2) - 1], Sec. 2.4, 3.2, 3.4).
  *   d_in_zero   label_words, from redash_garble_scale.
  *   d_offsets   offset_words, from redash_garble_scale.
  *   d_in_labels label_words, written.
@@ -167,7 +172,8 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
  *                remaining moduli (Sec. 3.3 consumes them while the Phase-A
  *                values are outputs).  Contents on entry are ignored and on
  *                return unspecified; may be NULL when work_words is 0.
- * Output labels carry floor(x/s) under the garbler's output zero-labels.
+ * Output labels carry floor(x/s) (see redash_params) under the garbler's
+ * output zero-labels.
  * REDASH_E_PARAM also when n >= 2^30 (a gadget's byte offset must fit in
  * 32 bits).
  */
@@ -176,8 +182,8 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
 
 /*
  * Garbler decodes the returned labels (Sec. 2.1): v_i = (Y_i[0] - O_i[0]) *
- * R_i[0]^{-1} mod m_i, y = CRT(v) in the signed range [-P/2, P/2)
- * (Sec. 2.4).  A gadget whose label differs from O_i + v_i R_i in any residue
+ * R_i[0]^{-1} mod m_i, y = CRT(v) in the signed range
+ * [-floor(P/2), ceil(P/2) - 1] (Sec. 2.4).  A gadget whose label differs from O_i + v_i R_i in any residue
  * is counted as bad (its d_y entry is still written).
  *   d_out_labels, d_out_zero  label_words; d_offsets offset_words.
  *   d_y          n int64, written.
@@ -191,7 +197,7 @@ int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const ui
 /*
  * The projection-gate hash alone (Sec. 2.3; construction in the conventions
  * above), for tests and for measuring the AES throughput of the device.
- *   q, m        input and output modulus (2..255, prime).
+ *   q, m        input and output modulus (2..255, prime or a power of two).
  *   count       number of labels.
  *   d_labels    W_q * count words, SoA: word w of label a at w * count + a.
  *   gadget_id   tweak high word.

@@ -213,10 +213,12 @@ def redash_hash_labels(q, m, count, labels, gadget_id, tau, out, stream=None):
 
 def label_words_of(m: int) -> int:
     """W_m, read off redash_plan: the base (2, m) holds W_2 = 4 words (128
-    one-bit residues) plus W_m."""
+    one-bit residues) plus W_m; an even m is paired with 251 instead."""
     if m == 2:
         return 4
-    return redash_plan(make_params([2, m], [1], 1, 0))["offset_words"] - 4
+    if m % 2:
+        return redash_plan(make_params([2, m], [1], 1, 0))["offset_words"] - 4
+    return redash_plan(make_params([m, 251], [1], 1, 0))["offset_words"] - label_words_of(251)
 
 
 class Buffers:

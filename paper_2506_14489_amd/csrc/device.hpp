@@ -340,10 +340,21 @@ __device__ __forceinline__ uint32_t frac_mul_carry(uint32_t (&V)[8], uint32_t pw
     return static_cast<uint32_t>(carry);
 }
 
+// The same with pw = 0 standing for 2^32 (m = 4, 16): the carry is the top
+// limb and the limbs move up by one.
+__device__ __forceinline__ uint32_t frac_carry_any(uint32_t (&V)[8], uint32_t pw) {
+    if (pw) return frac_mul_carry(V, pw);
+    const uint32_t top = V[7];
+#pragma unroll
+    for (int l = 7; l > 0; --l) V[l] = V[l - 1];
+    V[0] = 0;
+    return top;
+}
+
 __device__ __forceinline__ uint32_t digits_word(uint32_t (&V)[8], uint32_t w, const ModConst &mc) {
     const bool last = (w + 1 == mc.W);
     const uint32_t nres = last ? mc.glast : mc.g;
-    uint32_t D = frac_mul_carry(V, last ? mc.pw_last : mc.pw_g);
+    uint32_t D = frac_carry_any(V, last ? mc.pw_last : mc.pw_g);
     uint32_t out = 0;
     for (uint32_t j = nres; j-- > 1;) {
         uint32_t q = div_m(D, mc);
@@ -384,7 +395,7 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_
         const uint32_t r = (rw >> (b * j)) & mask;
         const uint32_t lj = (l >> (b * j)) & mask;
         const uint32_t v = ACC ? lj + mul24(c, p + r) : mul24(c, lj + mc.two_m - p - r);
-        const uint32_t q = mul24(v, mc.red_M) >> mc.red_s;
+        const uint32_t q = __umulhi(v, mc.red_M);
         return (v - mul24(q, m)) << (b * j);
     };
     uint32_t res = 0;
@@ -468,7 +479,7 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
         } else {
             const uint32_t v = ACC ? lj + mul24(c, __builtin_amdgcn_ubfe(p + r, 0, 16))
                                    : mul24(c, __builtin_amdgcn_ubfe(lj + mc.two_m - p - r, 0, 16));
-            const uint32_t q = __builtin_amdgcn_ubfe(mul24(v, mc.red_M), mc.red_s, 24);
+            const uint32_t q = __umulhi(v, mc.red_M);
             // (opaque: a shift folded into the product would widen its operand)
             res |= opaque(v - mul24(q, m)) << (B * j);
         }
@@ -480,7 +491,8 @@ __device__ __forceinline__ uint32_t fast_word_c(uint32_t D, uint32_t lo_M, uint3
 }
 
 // Dispatch on (residues in the word, bits per residue): the combinations
-// of the primes up to 37 are unrolled, anything else takes the loops.
+// of the primes up to 37 and of the short bases' moduli (8, 32, 97, 107,
+// 128, 167, 173) are unrolled, anything else takes the loops.
 template <bool ACC, bool TAB>
 __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uint32_t nlo, uint32_t lo_M,
                                                   uint32_t lo_s, uint32_t pw_lo, uint32_t c_hi, uint32_t c_lo,
@@ -493,7 +505,7 @@ __device__ __forceinline__ uint32_t fast_word_any(uint32_t D, uint32_t nres, uin
         return fast_word_c<ACC, NR, BB, TAB>(D, lo_M, lo_s, pw_lo, c_hi, c_lo, rw, l, c, mc, tk);
         REDASH_FW(16, 2) REDASH_FW(1, 2) REDASH_FW(10, 3) REDASH_FW(6, 3) REDASH_FW(8, 4) REDASH_FW(6, 4)
         REDASH_FW(3, 4) REDASH_FW(6, 5) REDASH_FW(5, 5) REDASH_FW(3, 5) REDASH_FW(2, 5) REDASH_FW(1, 5)
-        REDASH_FW(5, 6)
+        REDASH_FW(5, 6) REDASH_FW(3, 3) REDASH_FW(4, 7) REDASH_FW(3, 7) REDASH_FW(4, 8) REDASH_FW(2, 8)
 #undef REDASH_FW
         default: return fast_word<ACC>(D, nres, nlo, lo_M, lo_s, pw_lo, rw, l, c, mc);
     }
@@ -525,8 +537,8 @@ __device__ __forceinline__ uint32_t row_word_c(uint32_t D, uint32_t lo_M, uint32
     return res;
 }
 
-// row_word_c for any word shape; shapes outside the primes up to 37 take the
-// generic digit loop.
+// row_word_c for any word shape; shapes outside the unrolled list of
+// fast_word_any take the generic digit loop.
 __device__ __forceinline__ uint32_t row_word_any(uint32_t D, uint32_t nres, uint32_t lo_M, uint32_t lo_s,
                                                  uint32_t pw_lo, uint32_t c_hi, uint32_t c_lo, uint32_t bw,
                                                  const ModConst &mc) {
@@ -535,7 +547,7 @@ __device__ __forceinline__ uint32_t row_word_any(uint32_t D, uint32_t nres, uint
     case (NR) | ((BB) << 8): return row_word_c<NR, BB>(D, lo_M, lo_s, pw_lo, c_hi, c_lo, bw, mc);
         REDASH_RW(16, 2) REDASH_RW(1, 2) REDASH_RW(10, 3) REDASH_RW(6, 3) REDASH_RW(8, 4) REDASH_RW(6, 4)
         REDASH_RW(3, 4) REDASH_RW(6, 5) REDASH_RW(5, 5) REDASH_RW(3, 5) REDASH_RW(2, 5) REDASH_RW(1, 5)
-        REDASH_RW(5, 6)
+        REDASH_RW(5, 6) REDASH_RW(3, 3) REDASH_RW(4, 7) REDASH_RW(3, 7) REDASH_RW(4, 8) REDASH_RW(2, 8)
 #undef REDASH_RW
         default: {
             uint32_t res = 0;

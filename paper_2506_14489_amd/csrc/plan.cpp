@@ -29,7 +29,26 @@ uint32_t ipow(uint32_t m, uint32_t e) {
     return static_cast<uint32_t>(r);
 }
 
+uint64_t ipow64(uint32_t m, uint32_t e) {
+    uint64_t r = 1;
+    for (uint32_t i = 0; i < e; ++i) r *= m;
+    return r;
+}
+
+bool is_pow2(uint32_t v) { return v >= 2 && (v & (v - 1)) == 0; }
+
+uint32_t gcd(uint32_t a, uint32_t b) {
+    while (b) {
+        const uint32_t r = a % b;
+        a = b;
+        b = r;
+    }
+    return a;
+}
+
 }  // namespace
+
+bool modulus_ok(uint32_t m) { return m >= 2 && m <= 255 && (is_prime(m) || is_pow2(m)); }
 
 void division_constants(uint32_t m, uint64_t x_bound, uint32_t *outM, uint32_t *outS, uint32_t *outFix) {
     if ((m & (m - 1)) == 0) {  // a power of two (m >= 2): umulhi(x, 2^(32-e)) = x >> e
@@ -114,11 +133,19 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     mc->W = (mc->lam + mc->g - 1) / mc->g;
     mc->glast = mc->lam - (mc->W - 1) * mc->g;
     mc->mask = (mc->b == 32) ? 0xffffffffu : ((1u << mc->b) - 1u);
+    // Units of Z_m: every nonzero residue for a prime, the odd ones for 2^l.
+    const bool pow2 = is_pow2(m) && m > 2;
+    mc->phi = pow2 ? m / 2 : m - 1;
+    mc->r0 = pow2 ? m / 2 : m - 1;
+    // m^g reaches 2^32 only for m = 4 and m = 16 (b g = 32); it is stored
+    // as 0, and those moduli take the generic paths (fast stays 0).
+    const uint64_t pw_g64 = ipow64(m, mc->g), pw_last64 = ipow64(m, mc->glast);
+    const bool full_word = pw_g64 >= (1ull << 32) || pw_last64 >= (1ull << 32);
     if (m > 2) {
-        mc->pw_g = ipow(m, mc->g);
-        mc->pw_last = ipow(m, mc->glast);
+        mc->pw_g = static_cast<uint32_t>(pw_g64);
+        mc->pw_last = static_cast<uint32_t>(pw_last64);
     }
-    uint64_t bound = (m > 2) ? static_cast<uint64_t>(mc->pw_g) : (1ull << 32);
+    uint64_t bound = (m > 2 && !full_word) ? pw_g64 : (1ull << 32);
     // Products c * d of two residues (< m^2) are reduced with the same
     // constants, so the bound covers them as well.
     uint64_t sq = static_cast<uint64_t>(m) * m;
@@ -132,7 +159,9 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
         mc->sw_k |= ((1u << mc->b) - m) << (mc->b * f);
     }
     mc->two_m = 2 * m;
-    bool ok = mul24_constants(m, 3 * sq, &mc->red_M, &mc->red_s);
+    if (full_word) return;  // no fast constants: the packed-add fields above are all it uses
+    mc->red_M = static_cast<uint32_t>(((1ull << 32) + m - 1) / m);
+    bool ok = 3 * sq * sq < (1ull << 32);  // x m < 2^32 for x < 3 m^2 (every m <= 255)
     uint64_t part = 1;
     for (int k = 0; k < 2; ++k) {
         const uint32_t nres = k ? mc->glast : mc->g;
@@ -183,8 +212,12 @@ int build_plan(const redash_params *p, Plan *pl) {
     unsigned __int128 P = 1;
     for (uint32_t i = 0; i < p->k; ++i) {
         uint32_t m = p->moduli[i];
-        if (m < 2 || m > 255 || !is_prime(m)) return REDASH_E_PARAM;
-        if (i > 0 && m <= p->moduli[i - 1]) return REDASH_E_PARAM;  // ascending, hence pairwise coprime
+        // primes or powers of two (Sec. 4 uses one 2^l modulus), ascending,
+        // pairwise coprime (so at most one of them is even)
+        if (!modulus_ok(m)) return REDASH_E_PARAM;
+        if (i > 0 && m <= p->moduli[i - 1]) return REDASH_E_PARAM;
+        for (uint32_t j = 0; j < i; ++j)
+            if (gcd(m, p->moduli[j]) != 1) return REDASH_E_PARAM;
         P *= m;
     }
     if (P >= (static_cast<unsigned __int128>(1) << 63)) return REDASH_E_PARAM;
@@ -199,8 +232,11 @@ int build_plan(const redash_params *p, Plan *pl) {
         pl->S[a] = si;
     }
     const uint64_t P64 = static_cast<uint64_t>(P);
-    // ShiftDown adds P/(2s): it must be an integer (P even, 2 not in S).
-    if (P64 % (2 * s) != 0) return REDASH_E_PARAM;
+    // Shift constants (Sec. 3.4): up by U = floor(P/2), down by floor(U/s).
+    // Where P/(2s) is an integer these are P/2 and P/(2s) and the gadget
+    // returns floor(x/s); otherwise (odd P, or a scaled power of two) it
+    // returns floor((x + (U mod s)) / s).
+    const uint64_t U = P64 / 2, down = U / s;
 
     pl->k = p->k;
     pl->t = p->t;
@@ -219,8 +255,8 @@ int build_plan(const redash_params *p, Plan *pl) {
         fill_mod_const(p->moduli[i], &mc);
         mc.woff = woff;
         woff += mc.W;
-        mc.up = static_cast<uint32_t>((P64 / 2) % mc.m);
-        mc.down = static_cast<uint32_t>((P64 / (2 * s)) % mc.m);
+        mc.up = static_cast<uint32_t>(U % mc.m);
+        mc.down = static_cast<uint32_t>(down % mc.m);
     }
     pl->total_words = woff;
 

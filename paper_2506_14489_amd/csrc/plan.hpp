@@ -24,18 +24,22 @@ struct ModConst {
     uint32_t glast;    // residues in the last word: lam - (W - 1) g
     uint32_t woff;     // word offset of this modulus in a gadget's k labels
     uint32_t mask;     // (1 << b) - 1
-    uint32_t pw_g;     // m^g      (digits of one full word per 32-bit multiply)
-    uint32_t pw_last;  // m^glast
+    uint32_t pw_g;     // m^g      (digits of one full word per 32-bit multiply);
+                       // 0 stands for 2^32 (m = 4 and m = 16, whose fields fill the word)
+    uint32_t pw_last;  // m^glast  (0 likewise)
     // floor(x / m) for 32-bit x: if div_fix == 0, umulhi(x, divM) >> divS is
     // exact for every x < m^g (checked when the plan is built); otherwise
     // the round-up method with a fix-up step:
     //   t = umulhi(x, divM); floor(x/m) = (t + ((x - t) >> 1)) >> divS.
     uint32_t divM, divS, div_fix;
-    uint32_t up;       // (P/2) mod m      (ShiftUp)
-    uint32_t down;     // (P/(2s)) mod m   (ShiftDown)
+    uint32_t up;       // floor(P/2) mod m             (ShiftUp)
+    uint32_t down;     // floor(floor(P/2) / s) mod m  (ShiftDown)
+    uint32_t phi;      // order of the unit group of Z_m: m - 1 (prime), m / 2 (power of two)
+    uint32_t r0;       // radix of the offset's first digit: m - 1 (prime), m / 2 (2^l, l >= 2)
     // Evaluator fast path (fast == 1 when every bound below holds):
-    //  * red: floor(x/m) = (x * red_M) >> red_s for every x < 3 m^2, with
-    //    x * red_M < 2^32 (24-bit multiplies) -- one reduction per residue;
+    //  * red: floor(x/m) = umulhi(x, red_M), red_M = ceil(2^32 / m), for
+    //    every x < 3 m^2 (the error x (red_M m - 2^32) / 2^32 < x m / 2^32
+    //    stays below 1/m while x m^2 < 2^32) -- one multiply per residue;
     //  * sd: the same for every x below the larger part of a split word
     //    (parts below 2^23);
     //  * a word's nres digits D (nres = g, or glast for the last word) are
@@ -46,7 +50,7 @@ struct ModConst {
     //    a selected array element would be indexed at run time.)
     uint32_t fast;
     uint32_t two_m;  // 2m
-    uint32_t red_M, red_s, sd_M, sd_s;
+    uint32_t red_M, sd_M, sd_s;
     uint32_t nlo_f, pw_lo_f, lo_M_f, lo_s_f;
     uint32_t nlo_l, pw_lo_l, lo_M_l, lo_s_l;
     // Digits by fraction multiplication (fd == 1 when m^(2 nhi) < 2^32 for
@@ -122,11 +126,14 @@ struct Plan {
 // REDASH_E_PARAM.
 int build_plan(const redash_params *p, Plan *out);
 
+// A modulus the library accepts: a prime or a power of two in 2..255.
+bool modulus_ok(uint32_t m);
+
 // Residues per label and words per label for a modulus (2..255).
 uint32_t label_lambda(uint32_t m);
 uint32_t label_words(uint32_t m);
 
-// Fills one ModConst for modulus m (everything except woff, up, down).
+// Fills one ModConst for modulus m (everything except woff, wkoff, up, down).
 void fill_mod_const(uint32_t m, ModConst *mc);
 
 // Constants for floor(x / d), every x < x_bound (x_bound <= 2^32): if fix is

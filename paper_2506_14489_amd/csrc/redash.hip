@@ -71,7 +71,7 @@ struct LabelBufs {
     }
 };
 
-// Moduli without the fast constants (41..61 and the largest ones): one
+// Moduli without the fast constants (4, 16 and primes from 41 to 61): one
 // residue at a time with 32-bit divisions, in rolled loops; the gadget
 // configurations in use all take the fast path.
 __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
@@ -82,7 +82,7 @@ __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &
     for (uint32_t w = 0; w < mm.W; ++w) {
         const bool last = (w + 1 == mm.W);
         const uint32_t nres = last ? mm.glast : mm.g;
-        uint32_t D = frac_mul_carry(V, last ? mm.pw_last : mm.pw_g);
+        uint32_t D = frac_carry_any(V, last ? mm.pw_last : mm.pw_g);
         const uint32_t rw = next_word(row);
         const uint32_t l = next_word(tgt);
         uint32_t res = 0;
@@ -281,8 +281,10 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
 // Garbler: offsets, zero-labels, garbled rows.
 // ---------------------------------------------------------------------------
 
-// Offsets R_m: digits of rho(1, i) in the radices (m-1, m, m, ...), then
-// residue 0 incremented so that it is a unit of Z_m.  One thread per modulus.
+// Offsets R_m: digits of rho(1, i) in the radices (r0, m, m, ...), then
+// residue 0 mapped to a unit of Z_m (d + 1 for a prime m, r0 = m - 1;
+// 2d + 1 for m = 2^l, r0 = m/2), so that the m colours of a wire are
+// distinct.  One thread per modulus.
 __global__ void __launch_bounds__(64) k_offsets(const Plan P, const SeedKey key, uint32_t *__restrict__ offsets) {
     __shared__ uint32_t TT[kTableWords];
     stage_round_tables(TT, threadIdx.x, 64);
@@ -294,9 +296,9 @@ __global__ void __launch_bounds__(64) k_offsets(const Plan P, const SeedKey key,
     prg_fraction(TT, key.w, 1u, i, V);
     uint32_t words[kMaxW] = {0, 0, 0, 0, 0, 0};
     for (uint32_t r = 0; r < mc.lam; ++r) {
-        const uint32_t radix = r ? mc.m : mc.m - 1;
+        const uint32_t radix = r ? mc.m : mc.r0;
         uint32_t dgt = frac_mul_carry(V, radix);
-        if (r == 0) dgt += 1;
+        if (r == 0) dgt = (mc.r0 == mc.m - 1) ? dgt + 1 : 2 * dgt + 1;
         const uint32_t w = r / mc.g, pos = r % mc.g;
 #pragma unroll
         for (int ww = 0; ww < kMaxW; ++ww)
@@ -310,8 +312,9 @@ __global__ void __launch_bounds__(64) k_offsets(const Plan P, const SeedKey key,
 }
 
 __device__ __forceinline__ uint32_t inverse_unit(uint32_t r, const ModConst &mc) {
-    // r^(m-2) mod m (m prime, r != 0)
-    uint32_t e = mc.m - 2, base = r, acc = 1 % mc.m;
+    // r^(phi - 1) mod m for a unit r, phi the order of the unit group
+    // (m - 1 for a prime, m/2 for a power of two)
+    uint32_t e = mc.phi - 1, base = r, acc = 1 % mc.m;
     while (e) {
         if (e & 1u) acc = mul_mod(acc, base, mc);
         base = mul_mod(base, base, mc);
@@ -654,8 +657,9 @@ __global__ void __launch_bounds__(BLOCK) k_decode(const Plan P, const uint32_t *
             weight *= mc.m;
         }
     }
+    // signed range [-floor(P/2), ceil(P/2) - 1] (Sec. 2.4)
     int64_t out = static_cast<int64_t>(val);
-    if (val >= P.P / 2) out -= static_cast<int64_t>(P.P);
+    if (val >= (P.P + 1) / 2) out -= static_cast<int64_t>(P.P);
     y[a] = out;
     if (!ok) atomicAdd(bad, 1ull);
 }
@@ -816,13 +820,7 @@ int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const ui
 
 int redash_hash_labels(uint32_t q, uint32_t m, uint64_t count, const uint32_t *d_labels, uint32_t gadget_id,
                        const uint64_t *d_tau, uint32_t *d_out, hipStream_t stream) {
-    auto ok_mod = [](uint32_t v) {
-        if (v < 2 || v > 255) return false;
-        for (uint32_t d = 2; d * d <= v; ++d)
-            if (v % d == 0) return false;
-        return true;
-    };
-    if (!ok_mod(q) || !ok_mod(m)) return REDASH_E_PARAM;
+    if (!modulus_ok(q) || !modulus_ok(m)) return REDASH_E_PARAM;
     if (count == 0) return REDASH_OK;
     if (!d_labels || !d_tau || !d_out) return REDASH_E_NULL;
     ModConst mq, mm;

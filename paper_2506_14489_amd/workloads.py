@@ -21,6 +21,16 @@ workloads are synthetic with the shapes and value ranges of CNN layers:
              224x224 (stem, 16 block convs, 3 downsample convs, fc), each
              layer's output drawn from int8 inputs and weights of that layer's
              shape; s cycles 37, 31*37, 29; per-layer seeds 10..30
+
+The short and power-of-two bases of Sec. 4, each scaled by its power of two
+(ScaleQuant+ with s = 2^l), with 2^14 values uniform in the signed range of
+Z_P (the size of the paper's gadget micro-benchmark); P/(2s) is not an
+integer for any of them:
+
+* cpm8-8, cpm8-32 : the first 8 primes with 2 replaced by 2^3 or 2^5
+                    (the micro-benchmark bases), seeds 40, 41
+* short-f         : (32, 167, 173), the short base of model f, seed 42
+* short-F         : (32, 97, 107), the short base of model F, seed 43
 """
 
 from __future__ import annotations
@@ -81,6 +91,28 @@ BATCHED = _conv("batched", PRIMES_12, (11,), 3, (16, 64, 56, 56), 64, 3, 1, 1)
 CONFIGS = [TINY, DENSE, CONV, BATCHED]
 
 
+def _signed_uniform(name, moduli, scale_idx, n, seed):
+    P = 1
+    for m in moduli:
+        P *= m
+    return Workload(name, tuple(moduli), tuple(scale_idx), n, seed, "uniform", -(P // 2), P - P // 2)
+
+
+CPM8_8 = _signed_uniform("cpm8-8", (3, 5, 7, 8, 11, 13, 17, 19), (3,), 1 << 14, 40)
+CPM8_32 = _signed_uniform("cpm8-32", (3, 5, 7, 11, 13, 17, 19, 32), (7,), 1 << 14, 41)
+SHORT_F = _signed_uniform("short-f", (32, 167, 173), (0,), 1 << 14, 42)
+SHORT_BIG_F = _signed_uniform("short-F", (32, 97, 107), (0,), 1 << 14, 43)
+
+SHORT_BASES = [CPM8_8, CPM8_32, SHORT_F, SHORT_BIG_F]
+
+
+def at_size(w: Workload, n: int) -> Workload:
+    """A uniform workload with n values instead of w.n (same base, seed and range)."""
+    if w.kind != "uniform":
+        raise ValueError("only uniform workloads can be resized")
+    return Workload(w.name, w.moduli, w.scale_idx, n, w.seed, w.kind, w.low, w.high)
+
+
 def resnet18_layers():
     """The 21 scaled layers of a ResNet-18 at 224x224, batch 1, in forward
     order, with per-layer seeds 10..30 and s cycling 37, 31*37, 29."""
@@ -111,7 +143,7 @@ RESNET18 = resnet18_layers()
 
 
 def by_name(name: str) -> Workload:
-    for w in CONFIGS + RESNET18:
+    for w in CONFIGS + RESNET18 + SHORT_BASES:
         if w.name == name:
             return w
     raise KeyError(name)

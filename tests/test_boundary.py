@@ -44,6 +44,10 @@ PLAN_CASES = [(w.moduli, w.scale_idx) for w in WL.CONFIGS] + [
     (tuple(WL.PRIMES_12), (10, 11)), (tuple(WL.PRIMES_12), (9,)), ((2, 3), (1,)), ((2, 3, 5), (1, 2)),
     (tuple(rns.first_primes(15)), (13, 14)), (tuple(rns.first_primes(15)), (1, 5, 9)), ((2, 97, 251), (2,)),
     ((2, 3, 5, 7, 11, 13), (1, 2, 3, 4, 5)),
+] + [(w.moduli, w.scale_idx) for w in WL.SHORT_BASES] + [
+    # odd P, and every power of two up to 128 (m = 4 and 16 fill their words)
+    ((3, 5, 7), (1,)), ((3, 5, 7, 11, 13), (0, 4)), ((3, 4, 5), (1,)), ((3, 5, 16), (2,)),
+    ((5, 7, 64), (0,)), ((3, 128, 251), (1,)), ((4, 5, 7), (0, 2)),
 ]
 
 
@@ -70,7 +74,7 @@ def test_work_words(moduli, S):
     assert sz["work_words"] == n * sum(O.words(moduli[i]) for i in R[1:])
 
 
-@pytest.mark.parametrize("m", rns.first_primes(12) + [97, 107, 167, 173, 251])
+@pytest.mark.parametrize("m", rns.first_primes(12) + [97, 107, 167, 173, 251, 4, 8, 16, 32, 64, 128])
 def test_label_words_match_oracle(m):
     assert B.label_words_of(m) == O.words(m)
 
@@ -88,6 +92,11 @@ BAD = [
     ([2, 3, 257], [2]),
     ([2, 3, 5], [3]),
     ([2, 3, 5], []),
+    ([3, 5, 6], [0]),
+    ([2, 3, 32], [2]),
+    ([3, 16, 64], [0]),
+    ([9, 11, 13], [0]),
+    ([3, 5, 256], [0]),
     (list(rns.first_primes(16)), [15]),
 ]
 
@@ -144,7 +153,8 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_garble_scale(ctypes.byref(huge), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_encode(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_decode(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
-    assert L.redash_hash_labels(4, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_hash_labels(6, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_hash_labels(3, 9, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 256, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 5, 1, None, 0, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_eval_scale(None, fake, fake, fake, fake, None) == B.REDASH_E_NULL

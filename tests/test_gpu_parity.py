@@ -32,6 +32,14 @@ def _floor_div(x: np.ndarray, s: int) -> np.ndarray:
     return np.floor_divide(x, s)
 
 
+def _scaled(x: np.ndarray, moduli, S) -> np.ndarray:
+    """What the gadget returns: floor((x + r)/s), r = floor(P/2) mod s
+    (0, i.e. floor(x/s), whenever P/(2s) is an integer; the value-level
+    oracle's reading of the shift constants of Sec. 3.4)."""
+    s = rns.cardinality([moduli[i] for i in S])
+    return np.floor_divide(x + rns.rounding_offset(list(moduli), list(S)), s)
+
+
 def _params_pair(moduli, S, n, seed, a0=0):
     return B.make_params(moduli, S, n, seed, a0), O.make_params(moduli, S, n, seed)
 
@@ -41,7 +49,10 @@ def _params_pair(moduli, S, n, seed, a0=0):
 # ---------------------------------------------------------------------------
 
 HASH_PAIRS = [(2, 3), (3, 2), (37, 2), (2, 37), (11, 13), (5, 3), (37, 31), (17, 19), (97, 251), (251, 97),
-              (3, 5), (7, 37)]
+              (3, 5), (7, 37),
+              # power-of-two moduli (Sec. 4 bases), including 4 and 16 whose fields fill a word
+              (32, 167), (167, 32), (173, 32), (32, 97), (4, 3), (3, 4), (16, 5), (5, 16), (2, 64), (128, 7),
+              (8, 19), (251, 8)]
 
 
 @pytest.mark.parametrize("q,m", HASH_PAIRS)
@@ -81,15 +92,27 @@ SMALL = [
     ("base-2357-by-35", (2, 3, 5, 7), (2, 3), 210, 6, 0),
     ("k2", (2, 3), (1,), 6, 9, 0),
     ("large-moduli", (2, 97, 251), (2,), 300, 12, 3),
+    # the short and power-of-two bases of Sec. 4 (P/(2s) not an integer)
+    ("cpm8-8", WL.CPM8_8.moduli, WL.CPM8_8.scale_idx, 700, 40, 0),
+    ("cpm8-32", WL.CPM8_32.moduli, WL.CPM8_32.scale_idx, 600, 41, 100),
+    ("short-f", WL.SHORT_F.moduli, WL.SHORT_F.scale_idx, 1000, 42, 0),
+    ("short-F", WL.SHORT_BIG_F.moduli, WL.SHORT_BIG_F.scale_idx, 1000, 43, 5),
+    ("odd-P", (3, 5, 7, 11, 13), (0, 4), 500, 50, 0),
+    ("pow2-4-scaled", (3, 4, 5), (1,), 300, 51, 0),
+    ("pow2-4-remaining", (4, 5, 7), (1,), 300, 52, 7),
+    ("pow2-16", (3, 5, 7, 11, 16), (4,), 400, 53, 0),
+    ("pow2-64", (5, 7, 64, 67), (2,), 400, 54, 0),
+    ("pow2-128-product", (3, 128, 251), (0, 1), 400, 55, 0),
 ]
 
 
 def _small_inputs(moduli, n, seed):
     P = rns.cardinality(moduli)
     rng = np.random.default_rng(seed + 1000)
-    x = rng.integers(-(P // 2), P // 2, size=n, dtype=np.int64)
+    lo, hi = -(P // 2), P - P // 2  # the signed range [-floor(P/2), ceil(P/2) - 1]
+    x = rng.integers(lo, hi, size=n, dtype=np.int64)
     if n >= 2:
-        x[0], x[1] = -(P // 2), P // 2 - 1  # both ends of the signed range
+        x[0], x[1] = lo, hi - 1  # both ends of the signed range
     return x
 
 
@@ -122,8 +145,7 @@ def test_eval_on_oracle_tables_matches_oracle(case):
     got = H.to_u32(out)
     assert np.array_equal(got, Y)
     y, bad = O.decode(op, got, zout, offs)
-    s = rns.cardinality([moduli[i] for i in S])
-    assert bad.sum() == 0 and np.array_equal(y, _floor_div(x, s))
+    assert bad.sum() == 0 and np.array_equal(y, _scaled(x, moduli, S))
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
@@ -163,9 +185,8 @@ def test_gpu_pipeline_decodes_floor(case):
     bp = B.make_params(moduli, S, n, seed, a0)
     x = _small_inputs(moduli, n, seed)
     buf = H.gpu_pipeline(bp, x)
-    s = rns.cardinality([moduli[i] for i in S])
     assert int(buf.bad.item()) == 0
-    assert np.array_equal(buf.y.cpu().numpy()[:n], _floor_div(x, s))
+    assert np.array_equal(buf.y.cpu().numpy()[:n], _scaled(x, moduli, S))
 
 
 def test_eval_is_repeatable_and_leaves_inputs():
@@ -216,9 +237,10 @@ def _check_full(w: WL.Workload, n_sample: int):
     bp = B.make_params(w.moduli, w.scale_idx, n, w.seed)
     op = O.make_params(list(w.moduli), list(w.scale_idx), 1, w.seed)
     buf = H.gpu_pipeline(bp, x)
-    # every gadget: decode = floor(x/s) and every label valid
+    # every gadget: decode = floor(x/s) (floor((x + r)/s), see _scaled) and every label valid
+    expect = _scaled(x, w.moduli, w.scale_idx)
     assert int(buf.bad.item()) == 0
-    assert np.array_equal(buf.y.cpu().numpy()[:n], _floor_div(x, w.s))
+    assert np.array_equal(buf.y.cpu().numpy()[:n], expect)
     # sampled gadgets, word for word against the oracle garbling that gadget
     gad = _sample_gadgets(n, w.seed, n_sample)
     gates = O.gate_list(op)
@@ -240,7 +262,7 @@ def _check_full(w: WL.Workload, n_sample: int):
         assert np.array_equal(g_zin[sel], zin), a
         assert np.array_equal(g_zout[sel], zout), a
         # expected evaluator output: output zero-label + floor(x/s) * R
-        Yexp = O.encode(op, np.array([_floor_div(x[a], w.s)]), zout, offs)
+        Yexp = O.encode(op, expect[a:a + 1], zout, offs)
         assert np.array_equal(g_out[sel], Yexp), a
         # rows: gate blocks of (q-1) W words, gadget-major inside each gate
         tsel, base = [], 0
@@ -266,3 +288,15 @@ def test_full_size_batched():
 @pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
 def test_full_size_resnet18_layer(layer):
     _check_full(layer, 24)
+
+
+@pytest.mark.parametrize("w", WL.SHORT_BASES, ids=[w.name for w in WL.SHORT_BASES])
+def test_short_base_micro_benchmark_size(w):
+    """The paper's micro-benchmark size, 2^14 gadgets."""
+    _check_full(w, 128)
+
+
+@pytest.mark.parametrize("w", WL.SHORT_BASES, ids=[w.name for w in WL.SHORT_BASES])
+def test_short_base_at_batched_size(w):
+    """As many gadgets as the 16x64x56x56 map, the size the benchmark times."""
+    _check_full(WL.at_size(w, WL.BATCHED.n), 64)
