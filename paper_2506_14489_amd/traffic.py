@@ -27,9 +27,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15209159.5,  # mean of two dispatches: 15,208,225 and 15,210,094
-        "write_kib": 5048483.0,  # mean of 5,048,521 and 5,048,445
-        "sources_sha256": "0bbe7d589da7d044e13c47826824635ff90064e1a8d43fb1c1f54880f08fb588",
+        "fetch_kib": 15211545.7,  # mean of two dispatches: 15,210,247 and 15,212,844
+        "write_kib": 5049479.0,  # mean of 5,049,628 and 5,049,330
+        "sources_sha256": "eb8e0b936b0cb705748016c5e4da501de551fc4e19b98a8568b5201710d774a1",
     },
 }
 
