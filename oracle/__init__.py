@@ -8,6 +8,9 @@ touch it and fails loudly when its HIP library is missing.
 * ``rns``       -- value-level residue arithmetic (plain Python integers)
 * ``oracle``    -- ctypes wrapper of ``gc_oracle.c`` (plain C: AES-128 from
                    FIPS-197, label hash, PRG, garble, encode, eval, decode)
+* ``linear``    -- garbled dense and conv2d layers on LabelTensors (numpy):
+                   Y = sum w X for the evaluator, Z = sum w Z - b R for the
+                   garbler (Sec. 2.3 free operations)
 
 Parity unpinned by the paper: the exact label bits (hash construction, label
 length, PRG, tweaks, packing).  Those are pinned by FIPS-197 (AES), by the
