@@ -71,6 +71,79 @@ def expected_values(w, x):
     return np.floor_divide(x + (w.P // 2) % w.s, w.s)
 
 
+MFMA_I8_PEAK_TOPS = 5000.0  # dense int8 matrix-core peak of the MI355X, TOP/s
+
+
+def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
+    """The garbled conv layer that produces workload w's activations (Y = sum w X
+    on the labels of its int8 inputs), on the gadget's garbled input labels:
+    prepare the weights, garble the output zero-labels, time the evaluator,
+    decode every output.  Returns a summary dict."""
+    import torch
+
+    from paper_2506_14489_amd import binding as B
+    from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import workloads as WL
+
+    a, wt = WL.layer_operands(w)
+    n, c_in, h, wd = w.in_shape
+    c_out, _, kh, kw = w.w_shape
+    lp = B.make_linear_params(w.moduli, n, c_in, h, wd, c_out, kh, kw, w.stride, w.pad)
+    sz = B.redash_linear_plan(lp)
+    stream = torch.cuda.current_stream()
+    n_in = n * c_in * h * wd
+    assert n_in == params.n, "the layer's inputs reuse the gadget's garbled labels"
+    X = torch.empty_like(buf.in_labels)
+    B.redash_encode(params, torch.from_numpy(a.reshape(-1).astype(np.int64)).to(dev), buf.in_zero, buf.offsets, X,
+                    stream)
+    prep = torch.empty(sz["prepared_bytes"], dtype=torch.uint8, device=dev)
+    B.redash_linear_prepare(lp, torch.from_numpy(wt.astype(np.int32)).to(dev), prep, stream)
+    Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device=dev)
+    Z = torch.empty_like(Y)
+    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, Z, stream)
+    for _ in range(warmup):
+        B.redash_linear_eval(lp, X, prep, Y, stream)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        B.redash_linear_eval(lp, X, prep, Y, stream)
+    ev1.record(stream)
+    g0 = torch.cuda.Event(enable_timing=True)
+    g1 = torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, Z, stream)
+    g1.record(stream)
+    n_out = w.n
+    dp = B.make_params(w.moduli, w.scale_idx, n_out, w.seed)
+    y = torch.empty(n_out, dtype=torch.int64, device=dev)
+    bad = torch.zeros(1, dtype=torch.int64, device=dev)
+    B.redash_decode(dp, Y, Z, buf.offsets, y, bad, stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    ok = int(bad.item()) == 0 and np.array_equal(y.cpu().numpy(), WL.make_inputs(w))
+    if not ok:
+        log("linear layer: decode check FAILED")
+        sys.exit(1)
+    ops = cost.linear_ops_per_output(w.moduli, c_in, kh, kw) * n_out
+    tops = ops / (ms / 1e3) / 1e12
+    gbs = cost.linear_bytes(w.moduli, n_in, n_out) / (ms / 1e3) / 1e9
+    log(f"linear layer: eval {ms:.3f} ms per call, {tops:.0f} TOP/s")
+    return {
+        "layer": f"conv {kh}x{kw} stride {w.stride} pad {w.pad}, {c_in}->{c_out} channels, input {list(w.in_shape)}, "
+                 f"{len(w.moduli)} moduli",
+        "ms_per_call": round(ms, 4),
+        "outputs_per_s": round(n_out / (ms / 1e3), 1),
+        "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOP/s",
+                     "frac": round(tops / MFMA_I8_PEAK_TOPS, 4), "dtype": "i8",
+                     "ops_per_output": cost.linear_ops_per_output(w.moduli, c_in, kh, kw), "kernel": "k_linear"},
+        "hbm": {"achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)},
+        "garble_ms": round(g0.elapsed_time(g1), 4),
+        "check": "decode(eval labels, garbler zero-labels) = exact integer convolution, all outputs",
+        "steps": steps,
+    }
+
+
 def time_short_base(w, steps: int, warmup: int, dev):
     """Garble, encode and time the evaluator on one short-base workload;
     decode and check every gadget afterwards.  Returns a summary dict."""
@@ -133,6 +206,8 @@ def main():
     ap.add_argument("--no-check", action="store_true", help="skip the decode check after timing")
     ap.add_argument("--garble-steps", type=int, default=3,
                     help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
+    ap.add_argument("--no-linear", action="store_true",
+                    help="skip timing the garbled conv layer that produces the workload's activations")
     ap.add_argument("--no-short-bases", action="store_true",
                     help="skip timing the evaluator on the short and power-of-two bases of Sec. 4")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -298,6 +373,8 @@ def main():
         "check": check,
         "garble": garble,
     }
+    if not args.no_linear and w.kind == "conv":
+        result["linear"] = time_linear_layer(w, params, buf, args.steps, args.warmup, dev)
     del buf
     torch.cuda.empty_cache()
     if not args.no_short_bases:

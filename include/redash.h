@@ -210,6 +210,88 @@ int redash_hash_labels(uint32_t q, uint32_t m, uint64_t count, const uint32_t *d
 /* Static text for a return code. */
 const char *redash_strerror(int code);
 
+/* ========================================================================
+ * Garbled linear layers on LabelTensors (the layer that feeds the gadget)
+ * ========================================================================
+ *
+ * Arithmetic garbling makes addition and multiplication by a public constant
+ * free (Sec. 2.3): a dense or 2-D convolution layer with public integer
+ * weights w and bias b, y = W x + b, is evaluated on labels residue by
+ * residue, Y_o = sum_j w_oj X_j mod m, and the garbler, who knows the
+ * offsets R, sets the output zero-labels Z_o = sum_j w_oj Z_j - b_o R, so
+ * that Y_o carries y_o.  The paper runs these layers on LabelTensors with
+ * 32-bit residue arithmetic (Sec. 3.6); here the contraction runs on int8
+ * matrix cores (each residue and each weight reduced mod m fits a signed
+ * byte), with the reduction mod m and the PK32 packing fused into it.
+ *
+ * Layer: input NCHW (batch, c_in, h_in, w_in) of activations, weights OIHW
+ * (c_out, c_in, kh, kw), stride, zero padding `pad` (a padded input is the
+ * public constant 0, whose label is the all-zero label), output NCHW
+ * (batch, c_out, h_out, w_out) with h_out = (h_in + 2 pad - kh)/stride + 1,
+ * w_out likewise.  A dense layer (batch, in) -> (batch, out) is the case
+ * h_in = w_in = kh = kw = 1 (the NCHW and row-major layouts coincide).
+ * Activations are numbered in NCHW order; label tensors use the LabelTensor
+ * layout of the conventions above with n = the number of activations.
+ *
+ *   k, moduli   the RNS base, as in redash_params (primes or powers of two,
+ *               2..255, ascending, pairwise coprime, P < 2^63).
+ *   batch, c_in, h_in, w_in, c_out, kh, kw, stride, pad  the layer, with
+ *               every size >= 1, pad < kh and pad < kw, c_in kh kw <= 32768,
+ *               kh kw <= 64, and at most 2^30 - 1 input and output
+ *               activations.
+ */
+typedef struct {
+    uint32_t k;
+    uint32_t moduli[16];
+    uint32_t batch, c_in, h_in, w_in;
+    uint32_t c_out, kh, kw;
+    uint32_t stride, pad;
+} redash_linear_params;
+
+typedef struct {
+    uint64_t in_label_words;  /* input LabelTensor: batch c_in h_in w_in sum_i W_i   */
+    uint64_t out_label_words; /* output LabelTensor: batch c_out h_out w_out sum_i W_i */
+    uint64_t prepared_bytes;  /* prepared weights (redash_linear_prepare)          */
+    uint32_t h_out, w_out;
+    uint32_t offset_words;    /* the k offsets R_m (redash_linear_garble)          */
+} redash_linear_sizes;
+
+/* Host only.  Validates `p` and reports the sizes.  REDASH_E_NULL, REDASH_E_PARAM. */
+int redash_linear_plan(const redash_linear_params *p, redash_linear_sizes *out);
+
+/*
+ * Once per layer and base (weights are constants of the model): reduces every
+ * weight mod each m_i into the signed range of Z_m_i and lays it out for the
+ * layer kernels (the layout is private to the library; only its size,
+ * prepared_bytes, is public).
+ *   d_weights   c_out c_in kh kw int32 weights, OIHW (any int32 values).
+ *   d_prepared  prepared_bytes, written.
+ */
+int redash_linear_prepare(const redash_linear_params *p, const int32_t *d_weights, uint8_t *d_prepared,
+                          hipStream_t stream);
+
+/*
+ * Evaluator, online: Y = sum w X, every residue of every modulus (Sec. 2.3).
+ *   d_in_labels   in_label_words (read only).
+ *   d_prepared    from redash_linear_prepare with the same params.
+ *   d_out_labels  out_label_words, written; may not alias d_in_labels.
+ */
+int redash_linear_eval(const redash_linear_params *p, const uint32_t *d_in_labels, const uint8_t *d_prepared,
+                       uint32_t *d_out_labels, hipStream_t stream);
+
+/*
+ * Garbler: output zero-labels Z_o = sum w Z - b_o R (Sec. 2.3), so that the
+ * evaluator's output label of activation o carries sum w x + b_o.
+ *   d_in_zero   in_label_words: zero-labels of the layer's inputs.
+ *   d_prepared  from redash_linear_prepare with the same params.
+ *   d_bias      c_out int64 biases, or NULL for none.
+ *   d_offsets   offset_words: the offsets R_m (as from redash_garble_scale).
+ *   d_out_zero  out_label_words, written; may not alias d_in_zero.
+ */
+int redash_linear_garble(const redash_linear_params *p, const uint32_t *d_in_zero, const uint8_t *d_prepared,
+                         const int64_t *d_bias, const uint32_t *d_offsets, uint32_t *d_out_zero,
+                         hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -72,6 +72,49 @@ def make_params(moduli, scale_idx, n: int, seed: int, a0: int = 0) -> Params:
     return p
 
 
+class LinearParams(ctypes.Structure):
+    """Mirror of ``redash_linear_params``."""
+
+    _fields_ = [
+        ("k", ctypes.c_uint32),
+        ("moduli", ctypes.c_uint32 * 16),
+        ("batch", ctypes.c_uint32),
+        ("c_in", ctypes.c_uint32),
+        ("h_in", ctypes.c_uint32),
+        ("w_in", ctypes.c_uint32),
+        ("c_out", ctypes.c_uint32),
+        ("kh", ctypes.c_uint32),
+        ("kw", ctypes.c_uint32),
+        ("stride", ctypes.c_uint32),
+        ("pad", ctypes.c_uint32),
+    ]
+
+
+class LinearSizes(ctypes.Structure):
+    """Mirror of ``redash_linear_sizes``."""
+
+    _fields_ = [
+        ("in_label_words", ctypes.c_uint64),
+        ("out_label_words", ctypes.c_uint64),
+        ("prepared_bytes", ctypes.c_uint64),
+        ("h_out", ctypes.c_uint32),
+        ("w_out", ctypes.c_uint32),
+        ("offset_words", ctypes.c_uint32),
+    ]
+
+
+def make_linear_params(moduli, batch, c_in, h_in, w_in, c_out, kh=1, kw=1, stride=1, pad=0) -> LinearParams:
+    """A conv2d layer (NCHW input, OIHW weights); a dense layer is
+    h_in = w_in = kh = kw = 1."""
+    p = LinearParams()
+    p.k = len(moduli)
+    for i, m in enumerate(moduli):
+        p.moduli[i] = int(m)
+    p.batch, p.c_in, p.h_in, p.w_in = int(batch), int(c_in), int(h_in), int(w_in)
+    p.c_out, p.kh, p.kw, p.stride, p.pad = int(c_out), int(kh), int(kw), int(stride), int(pad)
+    return p
+
+
 _lib = None
 
 
@@ -95,8 +138,14 @@ def lib() -> ctypes.CDLL:
                                          vp, vp, vp]
         L.redash_strerror.argtypes = [ctypes.c_int]
         L.redash_strerror.restype = ctypes.c_char_p
+        lp = ctypes.POINTER(LinearParams)
+        L.redash_linear_plan.argtypes = [lp, ctypes.POINTER(LinearSizes)]
+        L.redash_linear_prepare.argtypes = [lp, vp, vp, vp]
+        L.redash_linear_eval.argtypes = [lp, vp, vp, vp, vp]
+        L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp]
         for name in ("redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale", "redash_decode",
-                     "redash_hash_labels"):
+                     "redash_hash_labels", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
+                     "redash_linear_garble"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,6 +258,52 @@ def redash_hash_labels(q, m, count, labels, gadget_id, tau, out, stream=None):
         int(q), int(m), int(count), _ptr(labels, torch.int32, wq * count, "labels"), int(gadget_id) & 0xFFFFFFFF,
         _ptr(tau, torch.int64, count, "tau"), _ptr(out, torch.int32, wm * count, "out"), _stream(stream)),
         "redash_hash_labels")
+
+
+def redash_linear_plan(params: LinearParams) -> dict:
+    s = LinearSizes()
+    _check(lib().redash_linear_plan(ctypes.byref(params), ctypes.byref(s)), "redash_linear_plan")
+    return {"in_label_words": s.in_label_words, "out_label_words": s.out_label_words,
+            "prepared_bytes": s.prepared_bytes, "h_out": s.h_out, "w_out": s.w_out,
+            "offset_words": s.offset_words}
+
+
+def linear_plan_rc(params: LinearParams) -> int:
+    """Return code of redash_linear_plan (no exception), for validation tests."""
+    s = LinearSizes()
+    return lib().redash_linear_plan(ctypes.byref(params), ctypes.byref(s))
+
+
+def redash_linear_prepare(params, weights, prepared, stream=None):
+    import torch
+
+    sz = redash_linear_plan(params)
+    nw = params.c_out * params.c_in * params.kh * params.kw
+    _check(lib().redash_linear_prepare(
+        ctypes.byref(params), _ptr(weights, torch.int32, nw, "weights"),
+        _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"), _stream(stream)), "redash_linear_prepare")
+
+
+def redash_linear_eval(params, in_labels, prepared, out_labels, stream=None):
+    import torch
+
+    sz = redash_linear_plan(params)
+    _check(lib().redash_linear_eval(
+        ctypes.byref(params), _ptr(in_labels, torch.int32, sz["in_label_words"], "in_labels"),
+        _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"),
+        _ptr(out_labels, torch.int32, sz["out_label_words"], "out_labels"), _stream(stream)), "redash_linear_eval")
+
+
+def redash_linear_garble(params, in_zero, prepared, bias, offsets, out_zero, stream=None):
+    import torch
+
+    sz = redash_linear_plan(params)
+    _check(lib().redash_linear_garble(
+        ctypes.byref(params), _ptr(in_zero, torch.int32, sz["in_label_words"], "in_zero"),
+        _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"),
+        _ptr(bias, torch.int64, params.c_out, "bias"),
+        _ptr(offsets, torch.int32, sz["offset_words"], "offsets"),
+        _ptr(out_zero, torch.int32, sz["out_label_words"], "out_zero"), _stream(stream)), "redash_linear_garble")
 
 
 def label_words_of(m: int) -> int:

@@ -120,3 +120,19 @@ def garble_ops_per_gadget(moduli, scale_idx) -> int:
             per_value += LIMB_OPS_PER_WORD * words(m) + OPS_PER_RESIDUE * lam(m)
         total += q * per_value
     return total
+
+
+# ---------------------------------------------------------------------------
+# Garbled linear layer (Y = sum w X on every residue), per output activation:
+#   * int8 matrix-core operations: 2 per multiply-add, c_in kh kw of them for
+#     each residue of each of the k labels: 2 c_in kh kw sum_m lambda_m;
+#   * algorithmic HBM bytes per launch: the input labels read once and the
+#     output labels written once, 4 sum_m W_m bytes per activation each (the
+#     prepared weights, under 0.5 MB for a 3x3x64x64 layer, are left out).
+# ---------------------------------------------------------------------------
+def linear_ops_per_output(moduli, c_in: int, kh: int, kw: int) -> int:
+    return 2 * c_in * kh * kw * sum(lam(m) for m in moduli)
+
+
+def linear_bytes(moduli, n_in: int, n_out: int) -> int:
+    return 4 * sum(words(m) for m in moduli) * (n_in + n_out)

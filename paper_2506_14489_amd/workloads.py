@@ -169,19 +169,29 @@ def _exact_conv_int8(a: np.ndarray, w: np.ndarray, stride: int, pad: int) -> np.
     return xi
 
 
+def layer_operands(w: Workload):
+    """The int8 input activations (in_shape) and int8 weights (w_shape) of a
+    conv or fc workload: the operands of the linear layer whose outputs are
+    the workload's activations."""
+    if w.kind not in ("conv", "fc"):
+        raise ValueError("only conv and fc workloads come from a layer")
+    rng = np.random.default_rng(w.seed)
+    a = rng.integers(-128, 128, size=w.in_shape, dtype=np.int8)
+    wt = rng.integers(-128, 128, size=w.w_shape, dtype=np.int8)
+    return a, wt
+
+
 def make_inputs(w: Workload) -> np.ndarray:
     """The activations x (int64, flattened NCHW) of a workload."""
     rng = np.random.default_rng(w.seed)
     if w.kind == "uniform":
         x = rng.integers(w.low, w.high, size=w.n, dtype=np.int64)
     elif w.kind == "conv":
-        a = rng.integers(-128, 128, size=w.in_shape, dtype=np.int8)
-        wt = rng.integers(-128, 128, size=w.w_shape, dtype=np.int8)
+        a, wt = layer_operands(w)
         x = _exact_conv_int8(a, wt, w.stride, w.pad).reshape(-1)
     elif w.kind == "fc":
-        a = rng.integers(-128, 128, size=w.in_shape, dtype=np.int8).astype(np.int64)
-        wt = rng.integers(-128, 128, size=w.w_shape, dtype=np.int8).astype(np.int64)
-        x = (a @ wt.T).reshape(-1)
+        a, wt = layer_operands(w)
+        x = (a.astype(np.int64) @ wt.astype(np.int64).T).reshape(-1)
     else:  # pragma: no cover
         raise ValueError(w.kind)
     assert x.shape == (w.n,)

@@ -17,7 +17,8 @@ from paper_2506_14489_amd import workloads as WL
 def test_library_exports_every_declared_symbol():
     names = B.declared_symbols()
     assert set(names) == {"redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale",
-                          "redash_decode", "redash_hash_labels", "redash_strerror"}
+                          "redash_decode", "redash_hash_labels", "redash_strerror", "redash_linear_plan",
+                          "redash_linear_prepare", "redash_linear_eval", "redash_linear_garble"}
     L = B.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -158,3 +159,77 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_hash_labels(3, 256, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 5, 1, None, 0, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_eval_scale(None, fake, fake, fake, fake, None) == B.REDASH_E_NULL
+
+
+# ---------------------------------------------------------------------------
+# garbled linear layers
+# ---------------------------------------------------------------------------
+
+def test_linear_structs_match_header():
+    # k, moduli[16], batch, c_in, h_in, w_in, c_out, kh, kw, stride, pad: 26 uint32
+    assert ctypes.sizeof(B.LinearParams) == 4 * 26
+    # in/out label words, prepared bytes (8-byte), h_out, w_out, offset_words (4-byte), padded to 8
+    assert ctypes.sizeof(B.LinearSizes) == 40
+    assert B.LinearSizes.h_out.offset == 24
+
+
+LINEAR_CASES = [
+    # moduli, batch, c_in, h, w, c_out, kh, kw, stride, pad
+    (WL.PRIMES_12, 16, 64, 56, 56, 64, 3, 3, 1, 1),
+    (WL.PRIMES_12, 1, 3, 224, 224, 64, 7, 7, 2, 3),
+    (WL.PRIMES_12, 1, 64, 56, 56, 128, 1, 1, 2, 0),
+    (WL.PRIMES_12, 1, 512, 1, 1, 1000, 1, 1, 1, 0),
+    ((32, 167, 173), 7, 10, 5, 6, 3, 2, 3, 1, 1),
+    ((2, 3, 5), 1, 1, 1, 1, 1, 1, 1, 1, 0),
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_CASES)
+def test_linear_plan_sizes(case):
+    from oracle import linear as OL
+
+    moduli, n, c_in, h, w, c_out, kh, kw, stride, pad = case
+    sz = B.redash_linear_plan(B.make_linear_params(moduli, n, c_in, h, w, c_out, kh, kw, stride, pad))
+    W = sum(OL.label_words(m) for m in moduli)
+    _, _, ho, wo = OL.conv_out_shape(n, c_in, h, w, c_out, kh, kw, stride, pad)
+    assert (sz["h_out"], sz["w_out"]) == (ho, wo)
+    assert sz["in_label_words"] == n * c_in * h * w * W
+    assert sz["out_label_words"] == n * c_out * ho * wo * W
+    assert sz["offset_words"] == W
+    assert sz["prepared_bytes"] >= len(moduli) * c_out * c_in * kh * kw
+
+
+LINEAR_BAD = [
+    ((2, 3, 6), 1, 4, 4, 4, 2, 3, 3, 1, 1),        # 6 is not a prime or a power of two
+    ((2, 3, 4), 1, 4, 4, 4, 2, 3, 3, 1, 1),        # 2 and 4 not coprime
+    ((3, 2), 1, 4, 4, 4, 2, 3, 3, 1, 1),           # not ascending
+    ((2, 3), 0, 4, 4, 4, 2, 3, 3, 1, 1),           # empty batch
+    ((2, 3), 1, 0, 4, 4, 2, 3, 3, 1, 1),
+    ((2, 3), 1, 4, 4, 4, 0, 3, 3, 1, 1),
+    ((2, 3), 1, 4, 4, 4, 2, 3, 3, 0, 1),           # stride 0
+    ((2, 3), 1, 4, 4, 4, 2, 3, 3, 1, 3),           # pad >= kernel
+    ((2, 3), 1, 4, 2, 2, 2, 5, 5, 1, 1),           # kernel larger than the padded input
+    ((2, 3), 1, 4, 20, 20, 2, 9, 9, 1, 1),         # more than 64 taps
+    ((2, 3), 1, 4096, 4, 4, 2, 3, 3, 1, 1),        # c_in kh kw > 32768
+    ((2, 3), 1024, 64, 128, 128, 2, 1, 1, 1, 0),   # 2^30 input activations
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_BAD)
+def test_linear_bad_params_rejected(case):
+    assert B.linear_plan_rc(B.make_linear_params(*case)) == B.REDASH_E_PARAM
+
+
+def test_linear_entry_points_validate_before_any_device_work():
+    L = B.lib()
+    fake = ctypes.c_void_p(4096)
+    bad = B.make_linear_params((2, 3, 6), 1, 4, 4, 4, 2, 3, 3, 1, 1)
+    good = B.make_linear_params((2, 3, 5), 1, 4, 4, 4, 2, 3, 3, 1, 1)
+    assert L.redash_linear_plan(None, ctypes.byref(B.LinearSizes())) == B.REDASH_E_NULL
+    assert L.redash_linear_prepare(ctypes.byref(bad), fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_linear_eval(ctypes.byref(bad), fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_linear_garble(ctypes.byref(bad), fake, fake, None, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_linear_prepare(ctypes.byref(good), None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_eval(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_eval(ctypes.byref(good), fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_linear_garble(ctypes.byref(good), fake, fake, None, None, fake, None) == B.REDASH_E_NULL

@@ -1,0 +1,171 @@
+"""GPU parity of the garbled linear layers (redash_linear_*) against the
+linear-layer oracle (oracle/linear.py), bit for bit.
+
+Small layers: every word of the evaluator's output labels and of the
+garbler's output zero-labels is compared with the oracle, over shapes that
+cover dense layers, strides, padding, several channel chunks, several groups
+of 64 output channels, ragged tiles, power-of-two and large moduli.  Full-size
+layers (the 3x3x64 convolution that produces the 16x64x56x56 batched map, and
+ResNet-18 layers) run end to end on the GPU: every output decodes to the
+exact integer convolution, and a seeded sample of output labels is compared
+with the oracle item by item.
+"""
+
+from __future__ import annotations
+
+import zlib
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import linear as OL  # noqa: E402
+from paper_2506_14489_amd import binding as B  # noqa: E402
+from paper_2506_14489_amd import workloads as WL  # noqa: E402
+
+import gpu_helpers as H  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU containers
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+
+def _dev_u8(n):
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device="cuda")
+
+
+def _random_labels(moduli, count, rng):
+    return OL.pack(moduli, [rng.integers(0, m, size=(count, OL.label_lambda(m))) for m in moduli], count)
+
+
+SMALL = [
+    # name, moduli, (batch, c_in, h, w), c_out, kh, kw, stride, pad
+    ("conv3x3-12primes", tuple(WL.PRIMES_12), (2, 5, 6, 7), 3, 3, 3, 1, 1),
+    ("conv3x3-wide-row", (2, 3, 5, 7, 11), (1, 16, 3, 70), 8, 3, 3, 1, 1),
+    ("conv-stride2", (3, 5, 7, 32), (1, 20, 9, 18), 6, 3, 3, 2, 1),
+    ("stem-like-7x7s2", (5, 7, 11), (1, 3, 20, 21), 9, 7, 7, 2, 3),
+    ("conv-chunks-and-groups", (2, 251), (1, 130, 3, 4), 70, 3, 3, 1, 1),
+    ("conv-1x1-stride2", (13, 16, 17), (2, 17, 6, 6), 5, 1, 1, 2, 0),
+    ("conv-2x3-nopad", (4, 5, 7), (1, 4, 5, 6), 3, 2, 3, 1, 0),
+    ("dense", tuple(WL.PRIMES_12), (33, 100, 1, 1), 70, 1, 1, 1, 0),
+    ("dense-batch1", (32, 167, 173), (1, 512, 1, 1), 10, 1, 1, 1, 0),
+    ("short-base-conv", (32, 97, 107), (1, 64, 5, 5), 64, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_linear_matches_oracle(case):
+    name, moduli, shape, c_out, kh, kw, stride, pad = case
+    n, c_in, h, w = shape
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    lp = B.make_linear_params(moduli, n, c_in, h, w, c_out, kh, kw, stride, pad)
+    sz = B.redash_linear_plan(lp)
+    count_in = n * c_in * h * w
+    X = _random_labels(moduli, count_in, rng)
+    Z = _random_labels(moduli, count_in, rng)
+    R = _random_labels(moduli, 1, rng)
+    wts = rng.integers(-2 ** 31, 2 ** 31, size=(c_out, c_in, kh, kw), dtype=np.int64)
+    wts[:, :, 0, 0] = rng.integers(-3, 4, size=(c_out, c_in))  # small weights too
+    bias = rng.integers(-2 ** 62, 2 ** 62, size=c_out, dtype=np.int64)
+    prep = _dev_u8(sz["prepared_bytes"])
+    B.redash_linear_prepare(lp, H.to_dev(wts.astype(np.int32)), prep)
+    out = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    B.redash_linear_eval(lp, H.to_dev(X), prep, out)
+    zout = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    B.redash_linear_garble(lp, H.to_dev(Z), prep, H.to_dev(bias), H.to_dev(R), zout)
+    torch.cuda.synchronize()
+    w32 = wts.astype(np.int32).astype(np.int64)  # the int32 weights the library was given
+    assert np.array_equal(H.to_u32(out), OL.conv_labels(moduli, X, shape, w32, stride, pad))
+    assert np.array_equal(H.to_u32(zout), OL.garble_conv(moduli, Z, shape, w32, bias, R, stride, pad))
+
+
+def test_linear_garble_without_bias_and_repeatability():
+    moduli = (2, 3, 5, 7, 11, 13)
+    shape, c_out = (1, 8, 5, 5), 4
+    rng = np.random.default_rng(3)
+    lp = B.make_linear_params(moduli, *shape, c_out, 3, 3, 1, 1)
+    sz = B.redash_linear_plan(lp)
+    Z = _random_labels(moduli, int(np.prod(shape)), rng)
+    R = _random_labels(moduli, 1, rng)
+    wts = rng.integers(-50, 50, size=(c_out, shape[1], 3, 3))
+    prep = _dev_u8(sz["prepared_bytes"])
+    B.redash_linear_prepare(lp, H.to_dev(wts.astype(np.int32)), prep)
+    zout = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    zd = H.to_dev(Z)
+    B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), zout)
+    torch.cuda.synchronize()
+    first = H.to_u32(zout).copy()
+    assert np.array_equal(first, OL.garble_conv(moduli, Z, shape, wts, None, R, 1, 1))
+    for _ in range(3):
+        B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), zout)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.to_u32(zout), first)
+    assert np.array_equal(H.to_u32(zd), Z)
+
+
+# ---------------------------------------------------------------------------
+# full-size layers on the GPU: garble inputs with the gadget garbler's PRG,
+# encode the int8 activations, run the layer both ways, decode every output
+# ---------------------------------------------------------------------------
+
+def _check_full_layer(w: WL.Workload, n_sample: int):
+    a, wt = WL.layer_operands(w)
+    moduli = w.moduli
+    if w.kind == "fc":
+        batch, c_in = w.in_shape
+        lp = B.make_linear_params(moduli, batch, c_in, 1, 1, w.w_shape[0])
+        shape, kshape = (batch, c_in, 1, 1), (w.w_shape[0], c_in, 1, 1)
+    else:
+        n, c_in, h, wd = w.in_shape
+        c_out, _, kh, kw = w.w_shape
+        lp = B.make_linear_params(moduli, n, c_in, h, wd, c_out, kh, kw, w.stride, w.pad)
+        shape, kshape = w.in_shape, w.w_shape
+    sz = B.redash_linear_plan(lp)
+    n_in, n_out = int(np.prod(shape)), w.n
+    # input zero-labels and offsets from the gadget garbler (its PRG over n_in items)
+    gp_in = B.make_params(moduli, w.scale_idx, n_in, w.seed)
+    g = B.Buffers(gp_in)
+    B.redash_garble_scale(gp_in, g.offsets, g.in_zero, g.out_zero, g.tables, g.work)
+    xa = torch.from_numpy(a.reshape(-1).astype(np.int64)).cuda()
+    B.redash_encode(gp_in, xa, g.in_zero, g.offsets, g.in_labels)
+    zin, X, offsets = g.in_zero, g.in_labels, g.offsets
+    del g
+    torch.cuda.empty_cache()
+    wts = torch.from_numpy(wt.reshape(kshape).astype(np.int32)).cuda()
+    prep = _dev_u8(sz["prepared_bytes"])
+    B.redash_linear_prepare(lp, wts, prep)
+    Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    Zo = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    B.redash_linear_eval(lp, X, prep, Y)
+    B.redash_linear_garble(lp, zin, prep, None, offsets, Zo)
+    # decode every output with the gadget library's decode (any scale set of the base)
+    gp_out = B.make_params(moduli, w.scale_idx, n_out, w.seed)
+    y = torch.empty(n_out, dtype=torch.int64, device="cuda")
+    bad = torch.zeros(1, dtype=torch.int64, device="cuda")
+    B.redash_decode(gp_out, Y, Zo, offsets, y, bad)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 0
+    assert np.array_equal(y.cpu().numpy(), WL.make_inputs(w))
+    # sampled output labels against the oracle, item by item
+    rng = np.random.default_rng(w.seed + 99)
+    items = np.unique(np.concatenate([np.arange(8), np.arange(n_out - 8, n_out),
+                                      rng.choice(n_out, size=min(n_sample, n_out), replace=False)]))
+    # the oracle needs the input labels of the receptive fields: fetch the whole input tensor
+    Xh = H.to_u32(X)
+    exp = OL.conv_labels_sampled(moduli, Xh, shape, wt.reshape(kshape).astype(np.int64),
+                                 1 if w.kind == "fc" else w.stride, 0 if w.kind == "fc" else w.pad, items)
+    li = H.label_index(moduli, n_out, items)
+    assert np.array_equal(H.gather(Y, li), exp)
+
+
+def test_full_size_batched_map_layer():
+    """The 3x3x64 convolution producing the 16x64x56x56 batched map (12 primes)."""
+    _check_full_layer(WL.BATCHED, 48)
+
+
+@pytest.mark.parametrize("layer", [WL.RESNET18[0], WL.RESNET18[7], WL.RESNET18[16], WL.RESNET18[-1]],
+                         ids=lambda w: w.name)
+def test_full_size_resnet18_layer(layer):
+    _check_full_layer(layer, 24)
