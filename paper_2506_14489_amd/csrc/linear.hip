@@ -15,13 +15,13 @@
 //   * The int32 accumulators are reduced mod m in the epilogue and the
 //     residues are packed straight into PK32 words.
 //
-// One workgroup (4 waves) computes, for one modulus i and one packed word w
-// of its labels, a tile of 64 output channels x XT output positions of one
-// output row.  Wave q takes residue j0 + q of the word; its 64 x XT tile is
-// 4 x (XT/16) MFMA 16x16x64 tiles.  Per channel chunk the weights (64
-// channels x the chunk's K bytes) and the four residues' input halos are
-// staged in LDS; the output words are merged across the waves in LDS and
-// stored coalesced.
+// One workgroup (4 waves) computes, for one modulus i, a tile of 64 output
+// channels x XT output positions of one output row, packed word by packed
+// word of the labels.  Wave q takes residue j0 + q of the word; its 64 x XT
+// tile is 4 x (XT/16) MFMA 16x16x64 tiles.  Per channel chunk the weights (64
+// channels x the chunk's K bytes; staged once per modulus when there is one
+// chunk) and the four residues' input halos are staged in LDS; the output
+// words are merged across the waves in LDS and stored coalesced.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
@@ -36,15 +36,15 @@ namespace {
 constexpr int kLinBlock = 256;      // 4 waves
 constexpr int kLinOTile = 64;       // output channels per workgroup
 constexpr uint32_t kLinMaxLds = 160 * 1024;
-constexpr uint32_t kLinMaxK = 32768;  // c_in kh kw: |sum w v| < 2^30
+constexpr uint32_t kLinMaxK = 16384;  // c_in kh kw: |sum w v| < 127 * 250 * 2^14 < 2^29
 constexpr uint32_t kLinMaxTaps = 64;
-constexpr uint32_t kLinMaxPairs = 96;  // (modulus, word) pairs: sum of W <= 15 * 6
+constexpr uint32_t kLinTwoPerCu = 80 * 1024;  // LDS bytes that let two workgroups share a CU
 
 struct LinMod {
     uint32_t m, b, g, W, glast;
     uint32_t woff;                // word offset of this modulus's block (in units of n)
     uint32_t divM, divS, div_fix; // floor(u / m) for every 32-bit u
-    uint32_t off;                 // m ceil(2^30 / m): makes every sum non-negative
+    uint32_t off;                 // m ceil(2^29 / m): makes every sum non-negative
 };
 
 struct LinPlan {
@@ -57,13 +57,16 @@ struct LinPlan {
     uint32_t xt, xtiles;          // output positions per tile, tiles per row
     uint32_t ck, kc, taps, ncc;   // channel chunk, K bytes per chunk (64-padded), kh kw, chunks
     uint32_t o_pad, ogroups;      // c_out rounded up to 64, its groups of 64
-    uint32_t xstride, xw;         // LDS bytes per staged input column; staged columns
+    uint32_t xw;                  // staged input columns per row
+    uint32_t xw_magic;            // floor(e / xw) = umulhi(e, xw_magic) for every staged item index e
+    uint32_t kw_magic;            // floor(t / kw) = umulhi(t, kw_magic) for every tap t < 64
+    uint32_t lg_ck, lg_c16n;      // log2 ck, log2 (ck / 16)
+    uint32_t swz_shift, swz_mask; // 16-byte chunk swizzle of a staged column (see k_linear)
+    uint32_t ostride;             // words per output-channel row of the merged output words
     uint32_t astride;             // LDS bytes per staged weight row
     uint32_t lds_a, lds_b, lds_bytes;
-    uint32_t npairs;
     uint64_t n_in, n_out;         // activations
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
-    uint8_t pair_mod[kLinMaxPairs], pair_word[kLinMaxPairs];
     LinMod mod[kMaxK];
 };
 
@@ -82,7 +85,14 @@ uint32_t round_up(uint32_t v, uint32_t q) { return (v + q - 1) / q * q; }
 uint32_t halo_bytes(const LinPlan &L, uint32_t xt, uint32_t *xw_out) {
     const uint32_t xw = (xt - 1) * L.stride + L.kw;
     if (xw_out) *xw_out = xw;
-    return L.kh * xw * L.xstride;
+    return L.kh * xw * L.ck;
+}
+
+// LDS bytes of a workgroup with tiles of xt positions: the weights, then the
+// four residues' halos (reused for the output words at the end).
+uint32_t lds_for(const LinPlan &L, uint32_t xt) {
+    const uint32_t hb = 4 * halo_bytes(L, xt, nullptr), ob = kLinOTile * (xt + 4) * 4;
+    return L.lds_a + (hb > ob ? hb : ob);
 }
 
 int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
@@ -161,35 +171,39 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     L->ncc = (p->c_in + ck - 1) / ck;
     L->o_pad = round_up(p->c_out, kLinOTile);
     L->ogroups = L->o_pad / kLinOTile;
-    // 16-byte fragment reads of 8 consecutive columns hit distinct banks
-    L->xstride = ck == 16 ? 16 : ck + 16;
+    // A staged column holds ck channel bytes in ck/16 chunks of 16; chunk q of
+    // column x sits at q ^ ((x >> swz_shift) & swz_mask), so that the 16-byte
+    // reads of 8 consecutive columns fall in 8 distinct 4-bank groups.
+    L->swz_mask = ck / 16 - 1;
+    L->swz_shift = ck == 64 ? 1 : ck == 32 ? 2 : 3;
+    // weight rows padded by 16 bytes: 8 consecutive rows in distinct bank groups
     L->astride = L->kc + 16;
     L->lds_a = kLinOTile * L->astride;
-    // widest tile (64, 32 or 16 positions) whose LDS image fits
+    // Tile width: 64, 32 or 16 positions, no wider than the row needs; the
+    // widest that lets two workgroups share a CU, else the widest that fits.
+    uint32_t need = 16;
+    while (need < 64 && need < L->cols) need *= 2;
     L->xt = 0;
-    for (uint32_t xt = 64; xt >= 16; xt /= 2) {
-        const uint32_t hb = 4 * halo_bytes(*L, xt, nullptr);
-        const uint32_t ob = kLinOTile * xt * 4;
-        const uint32_t b = hb > ob ? hb : ob;
-        if (L->lds_a + b <= kLinMaxLds) {
-            L->xt = xt;
-            L->lds_b = b;
-            break;
-        }
-    }
+    for (uint32_t xt = need; xt >= 16 && !L->xt; xt /= 2)
+        if (lds_for(*L, xt) <= kLinTwoPerCu) L->xt = xt;
+    for (uint32_t xt = need; xt >= 16 && !L->xt; xt /= 2)
+        if (lds_for(*L, xt) <= kLinMaxLds) L->xt = xt;
     if (!L->xt) return REDASH_E_PARAM;
-    // narrower tiles for narrow rows
-    while (L->xt > 16 && L->xt / 2 >= L->cols) {
-        L->xt /= 2;
-        const uint32_t hb = 4 * halo_bytes(*L, L->xt, nullptr);
-        const uint32_t ob = kLinOTile * L->xt * 4;
-        L->lds_b = hb > ob ? hb : ob;
-    }
     halo_bytes(*L, L->xt, &L->xw);
-    L->lds_bytes = L->lds_a + L->lds_b;
+    // with M = ceil(2^32 / d), umulhi(e, M) = floor(e / d) whenever e d < 2^32
+    // (the error e (M d - 2^32) / (d 2^32) < e / 2^32 stays below 1/d):
+    // e < kh (ck/16) xw <= 64 * 4 * 133 for the items, t < 64 for the taps
+    if (static_cast<uint64_t>(L->kh) * (ck / 16) * L->xw * L->xw >= (1ull << 32)) return REDASH_E_PARAM;
+    L->xw_magic = static_cast<uint32_t>(((1ull << 32) + L->xw - 1) / L->xw);
+    L->kw_magic = static_cast<uint32_t>(((1ull << 32) + p->kw - 1) / p->kw);
+    L->lg_ck = ck == 64 ? 6 : ck == 32 ? 5 : 4;
+    L->lg_c16n = L->lg_ck - 4;
+    L->ostride = L->xt + 4;  // the four lane groups of an atomic OR fall 16 banks apart
+    L->lds_bytes = lds_for(*L, L->xt);
+    L->lds_b = L->lds_bytes - L->lds_a;
     L->xtiles = (L->cols + L->xt - 1) / L->xt;
 
-    uint32_t woff = 0, np = 0;
+    uint32_t woff = 0;
     for (uint32_t i = 0; i < p->k; ++i) {
         ModConst mc;
         fill_mod_const(p->moduli[i], &mc);
@@ -201,16 +215,10 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         lm.glast = mc.glast;
         lm.woff = woff;
         woff += mc.W;
-        division_constants(mc.m, 1ull << 32, &lm.divM, &lm.divS, &lm.div_fix);
-        lm.off = static_cast<uint32_t>(((1ull << 30) + mc.m - 1) / mc.m * mc.m);
-        for (uint32_t w = 0; w < mc.W; ++w) {
-            if (np >= kLinMaxPairs) return REDASH_E_PARAM;
-            L->pair_mod[np] = static_cast<uint8_t>(i);
-            L->pair_word[np] = static_cast<uint8_t>(w);
-            ++np;
-        }
+        // every u below 2^31 (see the epilogue): the multiply-shift needs no fix-up
+        division_constants(mc.m, 1ull << 31, &lm.divM, &lm.divS, &lm.div_fix);
+        lm.off = static_cast<uint32_t>(((1ull << 29) + mc.m - 1) / mc.m * mc.m);
     }
-    L->npairs = np;
     L->rowsum_off = static_cast<uint64_t>(L->k) * L->ncc * L->o_pad * L->kc;
     return REDASH_OK;
 }
@@ -289,173 +297,204 @@ __global__ void __launch_bounds__(kLinBlock) k_linear(const LinPlan L, const uin
     extern __shared__ __align__(16) uint8_t lds[];
     uint8_t *Al = lds;
     uint8_t *Bl = lds + L.lds_a;
-    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a);  // after the last compute
+    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a);  // after a word's last compute
 
     const uint32_t tid = threadIdx.x, lane = tid % 64;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid / 64);
-    const uint32_t tile = blockIdx.x, pair = blockIdx.y, og = blockIdx.z;
+    const uint32_t tile = blockIdx.x, i = blockIdx.y, og = blockIdx.z;
     const uint32_t xtile = tile % L.xtiles;
     const uint32_t row = (tile / L.xtiles) % L.rows;
     const uint32_t img = tile / (L.xtiles * L.rows);
-    const uint32_t i = L.pair_mod[pair], w = L.pair_word[pair];
     const LinMod M = L.mod[i];
-    const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
-    const uint32_t XT = 16 * NCB;
+    constexpr uint32_t XT = 16 * NCB;
     const uint32_t x0 = xtile * XT;
-    const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
     const int32_t *rowsum = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
-    const uint32_t halo = L.kh * L.xw * L.xstride;  // bytes per residue
+    const uint32_t rowb = L.xw * L.ck;  // bytes per staged row of one residue
+    const uint32_t halo = L.kh * rowb;  // bytes per residue
     const uint32_t mask = (1u << M.b) - 1u;
+    const uint32_t ksteps = L.kc / 64;
+    const uint32_t kg = 16 * (lane / 16);
 
-    // output channel of element r of tile row-block ob for this lane
+    // output channel of element r of row block ob for this lane
     auto o_local = [&](int ob, int r) -> uint32_t { return ob * 16 + 4 * (lane / 16) + r; };
+    // byte offset of channel byte c (a multiple of 4) of staged column x
+    auto col_off = [&](uint32_t x, uint32_t c) -> uint32_t {
+        return x * L.ck + ((((c >> 4) ^ (x >> L.swz_shift)) & L.swz_mask) << 4) + (c & 15u);
+    };
 
-    // garbler: -b_o mod m for this lane's 16 output channels
+    // 128 * row sum per lane row (restores sum w v from sum w (v - 128)), and
+    // for the garbler -b_o mod m
+    int32_t rs[4][4];
     uint32_t negb[4][4];
-    if constexpr (GARBLE) {
-#pragma unroll
-        for (int ob = 0; ob < 4; ++ob)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const uint32_t o = og * kLinOTile + o_local(ob, r);
-                uint32_t v = 0;
-                if (bias && o < L.c_out) {
-                    int64_t bm = bias[o] % static_cast<int64_t>(M.m);
-                    if (bm < 0) bm += M.m;
-                    v = (M.m - static_cast<uint32_t>(bm)) % M.m;
-                }
-                negb[ob][r] = v;
-            }
-    }
-
-    uint32_t part[4][NCB][4];
 #pragma unroll
     for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
+        for (int r = 0; r < 4; ++r) {
+            rs[ob][r] = M.m > 128 ? 128 * rowsum[o_local(ob, r)] : 0;
+            negb[ob][r] = 0;
+            if constexpr (GARBLE) {
+                const uint32_t o = og * kLinOTile + o_local(ob, r);
+                if (bias && o < L.c_out) {
+                    int64_t bm = bias[o] % static_cast<int64_t>(M.m);
+                    if (bm < 0) bm += M.m;
+                    negb[ob][r] = (M.m - static_cast<uint32_t>(bm)) % M.m;
+                }
+            }
+        }
 
-    const uint32_t ksteps = L.kc / 64;
-    for (uint32_t j0 = 0; j0 < g; j0 += 4) {
-        v4i acc[4][NCB];
+    const int32_t ybase = static_cast<int32_t>(row * L.stride) - static_cast<int32_t>(L.pad);
+    const int32_t xbase = static_cast<int32_t>(x0 * L.stride) - static_cast<int32_t>(L.pad);
+    const uint32_t c16n = L.ck / 16;
+    const uint32_t items = L.kh * c16n * L.xw;
+    const bool full16 = L.c_in % 16 == 0;
+    // residues of moduli up to 128 are valid signed bytes as they are; above
+    // that they enter as v - 128 (v XOR 0x80), and 128 * rowsum restores sum w v
+    const bool shifted = M.m > 128;
+    const uint32_t flip = shifted ? 0x80808080u : 0u;
+    bool a_staged = false;
+
+    for (uint32_t w = 0; w < M.W; ++w) {
+        const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
+        const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
+        uint32_t part[4][NCB][4];
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) acc[ob][cb] = v4i{0, 0, 0, 0};
-        for (uint32_t cc = 0; cc < L.ncc; ++cc) {
-            __syncthreads();  // the previous chunk's fragments have been read
-            if (L.ncc > 1 || j0 == 0) {
-                // weights of this chunk: 64 rows of kc bytes, 16 bytes per load
-                const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad +
-                                            og * kLinOTile) * L.kc;
-                const uint32_t per_row = L.kc / 16;
-                for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
-                    const uint32_t rr = e / per_row, q = e % per_row;
-                    *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
-                        *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
-                }
-            }
-            // input halos of residues j0 .. j0+3: item (row r, 4 channels, column xin)
-            {
-                const uint32_t c4n = L.ck / 4;
-                const uint32_t items = L.kh * c4n * L.xw;
-                const int32_t ybase = static_cast<int32_t>(row * L.stride) - static_cast<int32_t>(L.pad);
-                const int32_t xbase = static_cast<int32_t>(x0 * L.stride) - static_cast<int32_t>(L.pad);
-                for (uint32_t e = tid; e < items; e += kLinBlock) {
-                    const uint32_t xin = e % L.xw;
-                    const uint32_t c4 = (e / L.xw) % c4n;
-                    const uint32_t r = e / (L.xw * c4n);
-                    const int32_t y = ybase + static_cast<int32_t>(r), x = xbase + static_cast<int32_t>(xin);
-                    const bool inside = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
-                                        x < static_cast<int32_t>(L.in_cols);
-                    uint32_t wd[4] = {0, 0, 0, 0};
-                    if (inside) {
-                        const uint32_t c0 = cc * L.ck + 4 * c4;
-                        const uint32_t a0 = img * L.sN + static_cast<uint32_t>(y) * L.sY +
-                                            static_cast<uint32_t>(x) * L.sX + c0 * L.sC;
+            for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            if (c0 + q < L.c_in) wd[q] = src[a0 + q * L.sC];
+                for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
+
+        for (uint32_t j0 = 0; j0 < g; j0 += 4) {
+            v4i acc[4][NCB];
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) acc[ob][cb] = v4i{0, 0, 0, 0};
+            for (uint32_t cc = 0; cc < L.ncc; ++cc) {
+                __syncthreads();  // the previous fragments (and output words) have been read
+                if (L.ncc > 1 || !a_staged) {
+                    // weights of this chunk: 64 rows of kc bytes, 16 bytes per load
+                    const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad +
+                                                og * kLinOTile) * L.kc;
+                    const uint32_t per_row = L.kc / 16;
+                    for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
+                        const uint32_t rr = e / per_row, q = e % per_row;
+                        *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
+                            *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
                     }
-                    uint8_t *dst = Bl + r * (L.xw * L.xstride) + xin * L.xstride + 4 * c4;
+                    a_staged = true;
+                }
+                // input halos of residues j0 .. j0+3; an item is (row r, 16 channels,
+                // column xin): 16 loads in flight, then one 16-byte store per residue
+                for (uint32_t e = tid; e < items; e += kLinBlock) {
+                    const uint32_t q1 = __umulhi(e, L.xw_magic);  // e / xw
+                    const uint32_t xin = e - q1 * L.xw;
+                    const uint32_t c16 = q1 & (c16n - 1u);
+                    const uint32_t r = q1 >> L.lg_c16n;
+                    const int32_t y = ybase + static_cast<int32_t>(r), x = xbase + static_cast<int32_t>(xin);
+                    const uint32_t c0 = cc * L.ck + 16 * c16;
+                    const bool valid = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
+                                       x < static_cast<int32_t>(L.in_cols) && c0 < L.c_in;
+                    uint32_t wd[16];
+                    if (valid) {
+                        const uint32_t *sp = src + (img * L.sN + static_cast<uint32_t>(y) * L.sY +
+                                                    static_cast<uint32_t>(x) * L.sX + c0 * L.sC);
+                        if (full16) {
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const uint32_t j = j0 + q;
-                        if (j < g) {
-                            const uint32_t sh = M.b * j;
-                            const uint32_t f0 = (wd[0] >> sh) & mask, f1 = (wd[1] >> sh) & mask;
-                            const uint32_t f2 = (wd[2] >> sh) & mask, f3 = (wd[3] >> sh) & mask;
-                            const uint32_t packed = (f0 | (f1 << 8) | (f2 << 16) | (f3 << 24)) ^ 0x80808080u;
-                            *reinterpret_cast<uint32_t *>(dst + q * halo) = packed;
+                            for (int q = 0; q < 16; ++q) wd[q] = sp[q * L.sC];
+                        } else {
+                            // channels past c_in meet zero weights: read any valid one
+                            const uint32_t last = L.c_in - 1 - c0;
+#pragma unroll
+                            for (int q = 0; q < 16; ++q) wd[q] = sp[(static_cast<uint32_t>(q) < last ? static_cast<uint32_t>(q) : last) * L.sC];
+                        }
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) wd[q] = 0;
+                    }
+                    const uint32_t dsto = r * rowb + xin * L.ck + (((c16 ^ (xin >> L.swz_shift)) & L.swz_mask) << 4);
+#pragma unroll
+                    for (int jq = 0; jq < 4; ++jq) {
+                        if (j0 + jq < g) {
+                            const uint32_t sh = M.b * (j0 + jq);
+                            uint4 v;
+                            uint32_t *vv = reinterpret_cast<uint32_t *>(&v);
+#pragma unroll
+                            for (int d = 0; d < 4; ++d) {
+                                const uint32_t f0 = __builtin_amdgcn_ubfe(wd[4 * d], sh, M.b);
+                                const uint32_t f1 = __builtin_amdgcn_ubfe(wd[4 * d + 1], sh, M.b);
+                                const uint32_t f2 = __builtin_amdgcn_ubfe(wd[4 * d + 2], sh, M.b);
+                                const uint32_t f3 = __builtin_amdgcn_ubfe(wd[4 * d + 3], sh, M.b);
+                                vv[d] = (f0 | (f1 << 8) | (f2 << 16) | (f3 << 24)) ^ flip;
+                            }
+                            *reinterpret_cast<uint4 *>(Bl + jq * halo + dsto) = v;
+                        }
+                    }
+                }
+                __syncthreads();
+                if (j0 + wave < g) {
+                    const uint8_t *Bw = Bl + wave * halo;
+                    for (uint32_t kk = 0; kk < ksteps; ++kk) {
+                        v4i a[4];
+#pragma unroll
+                        for (int ob = 0; ob < 4; ++ob)
+                            a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 +
+                                                                   kg);
+                        const uint32_t kidx = kk * 64 + kg;
+                        uint32_t tap = kidx >> L.lg_ck;
+                        const uint32_t coff = kidx & (L.ck - 1u);
+                        if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
+                        const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+#pragma unroll
+                        for (int cb = 0; cb < NCB; ++cb) {
+                            const uint32_t xcol = (cb * 16 + lane % 16) * L.stride + dx;
+                            const v4i bf = *reinterpret_cast<const v4i *>(Bw + dy * rowb + col_off(xcol, coff));
+#pragma unroll
+                            for (int ob = 0; ob < 4; ++ob)
+                                acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
                         }
                     }
                 }
             }
-            __syncthreads();
+            // epilogue of residue j0 + wave: u = sum w v + m ceil(2^29/m) (+ (-b mod m) R_j)
+            // lies in [0, 2^31); its residue mod m goes into the field
             if (j0 + wave < g) {
-                const uint8_t *Bw = Bl + wave * halo;
-                const uint32_t kg = 16 * (lane / 16);
-                for (uint32_t kk = 0; kk < ksteps; ++kk) {
-                    v4i a[4];
+                const uint32_t j = j0 + wave, sh = M.b * j;
+                uint32_t Rj = 0;
+                if constexpr (GARBLE) Rj = (offsets[M.woff + w] >> sh) & mask;
 #pragma unroll
-                    for (int ob = 0; ob < 4; ++ob)
-                        a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 + kg);
-                    const uint32_t kidx = kk * 64 + kg;
-                    uint32_t tap = kidx / L.ck;
-                    const uint32_t coff = kidx % L.ck;
-                    if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
-                    const uint32_t dy = tap / L.kw, dx = tap % L.kw;
+                for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-                    for (int cb = 0; cb < NCB; ++cb) {
-                        const uint32_t xcol = (cb * 16 + lane % 16) * L.stride + dx;
-                        const v4i bf = *reinterpret_cast<const v4i *>(Bw + dy * (L.xw * L.xstride) +
-                                                                       xcol * L.xstride + coff);
+                    for (int r = 0; r < 4; ++r) {
+                        uint32_t extra = static_cast<uint32_t>(rs[ob][r]) + M.off;
+                        if constexpr (GARBLE) extra += negb[ob][r] * Rj;
 #pragma unroll
-                        for (int ob = 0; ob < 4; ++ob)
-                            acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                        for (int cb = 0; cb < NCB; ++cb) {
+                            const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]) + extra;
+                            part[ob][cb][r] |= (u - lin_div(u, M) * M.m) << sh;
+                        }
                     }
-                }
             }
         }
-        // epilogue of residue j0 + wave: sum w v = acc + 128 rowsum, reduce mod m, insert the field
-        if (j0 + wave < g) {
-            const uint32_t j = j0 + wave, sh = M.b * j;
-            uint32_t Rj = 0;
-            if constexpr (GARBLE) Rj = (offsets[M.woff + w] >> sh) & mask;
+        // merge the waves' fields (disjoint bits) and store whole words
+        __syncthreads();
+        for (uint32_t e = tid; e < kLinOTile * L.ostride; e += kLinBlock) Ol[e] = 0;
+        __syncthreads();
 #pragma unroll
-            for (int ob = 0; ob < 4; ++ob)
+        for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int32_t rs = 128 * rowsum[o_local(ob, r)];
-                    uint32_t extra = M.off;
-                    if constexpr (GARBLE) extra += negb[ob][r] * Rj;
+            for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-                    for (int cb = 0; cb < NCB; ++cb) {
-                        const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r] + rs) + extra;
-                        const uint32_t res = u - lin_div(u, M) * M.m;
-                        part[ob][cb][r] |= res << sh;
-                    }
-                }
+                for (int r = 0; r < 4; ++r)
+                    if (part[ob][cb][r])
+                        atomicOr(&Ol[o_local(ob, r) * L.ostride + cb * 16 + lane % 16], part[ob][cb][r]);
+        __syncthreads();
+        uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out;
+        for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) {
+            const uint32_t ol = e / XT, xl = e % XT;
+            const uint32_t o = og * kLinOTile + ol, x = x0 + xl;
+            if (o < L.c_out && x < L.cols) dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
         }
-    }
-    // merge the waves' fields (disjoint bits) and store whole words
-    __syncthreads();
-    for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) Ol[e] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int ob = 0; ob < 4; ++ob)
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                if (part[ob][cb][r]) atomicOr(&Ol[o_local(ob, r) * XT + cb * 16 + lane % 16], part[ob][cb][r]);
-    __syncthreads();
-    uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out;
-    for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) {
-        const uint32_t ol = e / XT, xl = e % XT;
-        const uint32_t o = og * kLinOTile + ol, x = x0 + xl;
-        if (o < L.c_out && x < L.cols) dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[e];
     }
 }
 
@@ -478,7 +517,7 @@ int launch_linear_ncb(const LinPlan &L, const uint32_t *in, const uint8_t *prep,
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear<NCB, GARBLE>), dim3(static_cast<uint32_t>(tiles), L.npairs, L.ogroups),
+    hipLaunchKernelGGL((k_linear<NCB, GARBLE>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
                        dim3(kLinBlock), L.lds_bytes, stream, L, in, prep, bias, offsets, out);
     return lin_launched();
 }
