@@ -97,22 +97,23 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     B.redash_encode(params, torch.from_numpy(a.reshape(-1).astype(np.int64)).to(dev), buf.in_zero, buf.offsets, X,
                     stream)
     prep = torch.empty(sz["prepared_bytes"], dtype=torch.uint8, device=dev)
+    work = torch.empty(sz["work_bytes"], dtype=torch.uint8, device=dev)
     B.redash_linear_prepare(lp, torch.from_numpy(wt.astype(np.int32)).to(dev), prep, stream)
     Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device=dev)
     Z = torch.empty_like(Y)
-    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, Z, stream)
+    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
     for _ in range(warmup):
-        B.redash_linear_eval(lp, X, prep, Y, stream)
+        B.redash_linear_eval(lp, X, prep, work, Y, stream)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     for _ in range(steps):
-        B.redash_linear_eval(lp, X, prep, Y, stream)
+        B.redash_linear_eval(lp, X, prep, work, Y, stream)
     ev1.record(stream)
     g0 = torch.cuda.Event(enable_timing=True)
     g1 = torch.cuda.Event(enable_timing=True)
     g0.record(stream)
-    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, Z, stream)
+    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
     g1.record(stream)
     n_out = w.n
     dp = B.make_params(w.moduli, w.scale_idx, n_out, w.seed)

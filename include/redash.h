@@ -222,7 +222,9 @@ const char *redash_strerror(int code);
  * that Y_o carries y_o.  The paper runs these layers on LabelTensors with
  * 32-bit residue arithmetic (Sec. 3.6); here the contraction runs on int8
  * matrix cores (each residue and each weight reduced mod m fits a signed
- * byte), with the reduction mod m and the PK32 packing fused into it.
+ * byte): the input residues are unpacked once into byte planes in a
+ * caller-provided working buffer, and the reduction mod m and the PK32
+ * packing are fused into the contraction.
  *
  * Layer: input NCHW (batch, c_in, h_in, w_in) of activations, weights OIHW
  * (c_out, c_in, kh, kw), stride, zero padding `pad` (a padded input is the
@@ -252,6 +254,7 @@ typedef struct {
     uint64_t in_label_words;  /* input LabelTensor: batch c_in h_in w_in sum_i W_i   */
     uint64_t out_label_words; /* output LabelTensor: batch c_out h_out w_out sum_i W_i */
     uint64_t prepared_bytes;  /* prepared weights (redash_linear_prepare)          */
+    uint64_t work_bytes;      /* working buffer of redash_linear_eval / _garble    */
     uint32_t h_out, w_out;
     uint32_t offset_words;    /* the k offsets R_m (redash_linear_garble)          */
 } redash_linear_sizes;
@@ -274,10 +277,14 @@ int redash_linear_prepare(const redash_linear_params *p, const int32_t *d_weight
  * Evaluator, online: Y = sum w X, every residue of every modulus (Sec. 2.3).
  *   d_in_labels   in_label_words (read only).
  *   d_prepared    from redash_linear_prepare with the same params.
+ *   d_work        work_bytes of working storage: every input residue as a
+ *                 byte, one zero-padded channel-last plane per (modulus,
+ *                 residue).  Contents on entry are ignored and on return
+ *                 unspecified.
  *   d_out_labels  out_label_words, written; may not alias d_in_labels.
  */
 int redash_linear_eval(const redash_linear_params *p, const uint32_t *d_in_labels, const uint8_t *d_prepared,
-                       uint32_t *d_out_labels, hipStream_t stream);
+                       uint8_t *d_work, uint32_t *d_out_labels, hipStream_t stream);
 
 /*
  * Garbler: output zero-labels Z_o = sum w Z - b_o R (Sec. 2.3), so that the
@@ -286,10 +293,11 @@ int redash_linear_eval(const redash_linear_params *p, const uint32_t *d_in_label
  *   d_prepared  from redash_linear_prepare with the same params.
  *   d_bias      c_out int64 biases, or NULL for none.
  *   d_offsets   offset_words: the offsets R_m (as from redash_garble_scale).
+ *   d_work      work_bytes of working storage, as for redash_linear_eval.
  *   d_out_zero  out_label_words, written; may not alias d_in_zero.
  */
 int redash_linear_garble(const redash_linear_params *p, const uint32_t *d_in_zero, const uint8_t *d_prepared,
-                         const int64_t *d_bias, const uint32_t *d_offsets, uint32_t *d_out_zero,
+                         const int64_t *d_bias, const uint32_t *d_offsets, uint8_t *d_work, uint32_t *d_out_zero,
                          hipStream_t stream);
 
 #ifdef __cplusplus

@@ -97,6 +97,7 @@ class LinearSizes(ctypes.Structure):
         ("in_label_words", ctypes.c_uint64),
         ("out_label_words", ctypes.c_uint64),
         ("prepared_bytes", ctypes.c_uint64),
+        ("work_bytes", ctypes.c_uint64),
         ("h_out", ctypes.c_uint32),
         ("w_out", ctypes.c_uint32),
         ("offset_words", ctypes.c_uint32),
@@ -141,8 +142,8 @@ def lib() -> ctypes.CDLL:
         lp = ctypes.POINTER(LinearParams)
         L.redash_linear_plan.argtypes = [lp, ctypes.POINTER(LinearSizes)]
         L.redash_linear_prepare.argtypes = [lp, vp, vp, vp]
-        L.redash_linear_eval.argtypes = [lp, vp, vp, vp, vp]
-        L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp]
+        L.redash_linear_eval.argtypes = [lp, vp, vp, vp, vp, vp]
+        L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp, vp]
         for name in ("redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale", "redash_decode",
                      "redash_hash_labels", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
                      "redash_linear_garble"):
@@ -264,7 +265,7 @@ def redash_linear_plan(params: LinearParams) -> dict:
     s = LinearSizes()
     _check(lib().redash_linear_plan(ctypes.byref(params), ctypes.byref(s)), "redash_linear_plan")
     return {"in_label_words": s.in_label_words, "out_label_words": s.out_label_words,
-            "prepared_bytes": s.prepared_bytes, "h_out": s.h_out, "w_out": s.w_out,
+            "prepared_bytes": s.prepared_bytes, "work_bytes": s.work_bytes, "h_out": s.h_out, "w_out": s.w_out,
             "offset_words": s.offset_words}
 
 
@@ -284,17 +285,18 @@ def redash_linear_prepare(params, weights, prepared, stream=None):
         _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"), _stream(stream)), "redash_linear_prepare")
 
 
-def redash_linear_eval(params, in_labels, prepared, out_labels, stream=None):
+def redash_linear_eval(params, in_labels, prepared, work, out_labels, stream=None):
     import torch
 
     sz = redash_linear_plan(params)
     _check(lib().redash_linear_eval(
         ctypes.byref(params), _ptr(in_labels, torch.int32, sz["in_label_words"], "in_labels"),
         _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"),
+        _ptr(work, torch.uint8, sz["work_bytes"], "work"),
         _ptr(out_labels, torch.int32, sz["out_label_words"], "out_labels"), _stream(stream)), "redash_linear_eval")
 
 
-def redash_linear_garble(params, in_zero, prepared, bias, offsets, out_zero, stream=None):
+def redash_linear_garble(params, in_zero, prepared, bias, offsets, work, out_zero, stream=None):
     import torch
 
     sz = redash_linear_plan(params)
@@ -303,6 +305,7 @@ def redash_linear_garble(params, in_zero, prepared, bias, offsets, out_zero, str
         _ptr(prepared, torch.uint8, sz["prepared_bytes"], "prepared"),
         _ptr(bias, torch.int64, params.c_out, "bias"),
         _ptr(offsets, torch.int32, sz["offset_words"], "offsets"),
+        _ptr(work, torch.uint8, sz["work_bytes"], "work"),
         _ptr(out_zero, torch.int32, sz["out_label_words"], "out_zero"), _stream(stream)), "redash_linear_garble")
 
 

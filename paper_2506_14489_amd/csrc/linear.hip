@@ -4,24 +4,28 @@
 // (Sec. 2.3): Y_o = sum_j w_oj X_j mod m, residue by residue, and the garbler
 // sets Z_o = sum_j w_oj Z_j - b_o R.  Every residue of every label is an
 // independent convolution with the same weights, so the layer is one dense
-// integer contraction per (modulus, packed word): int8 matrix cores do it.
+// integer contraction per (modulus, residue): int8 matrix cores do it.
 //
 //   * A weight acts through its residue mod m; reduced into the signed range
 //     of Z_m it fits a signed byte for every m <= 255 (|w| <= 127).
-//   * A residue v in [0, m) enters as the byte v - 128 (v XOR 0x80), so the
-//     inputs need no per-modulus centring; the contraction then yields
-//     sum w (v - 128) and adding 128 * sum_k w (the row sums, prepared with
-//     the weights) restores sum w v exactly.
-//   * The int32 accumulators are reduced mod m in the epilogue and the
-//     residues are packed straight into PK32 words.
+//   * A residue v < m <= 128 is a valid signed byte as it is; for m > 128 it
+//     enters as v - 128 (v XOR 0x80), and adding 128 * sum_k w (the row sums,
+//     prepared with the weights) restores sum w v exactly.
 //
-// One workgroup (4 waves) computes, for one modulus i, a tile of 64 output
-// channels x XT output positions of one output row, packed word by packed
-// word of the labels.  Wave q takes residue j0 + q of the word; its 64 x XT
-// tile is 4 x (XT/16) MFMA 16x16x64 tiles.  Per channel chunk the weights (64
-// channels x the chunk's K bytes; staged once per modulus when there is one
-// chunk) and the four residues' input halos are staged in LDS; the output
-// words are merged across the waves in LDS and stored coalesced.
+// Two kernels per call:
+//   k_linear_unpack  reads the packed input labels once and writes every
+//                    residue as a byte into residue planes in the caller's
+//                    working buffer: plane (i, r) holds residue r of modulus
+//                    i for every input position, channel-last with the zero
+//                    padding already in place, so that a 16-byte load gives a
+//                    matrix-core fragment of 16 channels (HBM-bound);
+//   k_linear_gemm    per workgroup: one modulus, 64 output channels and a row
+//                    segment of XT (32 or 16) output positions; wave q takes
+//                    residue j0 + q of each packed word, 4 x (XT/16) MFMA 16x16x64
+//                    tiles, the weights staged in LDS, the input fragments
+//                    loaded from the planes; the int32 sums are reduced mod m
+//                    and the residues of a word merged across the waves in LDS
+//                    into PK32 words, stored coalesced.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
@@ -36,15 +40,18 @@ namespace {
 constexpr int kLinBlock = 256;      // 4 waves
 constexpr int kLinOTile = 64;       // output channels per workgroup
 constexpr uint32_t kLinMaxLds = 160 * 1024;
-constexpr uint32_t kLinMaxK = 16384;  // c_in kh kw: |sum w v| < 127 * 250 * 2^14 < 2^29
+constexpr uint32_t kLinMaxK = 16384;  // c_in kh kw (the epilogue bounds below)
 constexpr uint32_t kLinMaxTaps = 64;
-constexpr uint32_t kLinTwoPerCu = 80 * 1024;  // LDS bytes that let two workgroups share a CU
+constexpr uint32_t kLinMaxPairs = 96;  // (modulus, packed word) pairs: sum of W <= 15 * 6
+constexpr int kXcds = 8;               // MI355X: workgroups go round-robin to 8 XCDs
 
 struct LinMod {
     uint32_t m, b, g, W, glast;
-    uint32_t woff;                // word offset of this modulus's block (in units of n)
-    uint32_t divM, divS, div_fix; // floor(u / m) for every 32-bit u
-    uint32_t off;                 // m ceil(2^29 / m): makes every sum non-negative
+    uint32_t woff;     // word offset of this modulus's block (in units of n)
+    uint32_t lam_off;  // planes of the earlier moduli: sum of their lambda
+    // floor(u / m) = umulhi(u, divM) >> divS for every u the epilogue sees
+    uint32_t divM, divS;
+    uint32_t off;      // a multiple of m above |sum w v|: keeps u >= 0
 };
 
 struct LinPlan {
@@ -54,19 +61,23 @@ struct LinPlan {
     uint32_t rows, cols, nimg;    // output rows, columns, images (dense: 1, batch, 1)
     uint32_t sN, sC, sY, sX;      // input activation index = img sN + c sC + y sY + x sX
     uint32_t oN, oO, oY, oX;      // output activation index, likewise
+    uint32_t hp, wp, cp;          // plane rows and columns (padded) and channels (ncc ck)
     uint32_t xt, xtiles;          // output positions per tile, tiles per row
     uint32_t ck, kc, taps, ncc;   // channel chunk, K bytes per chunk (64-padded), kh kw, chunks
-    uint32_t o_pad, ogroups;      // c_out rounded up to 64, its groups of 64
-    uint32_t xw;                  // staged input columns per row
-    uint32_t xw_magic;            // floor(e / xw) = umulhi(e, xw_magic) for every staged item index e
+    uint32_t lg_ck;
     uint32_t kw_magic;            // floor(t / kw) = umulhi(t, kw_magic) for every tap t < 64
-    uint32_t lg_ck, lg_c16n;      // log2 ck, log2 (ck / 16)
-    uint32_t swz_shift, swz_mask; // 16-byte chunk swizzle of a staged column (see k_linear)
-    uint32_t ostride;             // words per output-channel row of the merged output words
+    uint32_t o_pad, ogroups;      // c_out rounded up to 64, its groups of 64
     uint32_t astride;             // LDS bytes per staged weight row
-    uint32_t lds_a, lds_b, lds_bytes;
+    uint32_t ostride;             // words per output-channel row of the merged output words
+    uint32_t xw, xstride;         // staged input columns of a tile; LDS bytes per staged column
+    uint32_t halo;                // LDS bytes of one residue's staged input (kh xw xstride)
+    uint32_t lds_a, lds_b, lds_o, lds_bytes;
+    uint32_t npairs;
     uint64_t n_in, n_out;         // activations
+    uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
+    uint32_t total_lam;           // planes: sum of lambda over the base
+    uint8_t pair_mod[kLinMaxPairs], pair_word[kLinMaxPairs];
     LinMod mod[kMaxK];
 };
 
@@ -80,20 +91,6 @@ uint32_t gcd32(uint32_t a, uint32_t b) {
 }
 
 uint32_t round_up(uint32_t v, uint32_t q) { return (v + q - 1) / q * q; }
-
-// LDS bytes of one residue's input halo for a tile of xt positions.
-uint32_t halo_bytes(const LinPlan &L, uint32_t xt, uint32_t *xw_out) {
-    const uint32_t xw = (xt - 1) * L.stride + L.kw;
-    if (xw_out) *xw_out = xw;
-    return L.kh * xw * L.ck;
-}
-
-// LDS bytes of a workgroup with tiles of xt positions: the weights, then the
-// four residues' halos (reused for the output words at the end).
-uint32_t lds_for(const LinPlan &L, uint32_t xt) {
-    const uint32_t hb = 4 * halo_bytes(L, xt, nullptr), ob = kLinOTile * (xt + 4) * 4;
-    return L.lds_a + (hb > ob ? hb : ob);
-}
 
 int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     if (!p || !L) return REDASH_E_NULL;
@@ -167,43 +164,43 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     uint32_t ck = 64;
     while (ck > 16 && (ck / 2 >= cin16 || round_up(L->taps * ck, 64) > 1024)) ck /= 2;
     L->ck = ck;
+    L->lg_ck = ck == 64 ? 6 : ck == 32 ? 5 : 4;
     L->kc = round_up(L->taps * ck, 64);
     L->ncc = (p->c_in + ck - 1) / ck;
+    L->cp = L->ncc * ck;
+    L->hp = L->in_rows + 2 * p->pad;
+    L->wp = L->in_cols + 2 * p->pad;
+    // with M = ceil(2^32 / kw), umulhi(t, M) = floor(t / kw) whenever t kw < 2^32
+    L->kw_magic = static_cast<uint32_t>(((1ull << 32) + p->kw - 1) / p->kw);
     L->o_pad = round_up(p->c_out, kLinOTile);
     L->ogroups = L->o_pad / kLinOTile;
-    // A staged column holds ck channel bytes in ck/16 chunks of 16; chunk q of
-    // column x sits at q ^ ((x >> swz_shift) & swz_mask), so that the 16-byte
-    // reads of 8 consecutive columns fall in 8 distinct 4-bank groups.
-    L->swz_mask = ck / 16 - 1;
-    L->swz_shift = ck == 64 ? 1 : ck == 32 ? 2 : 3;
-    // weight rows padded by 16 bytes: 8 consecutive rows in distinct bank groups
+    // weight rows padded by 16 bytes: 8 consecutive rows fall in distinct bank groups
     L->astride = L->kc + 16;
     L->lds_a = kLinOTile * L->astride;
-    // Tile width: 64, 32 or 16 positions, no wider than the row needs; the
-    // widest that lets two workgroups share a CU, else the widest that fits.
-    uint32_t need = 16;
-    while (need < 64 && need < L->cols) need *= 2;
-    L->xt = 0;
-    for (uint32_t xt = need; xt >= 16 && !L->xt; xt /= 2)
-        if (lds_for(*L, xt) <= kLinTwoPerCu) L->xt = xt;
-    for (uint32_t xt = need; xt >= 16 && !L->xt; xt /= 2)
-        if (lds_for(*L, xt) <= kLinMaxLds) L->xt = xt;
-    if (!L->xt) return REDASH_E_PARAM;
-    halo_bytes(*L, L->xt, &L->xw);
-    // with M = ceil(2^32 / d), umulhi(e, M) = floor(e / d) whenever e d < 2^32
-    // (the error e (M d - 2^32) / (d 2^32) < e / 2^32 stays below 1/d):
-    // e < kh (ck/16) xw <= 64 * 4 * 133 for the items, t < 64 for the taps
-    if (static_cast<uint64_t>(L->kh) * (ck / 16) * L->xw * L->xw >= (1ull << 32)) return REDASH_E_PARAM;
-    L->xw_magic = static_cast<uint32_t>(((1ull << 32) + L->xw - 1) / L->xw);
-    L->kw_magic = static_cast<uint32_t>(((1ull << 32) + p->kw - 1) / p->kw);
-    L->lg_ck = ck == 64 ? 6 : ck == 32 ? 5 : 4;
-    L->lg_c16n = L->lg_ck - 4;
+    // Staged input: per residue kh rows of xw columns of ck channel bytes,
+    // columns padded to xstride (16-byte accesses of 8 consecutive columns
+    // then fall in distinct bank groups; ck = 16 needs no padding).
+    L->xstride = ck == 16 ? 16 : ck + 16;
+    // tile width: 32 or 16 positions, no wider than the row needs (64 would
+    // not fit the registers of two waves per SIMD), and at most 512 staged
+    // 16-byte pieces per residue (two per thread)
+    L->xt = 32;
+    while (L->xt > 16 && L->xt / 2 >= L->cols) L->xt /= 2;
+    auto pieces = [&](uint32_t xt) { return L->kh * ((xt - 1) * p->stride + p->kw) * (ck / 16); };
+    if (L->xt == 32 && pieces(32) > 2 * kLinBlock) L->xt = 16;
+    if (pieces(L->xt) > 2 * kLinBlock) return REDASH_E_PARAM;
+    L->xw = (L->xt - 1) * p->stride + p->kw;
+    L->halo = L->kh * L->xw * L->xstride;
     L->ostride = L->xt + 4;  // the four lane groups of an atomic OR fall 16 banks apart
-    L->lds_bytes = lds_for(*L, L->xt);
-    L->lds_b = L->lds_bytes - L->lds_a;
+    L->lds_b = 4 * L->halo;
+    L->lds_o = kLinOTile * L->ostride * 4;
+    L->lds_bytes = L->lds_a + L->lds_b + L->lds_o;
+    if (L->lds_bytes > kLinMaxLds) return REDASH_E_PARAM;
     L->xtiles = (L->cols + L->xt - 1) / L->xt;
+    L->plane_bytes = static_cast<uint64_t>(L->nimg) * L->hp * L->wp * L->cp;
+    if (L->plane_bytes >= (1ull << 32)) return REDASH_E_PARAM;  // 32-bit offsets within a plane
 
-    uint32_t woff = 0;
+    uint32_t woff = 0, lam_off = 0, np = 0;
     for (uint32_t i = 0; i < p->k; ++i) {
         ModConst mc;
         fill_mod_const(p->moduli[i], &mc);
@@ -214,16 +211,41 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         lm.W = mc.W;
         lm.glast = mc.glast;
         lm.woff = woff;
+        lm.lam_off = lam_off;
         woff += mc.W;
-        // every u below 2^31 (see the epilogue): the multiply-shift needs no fix-up
-        division_constants(mc.m, 1ull << 31, &lm.divM, &lm.divS, &lm.div_fix);
-        lm.off = static_cast<uint32_t>(((1ull << 29) + mc.m - 1) / mc.m * mc.m);
+        lam_off += mc.lam;
+        // |sum w v| <= K floor(m/2) (m - 1) =: B (signed weights, residues v < m);
+        // u = sum w v + off (+ (-b mod m) R_j, below m^2) lies in [0, 2B + m^2),
+        // below 2^31 for K <= 16384, and u / m < 2^23 (a signed 24-bit product)
+        const uint64_t K = static_cast<uint64_t>(L->taps) * p->c_in;
+        const uint64_t B = K * (mc.m / 2) * (mc.m - 1);
+        lm.off = static_cast<uint32_t>((B + mc.m - 1) / mc.m * mc.m);
+        const uint64_t u_max = lm.off + B + static_cast<uint64_t>(mc.m) * mc.m;
+        if (u_max >= (1ull << 31) || u_max / mc.m >= (1ull << 23)) return REDASH_E_PARAM;
+        if (u_max * mc.m < (1ull << 32)) {
+            lm.divM = static_cast<uint32_t>(((1ull << 32) + mc.m - 1) / mc.m);  // exact: u m < 2^32
+            lm.divS = 0;
+        } else {
+            uint32_t fix = 0;
+            division_constants(mc.m, 1ull << 31, &lm.divM, &lm.divS, &fix);
+            if (fix) return REDASH_E_PARAM;  // not reached: below 2^31 the round-up method is exact
+        }
+        for (uint32_t w = 0; w < mc.W; ++w) {
+            if (np >= kLinMaxPairs) return REDASH_E_PARAM;
+            L->pair_mod[np] = static_cast<uint8_t>(i);
+            L->pair_word[np] = static_cast<uint8_t>(w);
+            ++np;
+        }
     }
+    L->npairs = np;
+    L->total_lam = lam_off;
     L->rowsum_off = static_cast<uint64_t>(L->k) * L->ncc * L->o_pad * L->kc;
     return REDASH_OK;
 }
 
 uint64_t prepared_bytes(const LinPlan &L) { return L.rowsum_off + 4ull * L.k * L.o_pad; }
+
+uint64_t work_bytes(const LinPlan &L) { return static_cast<uint64_t>(L.total_lam) * L.plane_bytes; }
 
 uint32_t total_words(const LinPlan &L) {
     uint32_t t = 0;
@@ -279,29 +301,91 @@ __global__ void __launch_bounds__(256) k_linear_rowsums(const LinPlan L, const i
 }
 
 // ---------------------------------------------------------------------------
-// The layer kernel.
+// Residue planes.  Plane q = lam_off_i + r (residue r of modulus i) holds
+// plane_bytes bytes: position (img, yp, xp) of the zero-padded input at
+// ((img hp + yp) wp + xp) cp, its cp channel bytes after it.  A byte is the
+// residue v (m <= 128) or v XOR 0x80 (m > 128); padding holds the byte of
+// v = 0, channels past c_in meet zero weights.
 // ---------------------------------------------------------------------------
-typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t lin_div(uint32_t u, const LinMod &M) {
-    const uint32_t t = __umulhi(u, M.divM);
-    return M.div_fix ? (t + ((u - t) >> 1)) >> M.divS : t >> M.divS;
+// A word at byte offset `off` (below 2^32) of a uniform base: the offset stays
+// a 32-bit VGPR next to a scalar base address.
+__device__ __forceinline__ uint32_t load_word(const uint32_t *base, uint32_t off) {
+    asm("" : "+v"(off));
+    return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(base) + off);
 }
 
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4i load16(const uint8_t *base, uint32_t off) {
+    asm("" : "+v"(off));
+    return *reinterpret_cast<const v4i *>(base + off);
+}
+
+// One thread per (padded position, 16-channel group): consecutive threads
+// write consecutive 16-byte pieces of a plane.
+__global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const uint32_t *__restrict__ in,
+                                                       uint8_t *__restrict__ planes) {
+    const uint32_t pair = blockIdx.y;
+    const uint32_t i = L.pair_mod[pair], w = L.pair_word[pair];
+    const LinMod M = L.mod[i];
+    const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
+    const uint32_t ngrp = L.cp / 16;
+    const uint32_t tid = blockIdx.x * 256 + threadIdx.x;
+    if (tid >= L.nimg * L.hp * L.wp * ngrp) return;
+    const uint32_t pp = tid / ngrp, c0 = 16 * (tid % ngrp);
+    const uint32_t xp = pp % L.wp, t = pp / L.wp;
+    const uint32_t yp = t % L.hp, img = t / L.hp;
+    const int32_t y = static_cast<int32_t>(yp) - static_cast<int32_t>(L.pad);
+    const int32_t x = static_cast<int32_t>(xp) - static_cast<int32_t>(L.pad);
+    const bool live = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
+                      x < static_cast<int32_t>(L.in_cols) && c0 < L.c_in;
+    const uint32_t flip = M.m > 128 ? 0x80808080u : 0u;
+    const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
+    const uint32_t step = L.sC * 4u;
+    // padding and channels past c_in read a valid word (position (0, 0), or
+    // the last channel) and are masked below
+    const uint32_t a0 =
+        live ? (img * L.sN + static_cast<uint32_t>(y) * L.sY + static_cast<uint32_t>(x) * L.sX + c0 * L.sC) * 4u : 0u;
+    const uint32_t last = live ? L.c_in - 1 - c0 : 0u;
+    uint32_t wd[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) wd[q] = load_word(src, a0 + (static_cast<uint32_t>(q) < last ? q : last) * step);
+    uint8_t *dst = planes + static_cast<uint64_t>(M.lam_off + w * M.g) * L.plane_bytes + static_cast<uint64_t>(pp) * L.cp + c0;
+    for (uint32_t jr = 0; jr < g; ++jr) {
+        const uint32_t sh = M.b * jr;
+        v4i v;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t f0 = __builtin_amdgcn_ubfe(wd[4 * d], sh, M.b);
+            const uint32_t f1 = __builtin_amdgcn_ubfe(wd[4 * d + 1], sh, M.b);
+            const uint32_t f2 = __builtin_amdgcn_ubfe(wd[4 * d + 2], sh, M.b);
+            const uint32_t f3 = __builtin_amdgcn_ubfe(wd[4 * d + 3], sh, M.b);
+            v[d] = static_cast<int32_t>(live ? (f0 | (f1 << 8) | (f2 << 16) | (f3 << 24)) ^ flip : flip);
+        }
+        *reinterpret_cast<v4i *>(dst + static_cast<uint64_t>(jr) * L.plane_bytes) = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The contraction.
+// ---------------------------------------------------------------------------
 template <int NCB, bool GARBLE>
-__global__ void __launch_bounds__(kLinBlock) k_linear(const LinPlan L, const uint32_t *__restrict__ in,
-                                                      const uint8_t *__restrict__ prep,
-                                                      const int64_t *__restrict__ bias,
-                                                      const uint32_t *__restrict__ offsets,
-                                                      uint32_t *__restrict__ out) {
+__global__ void __launch_bounds__(kLinBlock) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t *__restrict__ prep,
+              const int64_t *__restrict__ bias, const uint32_t *__restrict__ offsets, uint32_t *__restrict__ out) {
     extern __shared__ __align__(16) uint8_t lds[];
     uint8_t *Al = lds;
     uint8_t *Bl = lds + L.lds_a;
-    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a);  // after a word's last compute
+    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a + L.lds_b);
 
     const uint32_t tid = threadIdx.x, lane = tid % 64;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid / 64);
-    const uint32_t tile = blockIdx.x, i = blockIdx.y, og = blockIdx.z;
+    // consecutive tiles (neighbouring output rows, which share input rows) on
+    // one XCD, whose L2 then serves the shared plane rows
+    const uint32_t nb = gridDim.x, full = nb / kXcds * kXcds;
+    const uint32_t tile = blockIdx.x < full ? (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds : blockIdx.x;
+    const uint32_t i = blockIdx.y, og = blockIdx.z;
     const uint32_t xtile = tile % L.xtiles;
     const uint32_t row = (tile / L.xtiles) % L.rows;
     const uint32_t img = tile / (L.xtiles * L.rows);
@@ -309,28 +393,23 @@ __global__ void __launch_bounds__(kLinBlock) k_linear(const LinPlan L, const uin
     constexpr uint32_t XT = 16 * NCB;
     const uint32_t x0 = xtile * XT;
     const int32_t *rowsum = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
-    const uint32_t rowb = L.xw * L.ck;  // bytes per staged row of one residue
-    const uint32_t halo = L.kh * rowb;  // bytes per residue
-    const uint32_t mask = (1u << M.b) - 1u;
     const uint32_t ksteps = L.kc / 64;
     const uint32_t kg = 16 * (lane / 16);
+    const uint32_t rowb = L.xw * L.xstride;
 
     // output channel of element r of row block ob for this lane
     auto o_local = [&](int ob, int r) -> uint32_t { return ob * 16 + 4 * (lane / 16) + r; };
-    // byte offset of channel byte c (a multiple of 4) of staged column x
-    auto col_off = [&](uint32_t x, uint32_t c) -> uint32_t {
-        return x * L.ck + ((((c >> 4) ^ (x >> L.swz_shift)) & L.swz_mask) << 4) + (c & 15u);
-    };
 
-    // 128 * row sum per lane row (restores sum w v from sum w (v - 128)), and
-    // for the garbler -b_o mod m
-    int32_t rs[4][4];
-    uint32_t negb[4][4];
+    // The accumulators start at base[ob][r] = 128 rowsum (m > 128) + off
+    // (+ (-b mod m) R_j for the garbler) and end at u = sum w v + off (+ ...)
+    // in [0, 2^31) with u / m < 2^23.
+    const bool shifted = M.m > 128;
+    uint32_t base[4][4], negb[4][4];
 #pragma unroll
     for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            rs[ob][r] = M.m > 128 ? 128 * rowsum[o_local(ob, r)] : 0;
+            base[ob][r] = (shifted ? static_cast<uint32_t>(128 * rowsum[o_local(ob, r)]) : 0u) + M.off;
             negb[ob][r] = 0;
             if constexpr (GARBLE) {
                 const uint32_t o = og * kLinOTile + o_local(ob, r);
@@ -342,159 +421,176 @@ __global__ void __launch_bounds__(kLinBlock) k_linear(const LinPlan L, const uin
             }
         }
 
-    const int32_t ybase = static_cast<int32_t>(row * L.stride) - static_cast<int32_t>(L.pad);
-    const int32_t xbase = static_cast<int32_t>(x0 * L.stride) - static_cast<int32_t>(L.pad);
+    // This thread's (at most two) staged pieces: piece e = tid + 256 t of a
+    // residue's halo is (row dy, column xin, 16 channels c16); its plane
+    // offset (the column clamped into the padded row: the columns past the
+    // row feed outputs that are dropped) and its LDS offset.
     const uint32_t c16n = L.ck / 16;
-    const uint32_t items = L.kh * c16n * L.xw;
-    const bool full16 = L.c_in % 16 == 0;
-    // residues of moduli up to 128 are valid signed bytes as they are; above
-    // that they enter as v - 128 (v XOR 0x80), and 128 * rowsum restores sum w v
-    const bool shifted = M.m > 128;
-    const uint32_t flip = shifted ? 0x80808080u : 0u;
+    const uint32_t pieces = L.kh * L.xw * c16n;
+    uint32_t poff[2], loff[2];
+    bool pval[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const uint32_t e = tid + t * kLinBlock;
+        pval[t] = e < pieces;
+        const uint32_t ee = pval[t] ? e : 0u;
+        const uint32_t c16 = ee % c16n, xin = (ee / c16n) % L.xw, dy = ee / (c16n * L.xw);
+        uint32_t xp = x0 * L.stride + xin;
+        xp = xp < L.wp ? xp : L.wp - 1;
+        poff[t] = ((img * L.hp + row * L.stride + dy) * L.wp + xp) * L.cp + 16 * c16;
+        loff[t] = dy * rowb + xin * L.xstride + 16 * c16;
+    }
+    // fragment columns of this lane in the staged rows (tile column cb)
+    uint32_t colb[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) colb[cb] = (cb * 16 + lane % 16) * L.stride * L.xstride;
+
+    // Stages (w, j0, cc) in order: packed word, group of four residues,
+    // channel chunk.  The pieces of the next stage are loaded into registers
+    // while the current stage computes.
+    struct Stage {
+        uint32_t w, j0, cc;
+    };
+    auto g_of = [&](uint32_t w) { return (w + 1 == M.W) ? M.glast : M.g; };
+    auto advance = [&](Stage &st) {
+        if (++st.cc == L.ncc) {
+            st.cc = 0;
+            st.j0 += 4;
+            if (st.j0 >= g_of(st.w)) {
+                st.j0 = 0;
+                ++st.w;
+            }
+        }
+    };
+    auto load_stage = [&](v4i (&pf)[2][4], const Stage &st) {
+        const uint32_t g = g_of(st.w);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t j = st.j0 + q < g ? st.j0 + q : 0u;
+            const uint8_t *plane = planes + static_cast<uint64_t>(M.lam_off + st.w * M.g + j) * L.plane_bytes;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) pf[t][q] = load16(plane, pval[t] ? poff[t] + st.cc * L.ck : 0u);
+        }
+    };
+
+    uint32_t part[4][NCB][4];
+    v4i acc[4][NCB];
     bool a_staged = false;
+    Stage cur{0, 0, 0}, ahead{0, 0, 0};
+    v4i pfA[2][4];
+    load_stage(pfA, ahead);
+    advance(ahead);
 
-    for (uint32_t w = 0; w < M.W; ++w) {
-        const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
-        const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
-        uint32_t part[4][NCB][4];
-#pragma unroll
-        for (int ob = 0; ob < 4; ++ob)
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
-
-        for (uint32_t j0 = 0; j0 < g; j0 += 4) {
-            v4i acc[4][NCB];
+    // One stage with the pieces in pf; returns false after the last stage.
+    auto stage = [&](v4i (&pf)[2][4]) -> bool {
+        const uint32_t w = cur.w, j0 = cur.j0, cc = cur.cc;
+        const uint32_t g = g_of(w);
+        const uint32_t j = j0 + wave;  // this wave's residue
+        if (j0 == 0 && cc == 0) {
 #pragma unroll
             for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) acc[ob][cb] = v4i{0, 0, 0, 0};
-            for (uint32_t cc = 0; cc < L.ncc; ++cc) {
-                __syncthreads();  // the previous fragments (and output words) have been read
-                if (L.ncc > 1 || !a_staged) {
-                    // weights of this chunk: 64 rows of kc bytes, 16 bytes per load
-                    const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad +
-                                                og * kLinOTile) * L.kc;
-                    const uint32_t per_row = L.kc / 16;
-                    for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
-                        const uint32_t rr = e / per_row, q = e % per_row;
-                        *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
-                            *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
-                    }
-                    a_staged = true;
+                for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
+        }
+        if (cc == 0) {
+            uint32_t Rj = 0;
+            if constexpr (GARBLE) Rj = (offsets[M.woff + w] >> (M.b * j)) & ((1u << M.b) - 1u);
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int32_t b0 = static_cast<int32_t>(base[ob][r] + negb[ob][r] * Rj);
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) acc[ob][cb][r] = b0;
                 }
-                // input halos of residues j0 .. j0+3; an item is (row r, 16 channels,
-                // column xin): 16 loads in flight, then one 16-byte store per residue
-                for (uint32_t e = tid; e < items; e += kLinBlock) {
-                    const uint32_t q1 = __umulhi(e, L.xw_magic);  // e / xw
-                    const uint32_t xin = e - q1 * L.xw;
-                    const uint32_t c16 = q1 & (c16n - 1u);
-                    const uint32_t r = q1 >> L.lg_c16n;
-                    const int32_t y = ybase + static_cast<int32_t>(r), x = xbase + static_cast<int32_t>(xin);
-                    const uint32_t c0 = cc * L.ck + 16 * c16;
-                    const bool valid = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
-                                       x < static_cast<int32_t>(L.in_cols) && c0 < L.c_in;
-                    uint32_t wd[16];
-                    if (valid) {
-                        const uint32_t *sp = src + (img * L.sN + static_cast<uint32_t>(y) * L.sY +
-                                                    static_cast<uint32_t>(x) * L.sX + c0 * L.sC);
-                        if (full16) {
-#pragma unroll
-                            for (int q = 0; q < 16; ++q) wd[q] = sp[q * L.sC];
-                        } else {
-                            // channels past c_in meet zero weights: read any valid one
-                            const uint32_t last = L.c_in - 1 - c0;
-#pragma unroll
-                            for (int q = 0; q < 16; ++q) wd[q] = sp[(static_cast<uint32_t>(q) < last ? static_cast<uint32_t>(q) : last) * L.sC];
-                        }
-                    } else {
-#pragma unroll
-                        for (int q = 0; q < 16; ++q) wd[q] = 0;
-                    }
-                    const uint32_t dsto = r * rowb + xin * L.ck + (((c16 ^ (xin >> L.swz_shift)) & L.swz_mask) << 4);
-#pragma unroll
-                    for (int jq = 0; jq < 4; ++jq) {
-                        if (j0 + jq < g) {
-                            const uint32_t sh = M.b * (j0 + jq);
-                            uint4 v;
-                            uint32_t *vv = reinterpret_cast<uint32_t *>(&v);
-#pragma unroll
-                            for (int d = 0; d < 4; ++d) {
-                                const uint32_t f0 = __builtin_amdgcn_ubfe(wd[4 * d], sh, M.b);
-                                const uint32_t f1 = __builtin_amdgcn_ubfe(wd[4 * d + 1], sh, M.b);
-                                const uint32_t f2 = __builtin_amdgcn_ubfe(wd[4 * d + 2], sh, M.b);
-                                const uint32_t f3 = __builtin_amdgcn_ubfe(wd[4 * d + 3], sh, M.b);
-                                vv[d] = (f0 | (f1 << 8) | (f2 << 16) | (f3 << 24)) ^ flip;
-                            }
-                            *reinterpret_cast<uint4 *>(Bl + jq * halo + dsto) = v;
-                        }
-                    }
-                }
-                __syncthreads();
-                if (j0 + wave < g) {
-                    const uint8_t *Bw = Bl + wave * halo;
-                    for (uint32_t kk = 0; kk < ksteps; ++kk) {
-                        v4i a[4];
-#pragma unroll
-                        for (int ob = 0; ob < 4; ++ob)
-                            a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 +
-                                                                   kg);
-                        const uint32_t kidx = kk * 64 + kg;
-                        uint32_t tap = kidx >> L.lg_ck;
-                        const uint32_t coff = kidx & (L.ck - 1u);
-                        if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
-                        const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
-#pragma unroll
-                        for (int cb = 0; cb < NCB; ++cb) {
-                            const uint32_t xcol = (cb * 16 + lane % 16) * L.stride + dx;
-                            const v4i bf = *reinterpret_cast<const v4i *>(Bw + dy * rowb + col_off(xcol, coff));
-#pragma unroll
-                            for (int ob = 0; ob < 4; ++ob)
-                                acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
-                        }
-                    }
-                }
+        }
+        __syncthreads();  // the previous stage's fragments have been read
+        if (L.ncc > 1 || !a_staged) {
+            // weights of chunk cc: 64 rows of kc bytes, 16 bytes per load
+            const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad + og * kLinOTile) * L.kc;
+            const uint32_t per_row = L.kc / 16;
+            for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
+                const uint32_t rr = e / per_row, q = e % per_row;
+                *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
+                    *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
             }
-            // epilogue of residue j0 + wave: u = sum w v + m ceil(2^29/m) (+ (-b mod m) R_j)
-            // lies in [0, 2^31); its residue mod m goes into the field
-            if (j0 + wave < g) {
-                const uint32_t j = j0 + wave, sh = M.b * j;
-                uint32_t Rj = 0;
-                if constexpr (GARBLE) Rj = (offsets[M.woff + w] >> sh) & mask;
+            a_staged = true;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (j0 + q < g) {
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    if (pval[t]) *reinterpret_cast<v4i *>(Bl + q * L.halo + loff[t]) = pf[t][q];
+            }
+        // pf is free: the next stage
+        if (ahead.w < M.W) load_stage(pf, ahead);
+        advance(ahead);
+        __syncthreads();
+        if (j < g) {
+            const uint8_t *Bw = Bl + wave * L.halo;
+            for (uint32_t kk = 0; kk < ksteps; ++kk) {
+                v4i a[4];
 #pragma unroll
                 for (int ob = 0; ob < 4; ++ob)
+                    a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 + kg);
+                const uint32_t kidx = kk * 64 + kg;
+                uint32_t tap = kidx >> L.lg_ck;
+                if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
+                const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+                const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        uint32_t extra = static_cast<uint32_t>(rs[ob][r]) + M.off;
-                        if constexpr (GARBLE) extra += negb[ob][r] * Rj;
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const v4i bf = *reinterpret_cast<const v4i *>(Bw + boff + colb[cb]);
 #pragma unroll
-                        for (int cb = 0; cb < NCB; ++cb) {
-                            const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]) + extra;
-                            part[ob][cb][r] |= (u - lin_div(u, M) * M.m) << sh;
-                        }
-                    }
+                    for (int ob = 0; ob < 4; ++ob)
+                        acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                }
             }
         }
-        // merge the waves' fields (disjoint bits) and store whole words
-        __syncthreads();
-        for (uint32_t e = tid; e < kLinOTile * L.ostride; e += kLinBlock) Ol[e] = 0;
-        __syncthreads();
+        if (cc + 1 == L.ncc && j < g) {
+            // epilogue of residue j: the residue of u mod m goes into the field
+            const uint32_t sh = M.b * j;
 #pragma unroll
-        for (int ob = 0; ob < 4; ++ob)
+            for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb)
+                for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (part[ob][cb][r])
-                        atomicOr(&Ol[o_local(ob, r) * L.ostride + cb * 16 + lane % 16], part[ob][cb][r]);
-        __syncthreads();
-        uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out;
-        for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) {
-            const uint32_t ol = e / XT, xl = e % XT;
-            const uint32_t o = og * kLinOTile + ol, x = x0 + xl;
-            if (o < L.c_out && x < L.cols) dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
+                    for (int r = 0; r < 4; ++r) {
+                        const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]);
+                        const uint32_t q = __umulhi(u, M.divM) >> M.divS;  // < 2^23
+                        const uint32_t res =
+                            static_cast<uint32_t>(__mul24(static_cast<int32_t>(q), -static_cast<int32_t>(M.m))) + u;
+                        part[ob][cb][r] |= res << sh;
+                    }
         }
+        advance(cur);
+        if (cur.w != w) {
+            // word w complete: merge the waves' fields (disjoint bits), store whole words
+            for (uint32_t e = tid; e < kLinOTile * L.ostride; e += kLinBlock) Ol[e] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (part[ob][cb][r])
+                            atomicOr(&Ol[o_local(ob, r) * L.ostride + cb * 16 + lane % 16], part[ob][cb][r]);
+            __syncthreads();
+            uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out;
+            for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) {
+                const uint32_t ol = e / XT, xl = e % XT;
+                const uint32_t o = og * kLinOTile + ol, x = x0 + xl;
+                if (o < L.c_out && x < L.cols)
+                    dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
+            }
+        }
+        return cur.w < M.W;
+    };
+    while (stage(pfA)) {
     }
 }
 
@@ -511,29 +607,31 @@ int lin_allow_lds(const void *kernel, uint32_t bytes) {
 }
 
 template <int NCB, bool GARBLE>
-int launch_linear_ncb(const LinPlan &L, const uint32_t *in, const uint8_t *prep, const int64_t *bias,
-                      const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
-    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear<NCB, GARBLE>), L.lds_bytes);
+int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
+                const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
+    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm<NCB, GARBLE>), L.lds_bytes);
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear<NCB, GARBLE>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
-                       dim3(kLinBlock), L.lds_bytes, stream, L, in, prep, bias, offsets, out);
+    hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
+                       dim3(kLinBlock), L.lds_bytes, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
 }
 
 template <bool GARBLE>
 int launch_linear(const LinPlan &L, const uint32_t *in, const uint8_t *prep, const int64_t *bias,
-                  const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
+                  const uint32_t *offsets, uint8_t *work, uint32_t *out, hipStream_t stream) {
     int dev = 0, v = 0;
     if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return REDASH_E_HIP;
     if (L.lds_bytes > static_cast<uint32_t>(v)) return REDASH_E_HIP;
-    switch (L.xt) {
-        case 64: return launch_linear_ncb<4, GARBLE>(L, in, prep, bias, offsets, out, stream);
-        case 32: return launch_linear_ncb<2, GARBLE>(L, in, prep, bias, offsets, out, stream);
-        default: return launch_linear_ncb<1, GARBLE>(L, in, prep, bias, offsets, out, stream);
-    }
+    const uint64_t nthr = static_cast<uint64_t>(L.nimg) * L.hp * L.wp * (L.cp / 16);
+    if (nthr >= (1ull << 32)) return REDASH_E_PARAM;
+    hipLaunchKernelGGL(k_linear_unpack, dim3(static_cast<uint32_t>((nthr + 255) / 256), L.npairs), dim3(256), 0, stream,
+                       L, in, work);
+    if (lin_launched()) return REDASH_E_HIP;
+    if (L.xt == 32) return launch_gemm<2, GARBLE>(L, work, prep, bias, offsets, out, stream);
+    return launch_gemm<1, GARBLE>(L, work, prep, bias, offsets, out, stream);
 }
 
 }  // namespace
@@ -553,6 +651,7 @@ int redash_linear_plan(const redash_linear_params *p, redash_linear_sizes *out) 
     out->in_label_words = L.n_in * tw;
     out->out_label_words = L.n_out * tw;
     out->prepared_bytes = prepared_bytes(L);
+    out->work_bytes = work_bytes(L);
     out->h_out = (p->h_in + 2 * p->pad - p->kh) / p->stride + 1;
     out->w_out = (p->w_in + 2 * p->pad - p->kw) / p->stride + 1;
     out->offset_words = tw;
@@ -575,22 +674,22 @@ int redash_linear_prepare(const redash_linear_params *p, const int32_t *d_weight
 }
 
 int redash_linear_eval(const redash_linear_params *p, const uint32_t *d_in_labels, const uint8_t *d_prepared,
-                       uint32_t *d_out_labels, hipStream_t stream) {
+                       uint8_t *d_work, uint32_t *d_out_labels, hipStream_t stream) {
     LinPlan L;
     const int rc = build_lin_plan(p, &L);
     if (rc) return rc;
-    if (!d_in_labels || !d_prepared || !d_out_labels) return REDASH_E_NULL;
-    return launch_linear<false>(L, d_in_labels, d_prepared, nullptr, nullptr, d_out_labels, stream);
+    if (!d_in_labels || !d_prepared || !d_work || !d_out_labels) return REDASH_E_NULL;
+    return launch_linear<false>(L, d_in_labels, d_prepared, nullptr, nullptr, d_work, d_out_labels, stream);
 }
 
 int redash_linear_garble(const redash_linear_params *p, const uint32_t *d_in_zero, const uint8_t *d_prepared,
-                         const int64_t *d_bias, const uint32_t *d_offsets, uint32_t *d_out_zero,
+                         const int64_t *d_bias, const uint32_t *d_offsets, uint8_t *d_work, uint32_t *d_out_zero,
                          hipStream_t stream) {
     LinPlan L;
     const int rc = build_lin_plan(p, &L);
     if (rc) return rc;
-    if (!d_in_zero || !d_prepared || !d_offsets || !d_out_zero) return REDASH_E_NULL;
-    return launch_linear<true>(L, d_in_zero, d_prepared, d_bias, d_offsets, d_out_zero, stream);
+    if (!d_in_zero || !d_prepared || !d_offsets || !d_work || !d_out_zero) return REDASH_E_NULL;
+    return launch_linear<true>(L, d_in_zero, d_prepared, d_bias, d_offsets, d_work, d_out_zero, stream);
 }
 
 }  // extern "C"

@@ -168,9 +168,9 @@ def test_entry_points_validate_before_any_device_work():
 def test_linear_structs_match_header():
     # k, moduli[16], batch, c_in, h_in, w_in, c_out, kh, kw, stride, pad: 26 uint32
     assert ctypes.sizeof(B.LinearParams) == 4 * 26
-    # in/out label words, prepared bytes (8-byte), h_out, w_out, offset_words (4-byte), padded to 8
-    assert ctypes.sizeof(B.LinearSizes) == 40
-    assert B.LinearSizes.h_out.offset == 24
+    # in/out label words, prepared and work bytes (8-byte), h_out, w_out, offset_words (4-byte), padded to 8
+    assert ctypes.sizeof(B.LinearSizes) == 48
+    assert B.LinearSizes.h_out.offset == 32
 
 
 LINEAR_CASES = [
@@ -197,6 +197,9 @@ def test_linear_plan_sizes(case):
     assert sz["out_label_words"] == n * c_out * ho * wo * W
     assert sz["offset_words"] == W
     assert sz["prepared_bytes"] >= len(moduli) * c_out * c_in * kh * kw
+    # one byte per residue per (zero-padded) input position and channel
+    lam_total = sum(OL.label_lambda(m) for m in moduli)
+    assert sz["work_bytes"] >= lam_total * n * c_in * h * w
 
 
 LINEAR_BAD = [
@@ -227,9 +230,11 @@ def test_linear_entry_points_validate_before_any_device_work():
     good = B.make_linear_params((2, 3, 5), 1, 4, 4, 4, 2, 3, 3, 1, 1)
     assert L.redash_linear_plan(None, ctypes.byref(B.LinearSizes())) == B.REDASH_E_NULL
     assert L.redash_linear_prepare(ctypes.byref(bad), fake, fake, None) == B.REDASH_E_PARAM
-    assert L.redash_linear_eval(ctypes.byref(bad), fake, fake, fake, None) == B.REDASH_E_PARAM
-    assert L.redash_linear_garble(ctypes.byref(bad), fake, fake, None, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_linear_eval(ctypes.byref(bad), fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_linear_garble(ctypes.byref(bad), fake, fake, None, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_linear_prepare(ctypes.byref(good), None, fake, None) == B.REDASH_E_NULL
-    assert L.redash_linear_eval(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
-    assert L.redash_linear_eval(ctypes.byref(good), fake, fake, None, None) == B.REDASH_E_NULL
-    assert L.redash_linear_garble(ctypes.byref(good), fake, fake, None, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_eval(ctypes.byref(good), fake, None, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_eval(ctypes.byref(good), fake, fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_eval(ctypes.byref(good), fake, fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_linear_garble(ctypes.byref(good), fake, fake, None, None, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_linear_garble(ctypes.byref(good), fake, fake, None, fake, None, fake, None) == B.REDASH_E_NULL

@@ -70,11 +70,12 @@ def test_linear_matches_oracle(case):
     wts[:, :, 0, 0] = rng.integers(-3, 4, size=(c_out, c_in))  # small weights too
     bias = rng.integers(-2 ** 62, 2 ** 62, size=c_out, dtype=np.int64)
     prep = _dev_u8(sz["prepared_bytes"])
+    work = _dev_u8(sz["work_bytes"])
     B.redash_linear_prepare(lp, H.to_dev(wts.astype(np.int32)), prep)
     out = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
-    B.redash_linear_eval(lp, H.to_dev(X), prep, out)
+    B.redash_linear_eval(lp, H.to_dev(X), prep, work, out)
     zout = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
-    B.redash_linear_garble(lp, H.to_dev(Z), prep, H.to_dev(bias), H.to_dev(R), zout)
+    B.redash_linear_garble(lp, H.to_dev(Z), prep, H.to_dev(bias), H.to_dev(R), work, zout)
     torch.cuda.synchronize()
     w32 = wts.astype(np.int32).astype(np.int64)  # the int32 weights the library was given
     assert np.array_equal(H.to_u32(out), OL.conv_labels(moduli, X, shape, w32, stride, pad))
@@ -91,15 +92,16 @@ def test_linear_garble_without_bias_and_repeatability():
     R = _random_labels(moduli, 1, rng)
     wts = rng.integers(-50, 50, size=(c_out, shape[1], 3, 3))
     prep = _dev_u8(sz["prepared_bytes"])
+    work = _dev_u8(sz["work_bytes"])
     B.redash_linear_prepare(lp, H.to_dev(wts.astype(np.int32)), prep)
     zout = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
     zd = H.to_dev(Z)
-    B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), zout)
+    B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), work, zout)
     torch.cuda.synchronize()
     first = H.to_u32(zout).copy()
     assert np.array_equal(first, OL.garble_conv(moduli, Z, shape, wts, None, R, 1, 1))
     for _ in range(3):
-        B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), zout)
+        B.redash_linear_garble(lp, zd, prep, None, H.to_dev(R), work, zout)
     torch.cuda.synchronize()
     assert np.array_equal(H.to_u32(zout), first)
     assert np.array_equal(H.to_u32(zd), Z)
@@ -135,11 +137,13 @@ def _check_full_layer(w: WL.Workload, n_sample: int):
     torch.cuda.empty_cache()
     wts = torch.from_numpy(wt.reshape(kshape).astype(np.int32)).cuda()
     prep = _dev_u8(sz["prepared_bytes"])
+    work = _dev_u8(sz["work_bytes"])
     B.redash_linear_prepare(lp, wts, prep)
     Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
     Zo = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
-    B.redash_linear_eval(lp, X, prep, Y)
-    B.redash_linear_garble(lp, zin, prep, None, offsets, Zo)
+    B.redash_linear_eval(lp, X, prep, work, Y)
+    B.redash_linear_garble(lp, zin, prep, None, offsets, work, Zo)
+    del work
     # decode every output with the gadget library's decode (any scale set of the base)
     gp_out = B.make_params(moduli, w.scale_idx, n_out, w.seed)
     y = torch.empty(n_out, dtype=torch.int64, device="cuda")
