@@ -8,8 +8,10 @@ a 1 GiB copy reads FETCH_SIZE = 524,300 KiB and WRITE_SIZE = 1,048,576 KiB,
 so FETCH_SIZE is scaled by 2 and WRITE_SIZE by 1).
 
 A figure is only valid for the kernel it was taken on: ``traffic_bytes``
-returns None as soon as any source file of the library differs from the one
-the counters were read on (a SHA-256 over the sources, in a fixed order).
+returns None as soon as any source file that defines the evaluation kernel
+differs from the one the counters were read on (a SHA-256 over those
+sources, in a fixed order; the linear-layer source and the C header, which
+the kernel does not depend on beyond the plan, are not part of it).
 """
 
 from __future__ import annotations
@@ -29,15 +31,20 @@ MEASURED = {
         "kernel": "k_eval",
         "fetch_kib": 15211545.7,  # mean of two dispatches: 15,210,247 and 15,212,844
         "write_kib": 5049479.0,  # mean of 5,049,628 and 5,049,330
-        "sources_sha256": "eb8e0b936b0cb705748016c5e4da501de551fc4e19b98a8568b5201710d774a1",
+        "sources_sha256": "578f12b650b763e3e13fadb6262e026d445e8511bc4b65040044fcdaeb963149",
     },
 }
 
 
+# the files that define k_eval: its source, the device helpers, the plan and the AES tables
+EVAL_SOURCES = ("redash.hip", "device.hpp", "plan.cpp", "plan.hpp", "aes_tables.hpp")
+
+
 def sources_sha256() -> str:
-    """SHA-256 over the library's source files (name and contents)."""
+    """SHA-256 over the evaluation kernel's source files (name and contents)."""
     h = hashlib.sha256()
-    for path in sorted(_build.SOURCES + _build.HEADERS, key=os.path.basename):
+    paths = [p for p in _build.SOURCES + _build.HEADERS if os.path.basename(p) in EVAL_SOURCES]
+    for path in sorted(paths, key=os.path.basename):
         h.update(os.path.basename(path).encode())
         with open(path, "rb") as f:
             h.update(f.read())
