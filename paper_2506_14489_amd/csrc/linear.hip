@@ -30,6 +30,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "../../include/redash.h"
 #include "plan.hpp"
 
@@ -370,7 +372,9 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
 // ---------------------------------------------------------------------------
 // The contraction.
 // ---------------------------------------------------------------------------
-template <int NCB, bool GARBLE>
+// K33: a 3x3 kernel with 64-channel chunks (taps = K steps, kc = 576), the K
+// loop unrolled with every fragment offset known but the row stride.
+template <int NCB, bool GARBLE, bool K33>
 __global__ void __launch_bounds__(kLinBlock) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t *__restrict__ prep,
               const int64_t *__restrict__ bias, const uint32_t *__restrict__ offsets, uint32_t *__restrict__ out) {
@@ -531,40 +535,71 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
         __syncthreads();
         if (j < g) {
             const uint8_t *Bw = Bl + wave * L.halo;
-            for (uint32_t kk = 0; kk < ksteps; ++kk) {
-                v4i a[4];
+            if constexpr (K33) {
+                // K step t is tap t = 3 dy + dx, the lane's 16 channels at kg
+                const uint8_t *Ar = Al + (lane % 16) * (576 + 16) + kg;
 #pragma unroll
-                for (int ob = 0; ob < 4; ++ob)
-                    a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 + kg);
-                const uint32_t kidx = kk * 64 + kg;
-                uint32_t tap = kidx >> L.lg_ck;
-                if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
-                const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
-                const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
+                for (int dy = 0; dy < 3; ++dy) {
+                    const uint8_t *Br = Bw + dy * rowb + kg;
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const v4i bf = *reinterpret_cast<const v4i *>(Bw + boff + colb[cb]);
+                    for (int dx = 0; dx < 3; ++dx) {
+                        const int kk = 3 * dy + dx;
+                        v4i a[4];
+#pragma unroll
+                        for (int ob = 0; ob < 4; ++ob)
+                            a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 16) + kk * 64);
+#pragma unroll
+                        for (int cb = 0; cb < NCB; ++cb) {
+                            const v4i bf = *reinterpret_cast<const v4i *>(Br + colb[cb] + dx * (64 + 16));
+#pragma unroll
+                            for (int ob = 0; ob < 4; ++ob)
+                                acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                        }
+                    }
+                }
+            } else {
+                for (uint32_t kk = 0; kk < ksteps; ++kk) {
+                    v4i a[4];
 #pragma unroll
                     for (int ob = 0; ob < 4; ++ob)
-                        acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                        a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 + kg);
+                    const uint32_t kidx = kk * 64 + kg;
+                    uint32_t tap = kidx >> L.lg_ck;
+                    if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
+                    const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+                    const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) {
+                        const v4i bf = *reinterpret_cast<const v4i *>(Bw + boff + colb[cb]);
+#pragma unroll
+                        for (int ob = 0; ob < 4; ++ob)
+                            acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                    }
                 }
             }
         }
         if (cc + 1 == L.ncc && j < g) {
             // epilogue of residue j: the residue of u mod m goes into the field
             const uint32_t sh = M.b * j;
+            auto epilogue = [&](auto shifts) {
 #pragma unroll
-            for (int ob = 0; ob < 4; ++ob)
+                for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb)
+                    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]);
-                        const uint32_t q = __umulhi(u, M.divM) >> M.divS;  // < 2^23
-                        const uint32_t res =
-                            static_cast<uint32_t>(__mul24(static_cast<int32_t>(q), -static_cast<int32_t>(M.m))) + u;
-                        part[ob][cb][r] |= res << sh;
-                    }
+                        for (int r = 0; r < 4; ++r) {
+                            const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]);
+                            uint32_t q = __umulhi(u, M.divM);  // < 2^23
+                            if constexpr (decltype(shifts)::value) q >>= M.divS;
+                            const uint32_t res =
+                                static_cast<uint32_t>(__mul24(static_cast<int32_t>(q), -static_cast<int32_t>(M.m))) + u;
+                            part[ob][cb][r] |= res << sh;
+                        }
+            };
+            if (M.divS == 0)
+                epilogue(std::integral_constant<bool, false>{});
+            else
+                epilogue(std::integral_constant<bool, true>{});
         }
         advance(cur);
         if (cur.w != w) {
@@ -606,16 +641,24 @@ int lin_allow_lds(const void *kernel, uint32_t bytes) {
                : REDASH_E_HIP;
 }
 
-template <int NCB, bool GARBLE>
+template <int NCB, bool GARBLE, bool K33>
 int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
                 const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
-    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm<NCB, GARBLE>), L.lds_bytes);
+    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm<NCB, GARBLE, K33>), L.lds_bytes);
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
+    hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE, K33>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
                        dim3(kLinBlock), L.lds_bytes, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
+}
+
+template <int NCB, bool GARBLE>
+int launch_gemm_k(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
+                  const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
+    if (L.kh == 3 && L.kw == 3 && L.ck == 64)
+        return launch_gemm<NCB, GARBLE, true>(L, planes, prep, bias, offsets, out, stream);
+    return launch_gemm<NCB, GARBLE, false>(L, planes, prep, bias, offsets, out, stream);
 }
 
 template <bool GARBLE>
@@ -630,8 +673,8 @@ int launch_linear(const LinPlan &L, const uint32_t *in, const uint8_t *prep, con
     hipLaunchKernelGGL(k_linear_unpack, dim3(static_cast<uint32_t>((nthr + 255) / 256), L.npairs), dim3(256), 0, stream,
                        L, in, work);
     if (lin_launched()) return REDASH_E_HIP;
-    if (L.xt == 32) return launch_gemm<2, GARBLE>(L, work, prep, bias, offsets, out, stream);
-    return launch_gemm<1, GARBLE>(L, work, prep, bias, offsets, out, stream);
+    if (L.xt == 32) return launch_gemm_k<2, GARBLE>(L, work, prep, bias, offsets, out, stream);
+    return launch_gemm_k<1, GARBLE>(L, work, prep, bias, offsets, out, stream);
 }
 
 }  // namespace
