@@ -652,6 +652,39 @@ int orc_garble(const orc_params *p, uint64_t a_begin, uint64_t count, uint32_t *
     return ORC_OK;
 }
 
+/* Garble gadgets a_begin .. a_begin+count-1 on input zero-labels the caller
+ * gives (the output zero-labels of the layer that feeds the gadget: in a
+ * circuit every wire's zero-label comes from the gate that produces it,
+ * Sec. 2.3), instead of drawing them from the PRG.  Everything else is as in
+ * orc_garble: offsets from the seed, tweaks from the global gadget index. */
+int orc_garble_given(const orc_params *p, uint64_t a_begin, uint64_t count, uint32_t *offsets,
+                     const uint32_t *in_zero, uint32_t *out_zero, uint32_t *tables) {
+    orc_plan pl;
+    int rc = make_plan(p, &pl);
+    if (rc) return rc;
+    if (!offsets || !in_zero || !out_zero) return ORC_ENULL;
+    uint8_t rk_seed[176];
+    seed_round_keys(p->seed, rk_seed);
+    uint32_t gadget_id = (uint32_t)p->seed;
+    static uint32_t R[ORC_MAXK][ORC_MAXLAMBDA];
+    memset(R, 0, sizeof R);
+    make_offsets(&pl, rk_seed, R);
+    for (uint32_t i = 0; i < pl.k; ++i) {
+        uint32_t words[ORC_MAXLAMBDA];
+        pk32_pack(pl.m[i], R[i], words);
+        memcpy(offsets + offset_block(&pl, i), words, pl.W[i] * sizeof(uint32_t));
+    }
+    for (uint64_t al = 0; al < count; ++al) {
+        uint64_t a = a_begin + al;
+        uint32_t zin[ORC_MAXK][ORC_MAXLAMBDA], zout[ORC_MAXK][ORC_MAXLAMBDA];
+        memset(zin, 0, sizeof zin);
+        for (uint32_t i = 0; i < pl.k; ++i) read_label(&pl, in_zero, i, count, al, zin[i]);
+        garble_one(&pl, gadget_id, a, R, zin, zout, tables, count, al, NULL);
+        for (uint32_t i = 0; i < pl.k; ++i) write_label(&pl, out_zero, i, count, al, zout[i]);
+    }
+    return ORC_OK;
+}
+
 /* X_{a,i} = Z_{a,i} + ((x_a mod P) mod m_i) R_i. */
 int orc_encode(const orc_params *p, uint64_t count, const int64_t *x, const uint32_t *zero,
                const uint32_t *offsets, uint32_t *labels) {

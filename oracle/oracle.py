@@ -73,6 +73,8 @@ def lib():
         _lib.orc_frac_digits.argtypes = [u32p, ctypes.c_int, u32p, ctypes.c_int, u32p]
         _lib.orc_garble.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint64,
                                     u32p, u32p, u32p, u32p]
+        _lib.orc_garble_given.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint64,
+                                          u32p, u32p, u32p, u32p]
         _lib.orc_encode.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64,
                                     ctypes.POINTER(ctypes.c_int64), u32p, u32p, u32p]
         _lib.orc_eval.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint64,
@@ -196,6 +198,20 @@ def garble(params: Params, a_begin: int, count: int, with_tables: bool = True):
     _check(lib().orc_garble(ctypes.byref(params), a_begin, count, _p(offsets), _p(zin), _p(zout),
                             _p(tables)))
     return offsets, zin, zout, tables
+
+
+def garble_given(params: Params, a_begin: int, count: int, in_zero: np.ndarray, with_tables: bool = True):
+    """Garble on the given input zero-labels (stride = count).  Returns
+    (offsets, out_zero, tables or None)."""
+    sz = sizes(params, count)
+    offsets = np.zeros(sz["offset_words"], np.uint32)
+    zin = np.ascontiguousarray(in_zero, dtype=np.uint32)
+    assert len(zin) == sz["label_words"]
+    zout = np.zeros(sz["label_words"], np.uint32)
+    tables = np.zeros(max(sz["table_words"], 1), np.uint32) if with_tables else None
+    _check(lib().orc_garble_given(ctypes.byref(params), a_begin, count, _p(offsets), _p(zin), _p(zout),
+                                  _p(tables)))
+    return offsets, zout, tables
 
 
 def encode(params: Params, x: np.ndarray, zero: np.ndarray, offsets: np.ndarray) -> np.ndarray:

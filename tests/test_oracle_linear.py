@@ -170,3 +170,45 @@ def test_sampled_equals_full():
         res_samp = L.unpack(moduli, samp, len(items))
         for rf, rs in zip(res_full, res_samp):
             assert np.array_equal(rf[items], rs)
+
+
+def test_garble_given_equals_garble_on_its_own_zero_labels():
+    """Garbling on given input zero-labels reproduces the PRG garbling when
+    given the PRG's zero-labels (same offsets, output zero-labels, rows)."""
+    moduli, S, n, seed = (2, 3, 5, 7, 11), [4], 37, 3
+    op = O.make_params(list(moduli), S, n, seed)
+    offs, zin, zout, tab = O.garble(op, 5, n)
+    offs2, zout2, tab2 = O.garble_given(op, 5, n, zin)
+    assert np.array_equal(offs, offs2) and np.array_equal(zout, zout2) and np.array_equal(tab, tab2)
+
+
+@pytest.mark.parametrize("moduli,S", [((2, 3, 5, 7, 11, 13), [5]), ((3, 5, 7, 11, 32), [4]),
+                                      ((2, 3, 5, 7, 11, 13, 17), [5, 6])])
+def test_conv_layer_feeds_the_gadget(moduli, S):
+    """A conv layer on labels, then the scaling gadget garbled on the layer's
+    output zero-labels: decoding the gadget's output labels gives
+    floor((W x + b + r) / s), r = floor(P/2) mod s (Sec. 2.3 free operations,
+    then Sec. 3.4), computed here from the plain integer convolution."""
+    shape, c_out, kh, kw, stride, pad = (1, 3, 4, 5), 2, 3, 3, 1, 1
+    rng = np.random.default_rng(len(moduli))
+    x = rng.integers(-6, 7, size=shape)
+    wts = rng.integers(-9, 10, size=(c_out, shape[1], kh, kw))
+    b = rng.integers(-40, 41, size=c_out)
+    n_in = int(np.prod(shape))
+    op_in = O.make_params(list(moduli), S, n_in, 21)
+    offs, zin, _zout, _ = O.garble(op_in, 0, n_in, with_tables=False)
+    X = O.encode(op_in, x.reshape(-1), zin, offs)
+    Y = L.conv_labels(moduli, X, shape, wts, stride, pad)
+    Z = L.garble_conv(moduli, zin, shape, wts, b, offs, stride, pad)
+    n_out = int(np.prod(L.conv_out_shape(*shape, c_out, kh, kw, stride, pad)))
+    op = O.make_params(list(moduli), S, n_out, 21)  # the same seed: the same offsets R
+    a0 = 1000                                         # gadgets with their own tweaks
+    offs2, gz_out, tab = O.garble_given(op, a0, n_out, Z)
+    assert np.array_equal(offs2, offs)
+    out = O.evaluate(op, a0, n_out, Y, tab)
+    y, bad = O.decode(op, out, gz_out, offs)
+    lin = np.array([int(v) for v in _direct_conv(x, wts, b, stride, pad).reshape(-1)], dtype=np.int64)
+    s_ = rns.cardinality([moduli[i] for i in S])
+    r = rns.rounding_offset(list(moduli), list(S))
+    assert bad.sum() == 0
+    assert np.array_equal(y, np.floor_divide(lin + r, s_))
