@@ -142,6 +142,24 @@ int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d
                         uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work, hipStream_t stream);
 
 /*
+ * Garbler on given input zero-labels: as redash_garble_scale, except that the
+ * input zero-labels Z are read from d_in_zero (label_words, read only) instead
+ * of being drawn from the PRG.  This chains a gadget after free operations
+ * (Sec. 2.3: sums and public multiples of labels, e.g. the output
+ * zero-labels of redash_linear_garble) whose labels were built on the same
+ * offsets: d_offsets is written from the seed exactly as redash_garble_scale
+ * writes it, so the seed must be the one whose offsets the zero-labels use.
+ * The tweaks are (seed, global gadget index a0 + a) as in
+ * redash_garble_scale: gadgets garbled under one seed must use disjoint
+ * ranges a0..a0+n-1, including the gadgets whose PRG zero-labels fed the
+ * free operations.  d_in_zero may not alias d_out_zero, d_tables or d_work.
+ * Return codes as for redash_garble_scale.
+ */
+int redash_garble_scale_given(const redash_params *p, uint32_t *d_offsets, const uint32_t *d_in_zero,
+                              uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work,
+                              hipStream_t stream);
+
+/*
  * Stand-in for the oblivious transfer of input labels (Sec. 2.1):
  * X_{a,i} = Z_{a,i} + ((x_a mod P) mod m_i) * R_{m_i}, residue-wise mod m_i.
  *   d_x         n signed activations (int64), any value (reduced mod P; the

@@ -132,6 +132,7 @@ def lib() -> ctypes.CDLL:
         pp = ctypes.POINTER(Params)
         L.redash_plan.argtypes = [pp, ctypes.POINTER(Sizes)]
         L.redash_garble_scale.argtypes = [pp, vp, vp, vp, vp, vp, vp]
+        L.redash_garble_scale_given.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_encode.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_eval_scale.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_decode.argtypes = [pp, vp, vp, vp, vp, vp, vp]
@@ -144,7 +145,7 @@ def lib() -> ctypes.CDLL:
         L.redash_linear_prepare.argtypes = [lp, vp, vp, vp]
         L.redash_linear_eval.argtypes = [lp, vp, vp, vp, vp, vp]
         L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp, vp]
-        for name in ("redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale", "redash_decode",
+        for name in ("redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale", "redash_decode",
                      "redash_hash_labels", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
                      "redash_linear_garble"):
             getattr(L, name).restype = ctypes.c_int
@@ -216,6 +217,20 @@ def redash_garble_scale(params, offsets, in_zero, out_zero, tables, work, stream
         _ptr(out_zero, torch.int32, sz["label_words"], "out_zero"),
         _ptr(tables, torch.int32, sz["table_words"], "tables"),
         _ptr(work, torch.int32, sz["work_words"], "work"), _stream(stream)), "redash_garble_scale")
+
+
+def redash_garble_scale_given(params, offsets, in_zero, out_zero, tables, work, stream=None):
+    """Garble on the caller's input zero-labels (read only), e.g. a garbled
+    linear layer's output zero-labels built on the same seed's offsets."""
+    import torch
+
+    sz = redash_plan(params)
+    _check(lib().redash_garble_scale_given(
+        ctypes.byref(params), _ptr(offsets, torch.int32, sz["offset_words"], "offsets"),
+        _ptr(in_zero, torch.int32, sz["label_words"], "in_zero"),
+        _ptr(out_zero, torch.int32, sz["label_words"], "out_zero"),
+        _ptr(tables, torch.int32, sz["table_words"], "tables"),
+        _ptr(work, torch.int32, sz["work_words"], "work"), _stream(stream)), "redash_garble_scale_given")
 
 
 def redash_encode(params, x, in_zero, offsets, in_labels, stream=None):

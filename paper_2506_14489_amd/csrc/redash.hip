@@ -422,10 +422,13 @@ __device__ __forceinline__ void fold_label(const uint32_t (&A)[kMaxW], const Mod
 // B0 = H(A_{v_0}) - (v_0 mod m) R_m; colour c >= 1 gives the row
 // B0 + (v_c mod m) R_m - H(A_{v_c}), two colours per AES batch.  The walk
 // keeps B_c = B0 + (v_c mod m) R_m, starting from B_0 = H(A_{v_0}).
-template <int BLOCK>
+// GIVEN: the input zero-labels are the caller's (zin, read only; zin_w
+// unused), e.g. the output zero-labels of a garbled linear layer; otherwise
+// they are drawn from the PRG into zin_w (== zin).
+template <int BLOCK, bool GIVEN>
 __global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kGarbleWaves, kGarbleWaves)))
-k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, uint32_t *zin, uint32_t *zout,
-         uint32_t *__restrict__ tab, uint32_t *work) {
+k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, const uint32_t *zin,
+         uint32_t *zin_w, uint32_t *zout, uint32_t *__restrict__ tab, uint32_t *work) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
@@ -441,7 +444,7 @@ k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, 
     const LabelBufs LB{zin, zout, work, n, static_cast<uint32_t>(a) * 4u};
 
     // Input zero-labels Z: digits of rho(2, ga k + i) (Sec. 2.3 label sampling).
-    for (uint32_t i = 0; i < P.k; ++i) {
+    for (uint32_t i = 0; i < (GIVEN ? 0u : P.k); ++i) {
         const ModConst mc = P.mod[i];
         uint32_t s[1][4];
         uint32_t V[8];
@@ -454,7 +457,7 @@ k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, 
             aes128_encrypt_n<1>(TT, s, ArgKey{key.w});
             static_for<4>([&](auto l) { V[4 * h + l] = s[0][l]; });
         });
-        uint32_t *dst = zin + static_cast<uint64_t>(mc.woff) * n;
+        uint32_t *dst = zin_w + static_cast<uint64_t>(mc.woff) * n;
         for (uint32_t w = 0; w < mc.W; ++w) LB.put(dst, w, prg_word(V, w, mc));
     }
 
@@ -749,8 +752,13 @@ int redash_plan(const redash_params *p, redash_sizes *out) {
     return REDASH_OK;
 }
 
-int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero, uint32_t *d_out_zero,
-                        uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+template <bool GIVEN>
+int garble_scale(const redash_params *p, uint32_t *d_offsets, const uint32_t *d_in_zero, uint32_t *d_in_zero_w,
+                 uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
     Plan P;
     int rc = build_plan(p, &P);
     if (rc) return rc;
@@ -765,10 +773,24 @@ int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = kEvalTableBase;  // the AES image and the round keys
     if (lds > max_lds) return REDASH_E_HIP;
-    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_garble<kGarbleBlock>), lds))) return rc;
-    hipLaunchKernelGGL(k_garble<kGarbleBlock>, dim3(grid_for(P.n, kGarbleBlock)), dim3(kGarbleBlock), lds, stream, P,
-                       key, d_offsets, d_in_zero, d_out_zero, d_tables, d_work);
+    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_garble<kGarbleBlock, GIVEN>), lds))) return rc;
+    hipLaunchKernelGGL((k_garble<kGarbleBlock, GIVEN>), dim3(grid_for(P.n, kGarbleBlock)), dim3(kGarbleBlock), lds,
+                       stream, P, key, d_offsets, d_in_zero, d_in_zero_w, d_out_zero, d_tables, d_work);
     return launched();
+}
+
+}  // namespace
+
+extern "C" {
+
+int redash_garble_scale(const redash_params *p, uint32_t *d_offsets, uint32_t *d_in_zero, uint32_t *d_out_zero,
+                        uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
+    return garble_scale<false>(p, d_offsets, d_in_zero, d_in_zero, d_out_zero, d_tables, d_work, stream);
+}
+
+int redash_garble_scale_given(const redash_params *p, uint32_t *d_offsets, const uint32_t *d_in_zero,
+                              uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
+    return garble_scale<true>(p, d_offsets, d_in_zero, nullptr, d_out_zero, d_tables, d_work, stream);
 }
 
 int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_in_zero, const uint32_t *d_offsets,

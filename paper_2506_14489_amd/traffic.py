@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15211545.7,  # mean of two dispatches: 15,210,247 and 15,212,844
-        "write_kib": 5049479.0,  # mean of 5,049,628 and 5,049,330
-        "sources_sha256": "578f12b650b763e3e13fadb6262e026d445e8511bc4b65040044fcdaeb963149",
+        "fetch_kib": 15210134.0,  # mean of two dispatches: 15,209,093 and 15,211,175
+        "write_kib": 5049111.7,  # mean of 5,049,190 and 5,049,033
+        "sources_sha256": "36ff70a177d9a67b9fd354546002fcc505164ebfd9574f6df4ed908d78084b61",
     },
 }
 

@@ -16,7 +16,7 @@ from paper_2506_14489_amd import workloads as WL
 
 def test_library_exports_every_declared_symbol():
     names = B.declared_symbols()
-    assert set(names) == {"redash_plan", "redash_garble_scale", "redash_encode", "redash_eval_scale",
+    assert set(names) == {"redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale",
                           "redash_decode", "redash_hash_labels", "redash_strerror", "redash_linear_plan",
                           "redash_linear_prepare", "redash_linear_eval", "redash_linear_garble"}
     L = B.lib()
@@ -152,6 +152,11 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, None, fake, None) == B.REDASH_E_NULL
     assert L.redash_garble_scale(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
     assert L.redash_garble_scale(ctypes.byref(huge), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_garble_scale_given(ctypes.byref(bad), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_garble_scale_given(ctypes.byref(good), None, fake, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale_given(ctypes.byref(good), fake, None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale_given(ctypes.byref(good), fake, fake, fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_garble_scale_given(ctypes.byref(huge), fake, fake, fake, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_encode(ctypes.byref(good), None, fake, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_decode(ctypes.byref(good), fake, fake, fake, fake, None, None) == B.REDASH_E_NULL
     assert L.redash_hash_labels(6, 3, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM

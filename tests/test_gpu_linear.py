@@ -112,7 +112,10 @@ def test_linear_garble_without_bias_and_repeatability():
 # encode the int8 activations, run the layer both ways, decode every output
 # ---------------------------------------------------------------------------
 
-def _check_full_layer(w: WL.Workload, n_sample: int):
+def _run_full_layer(w: WL.Workload):
+    """Garble the layer's inputs with the gadget garbler (PRG over n_in items,
+    gadgets 0..n_in-1), encode the int8 activations, run the layer both ways.
+    Returns (shape, kshape, wt, X, Y, Zo, offsets)."""
     a, wt = WL.layer_operands(w)
     moduli = w.moduli
     if w.kind == "fc":
@@ -125,8 +128,7 @@ def _check_full_layer(w: WL.Workload, n_sample: int):
         lp = B.make_linear_params(moduli, n, c_in, h, wd, c_out, kh, kw, w.stride, w.pad)
         shape, kshape = w.in_shape, w.w_shape
     sz = B.redash_linear_plan(lp)
-    n_in, n_out = int(np.prod(shape)), w.n
-    # input zero-labels and offsets from the gadget garbler (its PRG over n_in items)
+    n_in = int(np.prod(shape))
     gp_in = B.make_params(moduli, w.scale_idx, n_in, w.seed)
     g = B.Buffers(gp_in)
     B.redash_garble_scale(gp_in, g.offsets, g.in_zero, g.out_zero, g.tables, g.work)
@@ -143,7 +145,14 @@ def _check_full_layer(w: WL.Workload, n_sample: int):
     Zo = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
     B.redash_linear_eval(lp, X, prep, work, Y)
     B.redash_linear_garble(lp, zin, prep, None, offsets, work, Zo)
-    del work
+    del work, zin
+    torch.cuda.empty_cache()
+    return shape, kshape, wt, X, Y, Zo, offsets
+
+
+def _check_full_layer(w: WL.Workload, n_sample: int):
+    moduli, n_out = w.moduli, w.n
+    shape, kshape, wt, X, Y, Zo, offsets = _run_full_layer(w)
     # decode every output with the gadget library's decode (any scale set of the base)
     gp_out = B.make_params(moduli, w.scale_idx, n_out, w.seed)
     y = torch.empty(n_out, dtype=torch.int64, device="cuda")
@@ -173,3 +182,100 @@ def test_full_size_batched_map_layer():
                          ids=lambda w: w.name)
 def test_full_size_resnet18_layer(layer):
     _check_full_layer(layer, 24)
+
+
+# ---------------------------------------------------------------------------
+# a layer feeding the scaling gadget: the gadget is garbled on the layer's
+# output zero-labels (redash_garble_scale_given), evaluated on its output
+# labels, and decodes to floor((W x + b + r)/s)
+# ---------------------------------------------------------------------------
+
+def _scaled(x, moduli, S):
+    s_ = 1
+    for i in S:
+        s_ *= moduli[i]
+    P = 1
+    for m in moduli:
+        P *= m
+    return np.floor_divide(np.asarray(x, np.int64) + (P // 2) % s_, s_)
+
+
+CHAIN = [
+    # name, moduli, S, (batch, c_in, h, w), c_out, k, stride, pad
+    ("12primes-conv3x3", tuple(WL.PRIMES_12), (10, 11), (2, 9, 7, 6), 5, 3, 1, 1),
+    ("short-base-dense", WL.SHORT_F.moduli, WL.SHORT_F.scale_idx, (40, 70, 1, 1), 9, 1, 1, 0),
+    ("pow2-conv-stride2", (3, 5, 7, 11, 32), (4,), (1, 6, 9, 8), 4, 3, 2, 1),
+]
+
+
+@pytest.mark.parametrize("case", CHAIN, ids=[c[0] for c in CHAIN])
+def test_layer_feeds_gadget_matches_oracle(case):
+    from oracle import oracle as O
+
+    name, moduli, S, shape, c_out, k, stride, pad = case
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    seed, n_in = 31, int(np.prod(shape))
+    x = rng.integers(-8, 9, size=shape)
+    wts = rng.integers(-20, 21, size=(c_out, shape[1], k, k))
+    bias = rng.integers(-100, 101, size=c_out)
+    out_shape = OL.conv_out_shape(*shape, c_out, k, k, stride, pad)
+    n_out = int(np.prod(out_shape))
+    a0 = n_in  # the layer-output gadgets follow the input gadgets: distinct tweaks
+    # oracle chain
+    op_in = O.make_params(list(moduli), list(S), n_in, seed)
+    offs, zin, _z, _t = O.garble(op_in, 0, n_in, with_tables=False)
+    Xo = O.encode(op_in, x.reshape(-1), zin, offs)
+    Yo = OL.conv_labels(moduli, Xo, shape, wts, stride, pad)
+    Zo = OL.garble_conv(moduli, zin, shape, wts, bias, offs, stride, pad)
+    op = O.make_params(list(moduli), list(S), n_out, seed)
+    _o, gz_exp, tab_exp = O.garble_given(op, a0, n_out, Zo)
+    out_exp = O.evaluate(op, a0, n_out, Yo, tab_exp)
+    # GPU chain
+    gp_in = B.make_params(moduli, S, n_in, seed)
+    g = B.Buffers(gp_in)
+    B.redash_garble_scale(gp_in, g.offsets, g.in_zero, g.out_zero, g.tables, g.work)
+    B.redash_encode(gp_in, torch.from_numpy(x.reshape(-1).astype(np.int64)).cuda(), g.in_zero, g.offsets,
+                    g.in_labels)
+    lp = B.make_linear_params(moduli, *shape, c_out, k, k, stride, pad)
+    sz = B.redash_linear_plan(lp)
+    prep, work = _dev_u8(sz["prepared_bytes"]), _dev_u8(sz["work_bytes"])
+    B.redash_linear_prepare(lp, H.to_dev(wts.astype(np.int32)), prep)
+    Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    Z = torch.empty(sz["out_label_words"], dtype=torch.int32, device="cuda")
+    B.redash_linear_eval(lp, g.in_labels, prep, work, Y)
+    B.redash_linear_garble(lp, g.in_zero, prep, H.to_dev(bias.astype(np.int64)), g.offsets, work, Z)
+    gp = B.make_params(moduli, S, n_out, seed, a0)
+    gb = B.Buffers(gp)
+    B.redash_garble_scale_given(gp, gb.offsets, Z, gb.out_zero, gb.tables, gb.work)
+    B.redash_eval_scale(gp, Y, gb.tables, gb.out_labels, gb.work)
+    B.redash_decode(gp, gb.out_labels, gb.out_zero, gb.offsets, gb.y, gb.bad)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.to_u32(gb.offsets), offs)
+    assert np.array_equal(H.to_u32(Z), Zo) and np.array_equal(H.to_u32(Y), Yo)
+    assert np.array_equal(H.to_u32(gb.out_zero), gz_exp)
+    assert np.array_equal(H.to_u32(gb.tables)[: len(tab_exp)], tab_exp)
+    assert np.array_equal(H.to_u32(gb.out_labels), out_exp)
+    # the decoded value, from the plain integer convolution
+    lin = torch.nn.functional.conv2d(torch.from_numpy(x).double(), torch.from_numpy(wts).double(),
+                                     torch.from_numpy(bias).double(), stride=stride, padding=pad)
+    assert int(gb.bad.item()) == 0
+    assert np.array_equal(gb.y[:n_out].cpu().numpy(), _scaled(lin.numpy().reshape(-1).astype(np.int64), moduli, S))
+
+
+def test_full_size_batched_map_layer_feeds_gadget():
+    """The 3x3x64 layer of the 16x64x56x56 batched map, then the scaling
+    gadget on its 3.2M outputs: every output decodes to floor((conv + r)/s)."""
+    w = WL.BATCHED
+    _shape, _ks, _wt, X, Y, Zo, offsets = _run_full_layer(w)
+    del X
+    torch.cuda.empty_cache()
+    n_in = int(np.prod(w.in_shape))
+    gp = B.make_params(w.moduli, w.scale_idx, w.n, w.seed, n_in)
+    gb = B.Buffers(gp)
+    B.redash_garble_scale_given(gp, gb.offsets, Zo, gb.out_zero, gb.tables, gb.work)
+    B.redash_eval_scale(gp, Y, gb.tables, gb.out_labels, gb.work)
+    B.redash_decode(gp, gb.out_labels, gb.out_zero, gb.offsets, gb.y, gb.bad)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.to_u32(gb.offsets), H.to_u32(offsets))
+    assert int(gb.bad.item()) == 0
+    assert np.array_equal(gb.y.cpu().numpy(), _scaled(WL.make_inputs(w), w.moduli, w.scale_idx))

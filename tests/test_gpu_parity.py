@@ -15,6 +15,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
+from oracle import linear as OL  # noqa: E402
 from oracle import oracle as O  # noqa: E402
 from oracle import rns  # noqa: E402
 from paper_2506_14489_amd import binding as B  # noqa: E402
@@ -128,6 +129,26 @@ def test_garble_matches_oracle(case):
     assert np.array_equal(H.to_u32(buf.in_zero), zin)
     assert np.array_equal(H.to_u32(buf.out_zero), zout)
     assert np.array_equal(H.to_u32(buf.tables)[: len(tab)], tab)
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_garble_on_given_zero_labels_matches_oracle(case):
+    """redash_garble_scale_given on arbitrary valid zero-labels (as a free
+    operation would leave them) against the oracle, word for word; the
+    given labels are left untouched."""
+    name, moduli, S, n, seed, a0 = case
+    bp, op = _params_pair(moduli, S, n, seed, a0)
+    rng = np.random.default_rng(seed + 500)
+    zin = OL.pack(moduli, [rng.integers(0, m, size=(n, O.lam(m))) for m in moduli], n)
+    buf = B.Buffers(bp)
+    zd = H.to_dev(zin)
+    B.redash_garble_scale_given(bp, buf.offsets, zd, buf.out_zero, buf.tables, buf.work)
+    torch.cuda.synchronize()
+    offs, zout, tab = O.garble_given(op, a0, n, zin)
+    assert np.array_equal(H.to_u32(buf.offsets), offs)
+    assert np.array_equal(H.to_u32(buf.out_zero), zout)
+    assert np.array_equal(H.to_u32(buf.tables)[: len(tab)], tab)
+    assert np.array_equal(H.to_u32(zd), zin)
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
