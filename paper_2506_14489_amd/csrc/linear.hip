@@ -72,6 +72,7 @@ struct LinPlan {
     uint32_t astride;             // LDS bytes per staged weight row
     uint32_t ostride;             // words per output-channel row of the merged output words
     uint32_t xw, xstride;         // staged input columns of a tile; LDS bytes per staged column
+    uint32_t wpair;               // staging: the two columns of an 8-lane write group lie wpair apart
     uint32_t halo;                // LDS bytes of one residue's staged input (kh xw xstride)
     uint32_t lds_a, lds_b, lds_o, lds_bytes;
     uint32_t npairs;
@@ -176,13 +177,26 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     L->kw_magic = static_cast<uint32_t>(((1ull << 32) + p->kw - 1) / p->kw);
     L->o_pad = round_up(p->c_out, kLinOTile);
     L->ogroups = L->o_pad / kLinOTile;
-    // weight rows padded by 16 bytes: 8 consecutive rows fall in distinct bank groups
-    L->astride = L->kc + 16;
+    // 16-byte LDS reads of 16 rows (or columns) at a stride of S bytes, four
+    // 16-byte chunks each, run without bank conflicts on this LDS when
+    // S / 16 = 2 mod 4 (measured: 96, 160, 224, 608 are conflict-free; 80,
+    // 112, 128, 592 are not).  Weight rows: kc is a multiple of 64, so kc + 32.
+    L->astride = L->kc + 32;
     L->lds_a = kLinOTile * L->astride;
     // Staged input: per residue kh rows of xw columns of ck channel bytes,
-    // columns padded to xstride (16-byte accesses of 8 consecutive columns
-    // then fall in distinct bank groups; ck = 16 needs no padding).
-    L->xstride = ck == 16 ? 16 : ck + 16;
+    // columns padded to xstride.  A fragment reads 16 columns conv-stride
+    // apart: with 64-channel chunks the padding makes stride * xstride / 16
+    // = 2 mod 4 where it can (odd strides: 96 bytes; strides 2 mod 4: 80).
+    // 16-byte LDS writes go 8 lanes per cycle over 32 banks: the 8 lanes of
+    // a write group take two columns wpair apart so that their 4 chunks each
+    // fall in distinct bank groups (xstride / 16 = 6: 2 apart; 5: 4 apart).
+    if (ck == 64) {
+        L->xstride = (p->stride % 2 == 1) ? 96 : 80;
+        L->wpair = L->xstride == 96 ? 2 : 4;
+    } else {
+        L->xstride = ck == 16 ? 16 : ck + 16;
+        L->wpair = 1;
+    }
     // tile width: 32 or 16 positions, no wider than the row needs (64 would
     // not fit the registers of two waves per SIMD), and at most 512 staged
     // 16-byte pieces per residue (two per thread)
@@ -195,8 +209,10 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     L->halo = L->kh * L->xw * L->xstride;
     L->ostride = L->xt + 4;  // the four lane groups of an atomic OR fall 16 banks apart
     L->lds_b = 4 * L->halo;
+    // the merged output words overlay the staged inputs (used at the end of
+    // a packed word, after every wave has read its fragments)
     L->lds_o = kLinOTile * L->ostride * 4;
-    L->lds_bytes = L->lds_a + L->lds_b + L->lds_o;
+    L->lds_bytes = L->lds_a + (L->lds_b > L->lds_o ? L->lds_b : L->lds_o);
     if (L->lds_bytes > kLinMaxLds) return REDASH_E_PARAM;
     L->xtiles = (L->cols + L->xt - 1) / L->xt;
     L->plane_bytes = static_cast<uint64_t>(L->nimg) * L->hp * L->wp * L->cp;
@@ -372,16 +388,17 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
 // ---------------------------------------------------------------------------
 // The contraction.
 // ---------------------------------------------------------------------------
-// K33: a 3x3 kernel with 64-channel chunks (taps = K steps, kc = 576), the K
-// loop unrolled with every fragment offset known but the row stride.
-template <int NCB, bool GARBLE, bool K33>
+// K33 (> 0): a 3x3 kernel with 64-channel chunks (taps = K steps, kc = 576)
+// and K33 bytes per staged column, the K loop unrolled with every fragment
+// offset known but the row stride; 0: any kernel.
+template <int NCB, bool GARBLE, int K33>
 __global__ void __launch_bounds__(kLinBlock) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t *__restrict__ prep,
               const int64_t *__restrict__ bias, const uint32_t *__restrict__ offsets, uint32_t *__restrict__ out) {
     extern __shared__ __align__(16) uint8_t lds[];
     uint8_t *Al = lds;
     uint8_t *Bl = lds + L.lds_a;
-    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a + L.lds_b);
+    uint32_t *Ol = reinterpret_cast<uint32_t *>(lds + L.lds_a);  // overlays Bl
 
     const uint32_t tid = threadIdx.x, lane = tid % 64;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid / 64);
@@ -438,7 +455,12 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
         const uint32_t e = tid + t * kLinBlock;
         pval[t] = e < pieces;
         const uint32_t ee = pval[t] ? e : 0u;
-        const uint32_t c16 = ee % c16n, xin = (ee / c16n) % L.xw, dy = ee / (c16n * L.xw);
+        const uint32_t c16 = ee % c16n, dy = ee / (c16n * L.xw);
+        // column of this piece: within each full group of 2 wpair columns,
+        // write slot j takes column j / 2 + (j % 2) wpair (a bijection)
+        uint32_t xin = (ee / c16n) % L.xw;
+        const uint32_t grp = 2 * L.wpair, gb = xin - xin % grp;
+        if (gb + grp <= L.xw) xin = gb + (xin - gb) / 2 + ((xin - gb) % 2) * L.wpair;
         uint32_t xp = x0 * L.stride + xin;
         xp = xp < L.wp ? xp : L.wp - 1;
         poff[t] = ((img * L.hp + row * L.stride + dy) * L.wp + xp) * L.cp + 16 * c16;
@@ -535,9 +557,9 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
         __syncthreads();
         if (j < g) {
             const uint8_t *Bw = Bl + wave * L.halo;
-            if constexpr (K33) {
+            if constexpr (K33 > 0) {
                 // K step t is tap t = 3 dy + dx, the lane's 16 channels at kg
-                const uint8_t *Ar = Al + (lane % 16) * (576 + 16) + kg;
+                const uint8_t *Ar = Al + (lane % 16) * (576 + 32) + kg;
 #pragma unroll
                 for (int dy = 0; dy < 3; ++dy) {
                     const uint8_t *Br = Bw + dy * rowb + kg;
@@ -547,10 +569,10 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
                         v4i a[4];
 #pragma unroll
                         for (int ob = 0; ob < 4; ++ob)
-                            a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 16) + kk * 64);
+                            a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 32) + kk * 64);
 #pragma unroll
                         for (int cb = 0; cb < NCB; ++cb) {
-                            const v4i bf = *reinterpret_cast<const v4i *>(Br + colb[cb] + dx * (64 + 16));
+                            const v4i bf = *reinterpret_cast<const v4i *>(Br + colb[cb] + dx * K33);
 #pragma unroll
                             for (int ob = 0; ob < 4; ++ob)
                                 acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
@@ -603,7 +625,10 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
         }
         advance(cur);
         if (cur.w != w) {
-            // word w complete: merge the waves' fields (disjoint bits), store whole words
+            // word w complete: merge the waves' fields (disjoint bits), store
+            // whole words.  Ol overlays the staged inputs: every wave must be
+            // done with its fragments first.
+            __syncthreads();
             for (uint32_t e = tid; e < kLinOTile * L.ostride; e += kLinBlock) Ol[e] = 0;
             __syncthreads();
 #pragma unroll
@@ -629,6 +654,259 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     }
 }
 
+// ---------------------------------------------------------------------------
+// The contraction for one channel chunk (ncc = 1), with independent waves.
+// A workgroup stages the weights of its modulus and 64 output channels once;
+// then each wave takes its own tile (one output row segment of XT positions,
+// the 64 channels), stages its own input halo and runs through every residue
+// of every packed word of the modulus in turn: MFMA over the halo, the next
+// residue's halo written over it (LDS operations of a wave complete in
+// order), the one after loaded into registers, the epilogue, and each packed
+// word stored whole when its last residue is done.  No barrier after the
+// weights are staged.
+// ---------------------------------------------------------------------------
+constexpr int kWavePieces = 8;  // staged 16-byte pieces per lane (a halo has at most 512)
+
+template <int NCB, bool GARBLE, int K33>
+__global__ void __launch_bounds__(kLinBlock) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t *__restrict__ prep,
+                const int64_t *__restrict__ bias, const uint32_t *__restrict__ offsets, uint32_t *__restrict__ out) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    uint8_t *Al = lds;
+    const uint32_t tid = threadIdx.x, lane = tid % 64;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid / 64);
+    uint8_t *Bw = lds + L.lds_a + wave * L.halo;
+    // accumulator seeds per output channel: 128 rowsum (m > 128) + off, and
+    // for the garbler (-b mod m), to be multiplied by R_j
+    int32_t *seed = reinterpret_cast<int32_t *>(lds + L.lds_a + 4 * L.halo);
+    int32_t *negb = seed + kLinOTile;
+    const uint32_t i = blockIdx.y, og = blockIdx.z;
+    const LinMod M = L.mod[i];
+    if (tid < kLinOTile) {
+        const int32_t *rs = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
+        seed[tid] = static_cast<int32_t>((M.m > 128 ? static_cast<uint32_t>(128 * rs[tid]) : 0u) + M.off);
+        uint32_t nb = 0;
+        if constexpr (GARBLE) {
+            const uint32_t o = og * kLinOTile + tid;
+            if (bias && o < L.c_out) {
+                int64_t bm = bias[o] % static_cast<int64_t>(M.m);
+                if (bm < 0) bm += M.m;
+                nb = (M.m - static_cast<uint32_t>(bm)) % M.m;
+            }
+        }
+        negb[tid] = static_cast<int32_t>(nb);
+    }
+
+    // weights of the one chunk: 64 rows of kc bytes
+    {
+        const uint8_t *ap = prep + (static_cast<uint64_t>(i) * L.o_pad + og * kLinOTile) * L.kc;
+        const uint32_t per_row = L.kc / 16;
+        for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
+            const uint32_t rr = e / per_row, q = e % per_row;
+            *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
+                *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
+        }
+    }
+    __syncthreads();  // the only barrier
+
+    // this wave's tile; consecutive workgroups (neighbouring rows) on one XCD
+    const uint32_t nb = gridDim.x, full = nb / kXcds * kXcds;
+    const uint32_t blk = blockIdx.x < full ? (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds : blockIdx.x;
+    const uint32_t tile = blk * 4 + wave;
+    if (tile >= L.nimg * L.rows * L.xtiles) return;  // no barrier follows
+    const uint32_t xtile = tile % L.xtiles;
+    const uint32_t row = (tile / L.xtiles) % L.rows;
+    const uint32_t img = tile / (L.xtiles * L.rows);
+    constexpr uint32_t XT = 16 * NCB;
+    const uint32_t x0 = xtile * XT;
+    const uint32_t kg = 16 * (lane / 16);
+    const uint32_t rowb = L.xw * L.xstride;
+    auto o_local = [&](int ob, int r) -> uint32_t { return ob * 16 + 4 * (lane / 16) + r; };
+    const bool full_tile = x0 + XT <= L.cols && (og + 1) * kLinOTile <= L.c_out;
+
+    // staged pieces of this lane: piece e = lane + 64 s is (row dy, column,
+    // 16 channels); plane offset (column clamped into the padded row) and LDS
+    // offset; the 8 lanes of a write group take columns wpair apart
+    const uint32_t c16n = L.ck / 16;
+    const uint32_t pieces = L.kh * L.xw * c16n;
+    uint32_t poff[kWavePieces], loff[kWavePieces];
+#pragma unroll
+    for (int s = 0; s < kWavePieces; ++s) {
+        const uint32_t e = lane + 64 * s;
+        const uint32_t ee = e < pieces ? e : 0u;
+        const uint32_t c16 = ee % c16n, dy = ee / (c16n * L.xw);
+        uint32_t xin = (ee / c16n) % L.xw;
+        const uint32_t grp = 2 * L.wpair, gb = xin - xin % grp;
+        if (gb + grp <= L.xw) xin = gb + (xin - gb) / 2 + ((xin - gb) % 2) * L.wpair;
+        uint32_t xp = x0 * L.stride + xin;
+        xp = xp < L.wp ? xp : L.wp - 1;
+        poff[s] = ((img * L.hp + row * L.stride + dy) * L.wp + xp) * L.cp + 16 * c16;
+        loff[s] = e < pieces ? dy * rowb + xin * L.xstride + 16 * c16 : 0xffffffffu;  // ~0: not staged
+    }
+    uint32_t colb[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) colb[cb] = (cb * 16 + lane % 16) * L.stride * L.xstride;
+
+    // the residue sequence: (w, j) for w < W, j < g_w
+    auto g_of = [&](uint32_t w) { return (w + 1 == M.W) ? M.glast : M.g; };
+    auto plane_of = [&](uint32_t w, uint32_t j) {
+        return planes + static_cast<uint64_t>(M.lam_off + w * M.g + j) * L.plane_bytes;
+    };
+    v4i pf[kWavePieces];
+    auto load = [&](const uint8_t *plane) {
+#pragma unroll
+        for (int s = 0; s < kWavePieces; ++s) pf[s] = load16(plane, loff[s] != 0xffffffffu ? poff[s] : 0u);
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int s = 0; s < kWavePieces; ++s)
+            if (loff[s] != 0xffffffffu) *reinterpret_cast<v4i *>(Bw + loff[s]) = pf[s];
+    };
+    // (w1, j1): the residue whose pieces are in pf
+    uint32_t w1 = 0, j1 = 0;
+    auto next = [&](uint32_t &w, uint32_t &j) {
+        if (++j == g_of(w)) {
+            j = 0;
+            ++w;
+        }
+    };
+    load(plane_of(0, 0));
+    stage();
+    next(w1, j1);
+    if (w1 < M.W) load(plane_of(w1, j1));
+
+    uint32_t part[4][NCB][4];
+    v4i acc[4][NCB];
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
+
+    for (uint32_t w = 0; w < M.W; ++w) {
+        const uint32_t g = g_of(w);
+        uint32_t Rw = 0;
+        if constexpr (GARBLE) Rw = offsets[M.woff + w];
+        for (uint32_t j = 0; j < g; ++j) {
+            const int32_t Rj = GARBLE ? static_cast<int32_t>((Rw >> (M.b * j)) & ((1u << M.b) - 1u)) : 0;
+            // the seeds of this lane's 4 output channels of each row block
+            // (the C operand of the first K step)
+            v4i b0[4];
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob) {
+                b0[ob] = *reinterpret_cast<const v4i *>(seed + ob * 16 + 4 * (lane / 16));
+                if constexpr (GARBLE) b0[ob] += *reinterpret_cast<const v4i *>(negb + ob * 16 + 4 * (lane / 16)) * Rj;
+            }
+            if constexpr (K33 > 0) {
+                const uint8_t *Ar = Al + (lane % 16) * (576 + 32) + kg;
+#pragma unroll
+                for (int dy = 0; dy < 3; ++dy) {
+                    const uint8_t *Br = Bw + dy * rowb + kg;
+#pragma unroll
+                    for (int dx = 0; dx < 3; ++dx) {
+                        const int kk = 3 * dy + dx;
+                        v4i a[4];
+#pragma unroll
+                        for (int ob = 0; ob < 4; ++ob)
+                            a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 32) + kk * 64);
+#pragma unroll
+                        for (int cb = 0; cb < NCB; ++cb) {
+                            const v4i bf = *reinterpret_cast<const v4i *>(Br + colb[cb] + dx * K33);
+#pragma unroll
+                            for (int ob = 0; ob < 4; ++ob)
+                                acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, kk == 0 ? b0[ob] : acc[ob][cb],
+                                                                                    0, 0, 0);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) acc[ob][cb] = b0[ob];
+                const uint32_t ksteps = L.kc / 64;
+                for (uint32_t kk = 0; kk < ksteps; ++kk) {
+                    v4i a[4];
+#pragma unroll
+                    for (int ob = 0; ob < 4; ++ob)
+                        a[ob] = *reinterpret_cast<const v4i *>(Al + (ob * 16 + lane % 16) * L.astride + kk * 64 + kg);
+                    const uint32_t kidx = kk * 64 + kg;
+                    uint32_t tap = kidx >> L.lg_ck;
+                    if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
+                    const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+                    const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) {
+                        const v4i bf = *reinterpret_cast<const v4i *>(Bw + boff + colb[cb]);
+#pragma unroll
+                        for (int ob = 0; ob < 4; ++ob)
+                            acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, acc[ob][cb], 0, 0, 0);
+                    }
+                }
+            }
+            // the next residue's halo over this one (after this wave's reads,
+            // in LDS order), then the one after into registers
+            if (w1 < M.W) {
+                stage();
+                next(w1, j1);
+                if (w1 < M.W) load(plane_of(w1, j1));
+            }
+            // epilogue: residue of u mod m into field j
+            const uint32_t sh = M.b * j;
+            auto epilogue = [&](auto shifts) {
+#pragma unroll
+                for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const uint32_t u = static_cast<uint32_t>(acc[ob][cb][r]);
+                            uint32_t q = __umulhi(u, M.divM);  // < 2^23
+                            if constexpr (decltype(shifts)::value) q >>= M.divS;
+                            const uint32_t res =
+                                static_cast<uint32_t>(__mul24(static_cast<int32_t>(q), -static_cast<int32_t>(M.m))) + u;
+                            part[ob][cb][r] |= res << sh;
+                        }
+            };
+            if (M.divS == 0)
+                epilogue(std::integral_constant<bool, false>{});
+            else
+                epilogue(std::integral_constant<bool, true>{});
+        }
+        // word w complete: store it.  Element (ob, cb, r) of this lane is
+        // output channel og 64 + ob 16 + 4 (lane / 16) + r at position
+        // x0 + cb 16 + lane % 16: a per-lane offset plus a uniform step.
+        uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out + img * L.oN + row * L.oY +
+                         x0 * L.oX + og * kLinOTile * L.oO;
+        const uint32_t lo = 4 * (lane / 16) * L.oO + (lane % 16) * L.oX;
+        if (full_tile) {
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        uint32_t *d = dstp + (ob * 16 + r) * L.oO + cb * 16 * L.oX;
+                        d[lo] = part[ob][cb][r];
+                        part[ob][cb][r] = 0;
+                    }
+        } else {
+#pragma unroll
+            for (int ob = 0; ob < 4; ++ob)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const uint32_t o = og * kLinOTile + o_local(ob, r), x = x0 + cb * 16 + lane % 16;
+                        uint32_t *d = dstp + (ob * 16 + r) * L.oO + cb * 16 * L.oX;
+                        if (o < L.c_out && x < L.cols) d[lo] = part[ob][cb][r];
+                        part[ob][cb][r] = 0;
+                    }
+        }
+    }
+}
+
 namespace {
 
 int lin_launched() { return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP; }
@@ -641,7 +919,7 @@ int lin_allow_lds(const void *kernel, uint32_t bytes) {
                : REDASH_E_HIP;
 }
 
-template <int NCB, bool GARBLE, bool K33>
+template <int NCB, bool GARBLE, int K33>
 int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
                 const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
     int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm<NCB, GARBLE, K33>), L.lds_bytes);
@@ -653,12 +931,36 @@ int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, co
     return lin_launched();
 }
 
+template <int NCB, bool GARBLE, int K33>
+int launch_gemm_w(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
+                  const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
+    const uint32_t lds = L.lds_a + 4 * L.halo + 2 * kLinOTile * 4;
+    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm_w<NCB, GARBLE, K33>), lds);
+    if (rc) return rc;
+    const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
+    if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
+    hipLaunchKernelGGL((k_linear_gemm_w<NCB, GARBLE, K33>), dim3(static_cast<uint32_t>((tiles + 3) / 4), L.k, L.ogroups),
+                       dim3(kLinBlock), lds, stream, L, planes, prep, bias, offsets, out);
+    return lin_launched();
+}
+
 template <int NCB, bool GARBLE>
 int launch_gemm_k(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
                   const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
-    if (L.kh == 3 && L.kw == 3 && L.ck == 64)
-        return launch_gemm<NCB, GARBLE, true>(L, planes, prep, bias, offsets, out, stream);
-    return launch_gemm<NCB, GARBLE, false>(L, planes, prep, bias, offsets, out, stream);
+    // one channel chunk (and a halo of at most 8 pieces per lane): independent waves
+    if (L.ncc == 1 && L.kh * L.xw * (L.ck / 16) <= 64 * kWavePieces &&
+        L.lds_a + 4 * L.halo + 2 * kLinOTile * 4 <= kLinMaxLds) {
+        if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 96)
+            return launch_gemm_w<NCB, GARBLE, 96>(L, planes, prep, bias, offsets, out, stream);
+        if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 80)
+            return launch_gemm_w<NCB, GARBLE, 80>(L, planes, prep, bias, offsets, out, stream);
+        return launch_gemm_w<NCB, GARBLE, 0>(L, planes, prep, bias, offsets, out, stream);
+    }
+    if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 96)
+        return launch_gemm<NCB, GARBLE, 96>(L, planes, prep, bias, offsets, out, stream);
+    if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 80)
+        return launch_gemm<NCB, GARBLE, 80>(L, planes, prep, bias, offsets, out, stream);
+    return launch_gemm<NCB, GARBLE, 0>(L, planes, prep, bias, offsets, out, stream);
 }
 
 template <bool GARBLE>
