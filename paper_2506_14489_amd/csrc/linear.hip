@@ -667,7 +667,8 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
 // ---------------------------------------------------------------------------
 constexpr int kWavePieces = 8;  // staged 16-byte pieces per lane (a halo has at most 512)
 
-template <int NCB, bool GARBLE, int K33>
+// PL: staged pieces per lane (a 3x3 halo of 64-channel columns has at most 7 x 64)
+template <int NCB, bool GARBLE, int K33, int PL>
 __global__ void __launch_bounds__(kLinBlock) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t *__restrict__ prep,
                 const int64_t *__restrict__ bias, const uint32_t *__restrict__ offsets, uint32_t *__restrict__ out) {
@@ -726,12 +727,15 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
 
     // staged pieces of this lane: piece e = lane + 64 s is (row dy, column,
     // 16 channels); plane offset (column clamped into the padded row) and LDS
-    // offset; the 8 lanes of a write group take columns wpair apart
+    // offset (16 bits, 0xffff: not staged; two per register); the 8 lanes of
+    // a write group take columns wpair apart
     const uint32_t c16n = L.ck / 16;
     const uint32_t pieces = L.kh * L.xw * c16n;
-    uint32_t poff[kWavePieces], loff[kWavePieces];
+    uint32_t poff[PL], loff2[(PL + 1) / 2];
 #pragma unroll
-    for (int s = 0; s < kWavePieces; ++s) {
+    for (int s = 0; s < (PL + 1) / 2; ++s) loff2[s] = 0;
+#pragma unroll
+    for (int s = 0; s < PL; ++s) {
         const uint32_t e = lane + 64 * s;
         const uint32_t ee = e < pieces ? e : 0u;
         const uint32_t c16 = ee % c16n, dy = ee / (c16n * L.xw);
@@ -741,39 +745,34 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
         uint32_t xp = x0 * L.stride + xin;
         xp = xp < L.wp ? xp : L.wp - 1;
         poff[s] = ((img * L.hp + row * L.stride + dy) * L.wp + xp) * L.cp + 16 * c16;
-        loff[s] = e < pieces ? dy * rowb + xin * L.xstride + 16 * c16 : 0xffffffffu;  // ~0: not staged
+        const uint32_t lo = e < pieces ? dy * rowb + xin * L.xstride + 16 * c16 : 0xffffu;
+        loff2[s / 2] |= lo << (16 * (s % 2));
     }
+    auto loff = [&](int s) -> uint32_t { return (loff2[s / 2] >> (16 * (s % 2))) & 0xffffu; };
     uint32_t colb[NCB];
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) colb[cb] = (cb * 16 + lane % 16) * L.stride * L.xstride;
 
-    // the residue sequence: (w, j) for w < W, j < g_w
+    // residue rr = w g + j of the modulus (field j of packed word w) is
+    // plane lam_off + rr; the halo of residue rr + 1 is staged after the
+    // operations of residue rr, its pieces loaded one residue ahead
     auto g_of = [&](uint32_t w) { return (w + 1 == M.W) ? M.glast : M.g; };
-    auto plane_of = [&](uint32_t w, uint32_t j) {
-        return planes + static_cast<uint64_t>(M.lam_off + w * M.g + j) * L.plane_bytes;
-    };
-    v4i pf[kWavePieces];
-    auto load = [&](const uint8_t *plane) {
+    const uint32_t lam = (M.W - 1) * M.g + M.glast;
+    v4i pf[PL];
+    auto load = [&](uint32_t rr) {
+        const uint8_t *plane = planes + static_cast<uint64_t>(M.lam_off + rr) * L.plane_bytes;
 #pragma unroll
-        for (int s = 0; s < kWavePieces; ++s) pf[s] = load16(plane, loff[s] != 0xffffffffu ? poff[s] : 0u);
+        for (int s = 0; s < PL; ++s) pf[s] = load16(plane, lane + 64 * s < pieces ? poff[s] : 0u);
     };
     auto stage = [&]() {
 #pragma unroll
-        for (int s = 0; s < kWavePieces; ++s)
-            if (loff[s] != 0xffffffffu) *reinterpret_cast<v4i *>(Bw + loff[s]) = pf[s];
+        for (int s = 0; s < PL; ++s)
+            if (lane + 64 * s < pieces) *reinterpret_cast<v4i *>(Bw + loff(s)) = pf[s];
     };
-    // (w1, j1): the residue whose pieces are in pf
-    uint32_t w1 = 0, j1 = 0;
-    auto next = [&](uint32_t &w, uint32_t &j) {
-        if (++j == g_of(w)) {
-            j = 0;
-            ++w;
-        }
-    };
-    load(plane_of(0, 0));
+    load(0);
     stage();
-    next(w1, j1);
-    if (w1 < M.W) load(plane_of(w1, j1));
+    if (1 < lam) load(1);
+    uint32_t rr = 0;  // the residue being computed
 
     uint32_t part[4][NCB][4];
     v4i acc[4][NCB];
@@ -799,26 +798,41 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                 if constexpr (GARBLE) b0[ob] += *reinterpret_cast<const v4i *>(negb + ob * 16 + 4 * (lane / 16)) * Rj;
             }
             if constexpr (K33 > 0) {
+                // K step kk = 3 dy + dx; the fragments of step kk + 1 are
+                // loaded before the matrix-core operations of step kk
                 const uint8_t *Ar = Al + (lane % 16) * (576 + 32) + kg;
+                auto frag = [&](int kk, v4i(&a)[4], v4i(&bq)[NCB]) {
 #pragma unroll
-                for (int dy = 0; dy < 3; ++dy) {
-                    const uint8_t *Br = Bw + dy * rowb + kg;
+                    for (int ob = 0; ob < 4; ++ob)
+                        a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 32) + kk * 64);
+                    const uint8_t *Br = Bw + (kk / 3) * rowb + kg + (kk % 3) * K33;
 #pragma unroll
-                    for (int dx = 0; dx < 3; ++dx) {
-                        const int kk = 3 * dy + dx;
-                        v4i a[4];
+                    for (int cb = 0; cb < NCB; ++cb) bq[cb] = *reinterpret_cast<const v4i *>(Br + colb[cb]);
+                };
+                auto mma = [&](int kk, const v4i(&a)[4], const v4i(&bq)[NCB]) {
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
                         for (int ob = 0; ob < 4; ++ob)
-                            a[ob] = *reinterpret_cast<const v4i *>(Ar + ob * 16 * (576 + 32) + kk * 64);
+                            acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bq[cb], kk == 0 ? b0[ob] : acc[ob][cb],
+                                                                                0, 0, 0);
+                };
+                v4i fa0[4], fb0[NCB], fa1[4], fb1[NCB];
+                frag(0, fa0, fb0);
 #pragma unroll
-                        for (int cb = 0; cb < NCB; ++cb) {
-                            const v4i bf = *reinterpret_cast<const v4i *>(Br + colb[cb] + dx * K33);
-#pragma unroll
-                            for (int ob = 0; ob < 4; ++ob)
-                                acc[ob][cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ob], bf, kk == 0 ? b0[ob] : acc[ob][cb],
-                                                                                    0, 0, 0);
-                        }
+                for (int kk = 0; kk < 9; ++kk) {
+                    // (scheduling barriers keep the loads of step kk + 1
+                    // ahead of the operations of step kk)
+                    if (kk % 2 == 0) {
+                        if (kk + 1 < 9) frag(kk + 1, fa1, fb1);
+                        __builtin_amdgcn_sched_barrier(0);
+                        mma(kk, fa0, fb0);
+                    } else {
+                        if (kk + 1 < 9) frag(kk + 1, fa0, fb0);
+                        __builtin_amdgcn_sched_barrier(0);
+                        mma(kk, fa1, fb1);
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             } else {
 #pragma unroll
@@ -846,12 +860,12 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                 }
             }
             // the next residue's halo over this one (after this wave's reads,
-            // in LDS order), then the one after into registers
-            if (w1 < M.W) {
+            // in LDS order), then the one after into the registers
+            if (rr + 1 < lam) {
                 stage();
-                next(w1, j1);
-                if (w1 < M.W) load(plane_of(w1, j1));
+                if (rr + 2 < lam) load(rr + 2);
             }
+            ++rr;
             // epilogue: residue of u mod m into field j
             const uint32_t sh = M.b * j;
             auto epilogue = [&](auto shifts) {
@@ -934,12 +948,14 @@ int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, co
 template <int NCB, bool GARBLE, int K33>
 int launch_gemm_w(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, const int64_t *bias,
                   const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
+    constexpr int PL = K33 > 0 ? 7 : kWavePieces;
+    if (L.kh * L.xw * (L.ck / 16) > 64u * PL || L.halo > 0xffffu) return REDASH_E_PARAM;  // not reached
     const uint32_t lds = L.lds_a + 4 * L.halo + 2 * kLinOTile * 4;
-    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm_w<NCB, GARBLE, K33>), lds);
+    int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm_w<NCB, GARBLE, K33, PL>), lds);
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear_gemm_w<NCB, GARBLE, K33>), dim3(static_cast<uint32_t>((tiles + 3) / 4), L.k, L.ogroups),
+    hipLaunchKernelGGL((k_linear_gemm_w<NCB, GARBLE, K33, PL>), dim3(static_cast<uint32_t>((tiles + 3) / 4), L.k, L.ogroups),
                        dim3(kLinBlock), lds, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
 }
@@ -950,10 +966,9 @@ int launch_gemm_k(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, 
     // one channel chunk (and a halo of at most 8 pieces per lane): independent waves
     if (L.ncc == 1 && L.kh * L.xw * (L.ck / 16) <= 64 * kWavePieces &&
         L.lds_a + 4 * L.halo + 2 * kLinOTile * 4 <= kLinMaxLds) {
-        if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 96)
-            return launch_gemm_w<NCB, GARBLE, 96>(L, planes, prep, bias, offsets, out, stream);
-        if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 80)
-            return launch_gemm_w<NCB, GARBLE, 80>(L, planes, prep, bias, offsets, out, stream);
+        const bool k33 = L.kh == 3 && L.kw == 3 && L.ck == 64 && 3 * L.xw * 4 <= 7 * 64;
+        if (k33 && L.xstride == 96) return launch_gemm_w<NCB, GARBLE, 96>(L, planes, prep, bias, offsets, out, stream);
+        if (k33 && L.xstride == 80) return launch_gemm_w<NCB, GARBLE, 80>(L, planes, prep, bias, offsets, out, stream);
         return launch_gemm_w<NCB, GARBLE, 0>(L, planes, prep, bias, offsets, out, stream);
     }
     if (L.kh == 3 && L.kw == 3 && L.ck == 64 && L.xstride == 96)
