@@ -19,13 +19,18 @@
 //                    i for every input position, channel-last with the zero
 //                    padding already in place, so that a 16-byte load gives a
 //                    matrix-core fragment of 16 channels (HBM-bound);
-//   k_linear_gemm    per workgroup: one modulus, 64 output channels and a row
-//                    segment of XT (32 or 16) output positions; wave q takes
-//                    residue j0 + q of each packed word, 4 x (XT/16) MFMA 16x16x64
-//                    tiles, the weights staged in LDS, the input fragments
-//                    loaded from the planes; the int32 sums are reduced mod m
-//                    and the residues of a word merged across the waves in LDS
-//                    into PK32 words, stored coalesced.
+//   k_linear_gemm_w  (one channel chunk) per workgroup: one modulus and 64
+//                    output channels, the weights staged in LDS once; each
+//                    wave then takes its own row segment of XT (32 or 16)
+//                    output positions, 4 x (XT/16) MFMA 16x16x64 tiles, and
+//                    runs through every residue of the modulus with its own
+//                    staged input halo, reducing the int32 sums mod m into
+//                    PK32 fields and storing each packed word whole;
+//   k_linear_gemm    (several channel chunks) per workgroup: one modulus, 64
+//                    output channels and a row segment; wave q takes residue
+//                    j0 + q of each packed word, the halos and the weights of
+//                    each chunk staged by the workgroup, the residues of a
+//                    word merged across the waves in LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
