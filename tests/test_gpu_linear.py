@@ -52,6 +52,11 @@ SMALL = [
     ("dense", tuple(WL.PRIMES_12), (33, 100, 1, 1), 70, 1, 1, 1, 0),
     ("dense-batch1", (32, 167, 173), (1, 512, 1, 1), 10, 1, 1, 1, 0),
     ("short-base-conv", (32, 97, 107), (1, 64, 5, 5), 64, 3, 3, 1, 1),
+    # one 64-channel chunk: the kernel with independent waves, 3x3 paths
+    ("conv3x3-64ch-ragged-tiles", (3, 5, 7, 11, 13), (1, 64, 4, 70), 8, 3, 3, 1, 1),
+    ("conv3x3-64ch-stride2", (2, 3, 5, 7), (2, 64, 9, 20), 6, 3, 3, 2, 1),
+    ("conv3x3-64ch-m251-three-groups", (2, 251), (1, 64, 5, 9), 130, 3, 3, 1, 1),
+    ("conv3x3-64ch-whole-tiles", (5, 7, 64), (1, 64, 3, 64), 64, 3, 3, 1, 1),
 ]
 
 
@@ -178,8 +183,8 @@ def test_full_size_batched_map_layer():
     _check_full_layer(WL.BATCHED, 48)
 
 
-@pytest.mark.parametrize("layer", [WL.RESNET18[0], WL.RESNET18[7], WL.RESNET18[16], WL.RESNET18[-1]],
-                         ids=lambda w: w.name)
+@pytest.mark.parametrize("layer", [WL.RESNET18[0], WL.RESNET18[5], WL.RESNET18[7], WL.RESNET18[16],
+                                   WL.RESNET18[-1]], ids=lambda w: w.name)
 def test_full_size_resnet18_layer(layer):
     _check_full_layer(layer, 24)
 
