@@ -145,9 +145,10 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     }
 
 
-def time_short_base(w, steps: int, warmup: int, dev):
-    """Garble, encode and time the evaluator on one short-base workload;
-    decode and check every gadget afterwards.  Returns a summary dict."""
+def time_workload(w, steps: int, warmup: int, dev, values: str = "values uniform over the signed range"):
+    """Garble, encode and time the evaluator on one workload (HIP events over
+    `steps` calls); decode and check every gadget afterwards.  Returns a
+    summary dict."""
     import torch
 
     from paper_2506_14489_amd import binding as B
@@ -182,7 +183,7 @@ def time_short_base(w, steps: int, warmup: int, dev):
     gbs = cost.bytes_per_gadget(w.moduli, w.scale_idx) * n / (ms / 1e3) / 1e9
     log(f"{w.name}: eval {ms:.3f} ms per call, {n / (ms / 1e3):.3e} gadgets/s")
     return {
-        "workload": f"{w.name}: {n} gadgets, values uniform over the signed range",
+        "workload": f"{w.name}: {n} gadgets, {values}",
         "moduli": list(w.moduli),
         "scale": w.s,
         "gates_per_gadget": len(cost.gates(w.moduli, w.scale_idx)),
@@ -193,6 +194,52 @@ def time_short_base(w, steps: int, warmup: int, dev):
         "check": "decode = floor((x + (floor(P/2) mod s))/s) with every label valid, all gadgets",
         "steps": steps,
     }
+
+
+def time_resnet18(steps: int, warmup: int, dev):
+    """The 21 ResNet-18 layers one after another (each layer's activations from
+    its own int8 input and weights): sum of gadgets over sum of the per-layer
+    evaluation times."""
+    from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import workloads as WL
+
+    layers, n_tot, ms_tot, ops_tot = [], 0, 0.0, 0
+    for w in WL.RESNET18:
+        r = time_workload(w, steps, warmup, dev, values="the layer's exact conv/fc outputs")
+        layers.append({"layer": w.name, "gadgets": w.n, "scale": w.s, "ms_per_call": r["ms_per_call"]})
+        n_tot += w.n
+        ms_tot += r["ms_per_call"]
+        ops_tot += cost.ops_per_gadget(w.moduli, w.scale_idx) * w.n
+    tops = ops_tot / (ms_tot / 1e3) / 1e12
+    log(f"resnet18: {n_tot} gadgets in {ms_tot:.3f} ms over {len(layers)} layers")
+    return {
+        "gadgets": n_tot,
+        "ms_total": round(ms_tot, 4),
+        "gadgets_per_s": round(n_tot / (ms_tot / 1e3), 1),
+        "alu_frac": round(tops / ALU_PEAK_TOPS, 4),
+        "check": "every layer: decode = floor((x + (floor(P/2) mod s))/s) with every label valid",
+        "layers": layers,
+    }
+
+
+def copy_bandwidth(dev, mib: int = 2048, reps: int = 5) -> float:
+    """GB/s of a device-to-device copy (bytes read + bytes written)."""
+    import torch
+
+    src = torch.ones(mib * (1 << 20) // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * src.numel() * 4 * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
 
 
 def main():
@@ -209,6 +256,8 @@ def main():
                     help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
     ap.add_argument("--no-linear", action="store_true",
                     help="skip timing the garbled conv layer that produces the workload's activations")
+    ap.add_argument("--no-resnet18", action="store_true",
+                    help="skip timing the 21 ResNet-18 layers (sum of gadgets over sum of per-layer times)")
     ap.add_argument("--no-short-bases", action="store_true",
                     help="skip timing the evaluator on the short and power-of-two bases of Sec. 4")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -302,6 +351,15 @@ def main():
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
     log(f"eval: {ms_step:.3f} ms per call (events), wall {wall * 1e3 / args.steps:.3f} ms per call")
+    # the same number of calls again, each between its own pair of events: the median call
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for e0, e1 in evs:
+        e0.record(stream)
+        B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms_median = float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
+    log(f"eval: median {ms_median:.3f} ms per call over {args.steps} separately timed calls")
 
     check = "skipped"
     if not args.no_check:
@@ -315,6 +373,8 @@ def main():
         log(check)
 
     gadgets_per_s = n / (ms_step / 1e3)
+    copy_gbs = copy_bandwidth(dev)
+    log(f"device-to-device copy: {copy_gbs:.1f} GB/s (read + write)")
     bytes_g = cost.bytes_per_gadget(w.moduli, w.scale_idx)
     ops_g = cost.ops_per_gadget(w.moduli, w.scale_idx)
     lds_g = cost.lds_bytes_per_gadget(w.moduli, w.scale_idx)
@@ -362,6 +422,8 @@ def main():
             "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
             "bytes_per_gadget": round(bytes_g, 1),
             "measured_bytes_per_gadget": None if traffic_b is None else round(traffic_b / n, 1),
+            "copy_gbs": round(copy_gbs, 1),
+            "frac_of_copy": round(achieved_gbs / copy_gbs, 4),
         },
         "lds": {
             "achieved": round(lds_g * n / (ms_step / 1e3) / 1e9, 1),
@@ -371,6 +433,7 @@ def main():
             "bytes_per_gadget": lds_g,
         },
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
+        "ms_median_per_call": round(ms_median, 4),
         "check": check,
         "garble": garble,
     }
@@ -380,8 +443,10 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_short_bases:
         # the short and power-of-two bases of Sec. 4, at the batched map's gadget count
-        result["short_bases"] = [time_short_base(WL.at_size(sw, WL.BATCHED.n), max(args.steps // 2, 1),
-                                                 args.warmup, dev) for sw in WL.SHORT_BASES]
+        result["short_bases"] = [time_workload(WL.at_size(sw, WL.BATCHED.n), max(args.steps // 2, 1),
+                                               args.warmup, dev) for sw in WL.SHORT_BASES]
+    if not args.no_resnet18:
+        result["resnet18"] = time_resnet18(max(args.steps // 2, 1), args.warmup, dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -161,11 +161,10 @@ __device__ __forceinline__ void eval_update(uint32_t g, uint32_t d, const ModCon
 
 // Fills the free-operation tables (gates 0..ntab-1 that have one): byte v of
 // gate g's table is c (v mod m) mod m.  Wave w fills gates w, w + waves, ...
-template <int BLOCK>
-__device__ __forceinline__ void stage_free_op_tables(const Plan &P, uint32_t *lds, int tid) {
+__device__ __forceinline__ void stage_free_op_tables(const Plan &P, uint32_t *lds, int tid, uint32_t nwaves) {
     const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
     const uint32_t lane = static_cast<uint32_t>(tid) % 64u;
-    for (uint32_t g = wave; g < P.ntab; g += BLOCK / 64) {
+    for (uint32_t g = wave; g < P.ntab; g += nwaves) {
         const uint32_t d = P.gate[g];
         if (!gate_tab(d) || lane >= kTableBytes / 4) continue;
         const uint32_t m = P.mod[gate_dst(d)].m, c = gate_coeff(d);
@@ -237,12 +236,13 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    stage_perm_te02(lds, tid, BLOCK);
-    stage_hash_key(K, tid, BLOCK);
-    stage_free_op_tables<BLOCK>(P, lds, tid);
+    const int nthr = blockDim.x;  // BLOCK or fewer (a multiple of 64)
+    stage_perm_te02(lds, tid, nthr);
+    stage_hash_key(K, tid, nthr);
+    stage_free_op_tables(P, lds, tid, static_cast<uint32_t>(nthr) / 64u);
     __syncthreads();
     const PermTE02 TT = perm_te02();
-    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * nthr + tid;
     if (a >= P.n) return;  // no barrier follows
     const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(a) * 4u};
 
@@ -432,12 +432,13 @@ k_garble(const Plan P, const SeedKey key, const uint32_t *__restrict__ offsets, 
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    stage_perm_te02(lds, tid, BLOCK);
-    stage_hash_key(K, tid, BLOCK);
+    const int nthr = blockDim.x;  // BLOCK or fewer (a multiple of 64)
+    stage_perm_te02(lds, tid, nthr);
+    stage_hash_key(K, tid, nthr);
     __syncthreads();
     const PermTE02 TT = perm_te02();
     const LdsKey HK{K};
-    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * BLOCK + tid;
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * nthr + tid;
     if (a >= P.n) return;  // no barrier follows
     const uint64_t n = P.n;
     const uint64_t ga = P.a0 + a;
@@ -695,6 +696,21 @@ __global__ void __launch_bounds__(BLOCK) k_hash(const ModConst mq, const ModCons
 // ---------------------------------------------------------------------------
 namespace {
 
+// Threads per workgroup for n gadgets: the smallest multiple of 64 that keeps
+// the grid within one round of two workgroups per CU (the LDS image allows two),
+// at most `most`.  Small launches thus spread over every CU instead of filling
+// a few with long-running waves; large ones use `most`.
+int block_for(uint64_t n, int most, int *out) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return REDASH_E_HIP;
+    const uint64_t slots = 2ull * static_cast<uint64_t>(cus);
+    const uint64_t b = 64 * ((n + 64 * slots - 1) / (64 * slots));
+    *out = b < 64 ? 64 : (b > static_cast<uint64_t>(most) ? most : static_cast<int>(b));
+    return REDASH_OK;
+}
+
 // Largest LDS allocation a block may request on the current device.
 int max_lds_bytes(size_t *out) {
     int dev = 0, v = 0;
@@ -774,8 +790,10 @@ int garble_scale(const redash_params *p, uint32_t *d_offsets, const uint32_t *d_
     const uint32_t lds = kEvalTableBase;  // the AES image and the round keys
     if (lds > max_lds) return REDASH_E_HIP;
     if ((rc = allow_lds(reinterpret_cast<const void *>(&k_garble<kGarbleBlock, GIVEN>), lds))) return rc;
-    hipLaunchKernelGGL((k_garble<kGarbleBlock, GIVEN>), dim3(grid_for(P.n, kGarbleBlock)), dim3(kGarbleBlock), lds,
-                       stream, P, key, d_offsets, d_in_zero, d_in_zero_w, d_out_zero, d_tables, d_work);
+    int block = 0;
+    if ((rc = block_for(P.n, kGarbleBlock, &block))) return rc;
+    hipLaunchKernelGGL((k_garble<kGarbleBlock, GIVEN>), dim3(grid_for(P.n, block)), dim3(block), lds, stream, P, key,
+                       d_offsets, d_in_zero, d_in_zero_w, d_out_zero, d_tables, d_work);
     return launched();
 }
 
@@ -819,7 +837,9 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
     if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds))) return rc;
-    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, kEvalBlock)), dim3(kEvalBlock), lds, stream, P,
+    int block = 0;
+    if ((rc = block_for(P.n, kEvalBlock, &block))) return rc;
+    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, block)), dim3(block), lds, stream, P,
                        d_in_labels, d_tables, d_out_labels, d_work);
     return launched();
 }

@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15210134.0,  # mean of two dispatches: 15,209,093 and 15,211,175
-        "write_kib": 5049111.7,  # mean of 5,049,190 and 5,049,033
-        "sources_sha256": "36ff70a177d9a67b9fd354546002fcc505164ebfd9574f6df4ed908d78084b61",
+        "fetch_kib": 15213263.4,  # mean of four dispatches: 15,211,955 .. 15,213,809
+        "write_kib": 5049809.0,  # mean of four dispatches: 5,049,613 .. 5,049,921
+        "sources_sha256": "3f319bc6b82feaf8a48ffc564a46d79d89b5e51ea8583746f85edef4bf78f46c",
     },
 }
 
