@@ -232,12 +232,15 @@ def test_empty_calls_are_noops():
     offs = torch.empty(sz["offset_words"], dtype=torch.int32, device="cuda")
     e = torch.empty(1, dtype=torch.int32, device="cuda")
     B.redash_garble_scale(bp, offs, e, e, e, e)
+    offs2 = torch.empty_like(offs)
+    B.redash_garble_scale_given(bp, offs2, e, e, e, e)
     B.redash_eval_scale(bp, e, e, e, e)
     bad = torch.full((1,), 7, dtype=torch.int64, device="cuda")
     B.redash_decode(bp, e, e, offs, torch.empty(1, dtype=torch.int64, device="cuda"), bad)
     torch.cuda.synchronize()
     assert int(bad.item()) == 0
     assert np.array_equal(H.to_u32(offs), O.garble(O.make_params(WL.TINY.moduli, WL.TINY.scale_idx, 1, 0), 0, 1)[0])
+    assert np.array_equal(H.to_u32(offs2), H.to_u32(offs))
 
 
 # ---------------------------------------------------------------------------
