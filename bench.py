@@ -11,6 +11,7 @@ Prints one JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -104,6 +105,7 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
     for _ in range(warmup):
         B.redash_linear_eval(lp, X, prep, work, Y, stream)
+    gc.collect()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
@@ -164,6 +166,7 @@ def time_workload(w, steps: int, warmup: int, dev, values: str = "values uniform
     B.redash_encode(params, torch.from_numpy(x).to(dev), buf.in_zero, buf.offsets, buf.in_labels, stream)
     for _ in range(warmup):
         B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
+    gc.collect()  # no collector pause while the calls are queued
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
@@ -264,6 +267,10 @@ def main():
                     help="only run 3 device-to-device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
 
+    # The garbage collector runs only where gc.collect() is called, outside
+    # timed regions: a collection while short calls are being queued would
+    # leave the GPU idle inside the timed interval.
+    gc.disable()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(gadgets are independent: a multi-GPU run would shard them, see the design notes)",
@@ -338,6 +345,7 @@ def main():
 
     for _ in range(args.warmup):
         B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
+    gc.collect()
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)

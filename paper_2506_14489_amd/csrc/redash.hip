@@ -278,6 +278,57 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
 }
 
 // ---------------------------------------------------------------------------
+// The evaluator for calls too small to fill the GPU one gadget per lane.
+// A group of SPLIT waves shares 64 gadgets (one per lane); within a run of
+// gates that share a digit label (distinct destinations, no dependence among
+// them) wave j of the group takes gates j, j + SPLIT, ...; a workgroup
+// barrier after each run makes the updated labels (in global memory; the
+// waves of a workgroup share one write-through L1) visible to every wave
+// before the next run reads them.  The gate a wave works on stays uniform.
+// Same LDS image as k_eval.
+// ---------------------------------------------------------------------------
+template <int BLOCK, uint32_t SPLIT>
+__global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))
+k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__restrict__ tab, uint32_t *out,
+             uint32_t *work) {
+    extern __shared__ uint32_t lds[];
+    uint32_t *K = lds + kTableRegionBytes / 4;
+    const int tid = threadIdx.x;
+    const int nthr = blockDim.x;  // a multiple of 64 SPLIT, at most BLOCK
+    stage_perm_te02(lds, tid, nthr);
+    stage_hash_key(K, tid, nthr);
+    stage_free_op_tables(P, lds, tid, static_cast<uint32_t>(nthr) / 64u);
+    __syncthreads();
+    const PermTE02 TT = perm_te02();
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
+    const uint32_t part = wave % SPLIT, grp = wave / SPLIT;
+    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * (static_cast<uint32_t>(nthr) / SPLIT) + grp * 64u +
+                       static_cast<uint32_t>(tid) % 64u;
+    const bool live = a < P.n;  // dead lanes still take every barrier
+    const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(live ? a : 0) * 4u};
+    const uint64_t tau0 = (P.a0 + a) * P.G;
+    uint64_t toff = 0;  // table offset of gate g
+    for (uint32_t g = 0; g < P.G;) {
+        const uint32_t src = gate_src(P.gate[g]);
+        uint32_t r = 1;
+        while (g + r < P.G && gate_src(P.gate[g + r]) == src) ++r;
+        for (uint32_t i = 0; i < r; ++i) {
+            const uint32_t d = P.gate[g + i];
+            if (i % SPLIT == part && live) {
+                uint64_t t = toff;
+                uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW], tgt[kMaxChunk][kMaxW];
+                hash_chunk<1>(P, g + i, t, TT, K, LB, a, tau0, tab, V, row, tgt);
+                const ModConst mm = P.mod[gate_dst(d)];
+                eval_update(g + i, d, mm, V[0], row[0], tgt[0], LB);
+            }
+            toff += P.n * (P.mod[gate_src(d)].m - 1) * P.mod[gate_dst(d)].W;
+        }
+        __syncthreads();
+        g += r;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Garbler: offsets, zero-labels, garbled rows.
 // ---------------------------------------------------------------------------
 
@@ -735,6 +786,40 @@ int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
 
+// Launches one of the evaluators for n gadgets.  Calls that one round of
+// two workgroups per CU holds when a gadget takes 4 (or 2) waves use
+// k_eval_split with that split; larger calls k_eval, one gadget per lane.
+template <uint32_t SPLIT>
+int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
+                 hipStream_t stream) {
+    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval_split<kEvalBlock, SPLIT>), lds);
+    if (rc) return rc;
+    // block / SPLIT gadgets per workgroup, the block a multiple of 64 SPLIT
+    int per = 0;
+    if ((rc = block_for(P.n, kEvalBlock / static_cast<int>(SPLIT), &per))) return rc;
+    hipLaunchKernelGGL((k_eval_split<kEvalBlock, SPLIT>), dim3(grid_for(P.n, per)), dim3(per * static_cast<int>(SPLIT)),
+                       lds, stream, P, in, tab, out, work);
+    return launched();
+}
+
+int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
+                hipStream_t stream) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return REDASH_E_HIP;
+    const uint64_t round = 2ull * static_cast<uint64_t>(cus) * kEvalBlock;  // threads of one round
+    if (P.n <= round / 4) return launch_split<4>(P, lds, in, tab, out, work, stream);
+    if (P.n <= round / 2) return launch_split<2>(P, lds, in, tab, out, work, stream);
+    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds);
+    if (rc) return rc;
+    int block = 0;
+    if ((rc = block_for(P.n, kEvalBlock, &block))) return rc;
+    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, block)), dim3(block), lds, stream, P, in, tab, out, work);
+    return launched();
+}
+
+
 SeedKey seed_key(uint64_t seed) {
     RoundKeys rk = make_seed_round_keys(seed);
     SeedKey k;
@@ -836,12 +921,7 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
-    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds))) return rc;
-    int block = 0;
-    if ((rc = block_for(P.n, kEvalBlock, &block))) return rc;
-    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, block)), dim3(block), lds, stream, P,
-                       d_in_labels, d_tables, d_out_labels, d_work);
-    return launched();
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream);
 }
 
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,
