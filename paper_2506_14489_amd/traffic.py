@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15213263.4,  # mean of four dispatches: 15,211,955 .. 15,213,809
-        "write_kib": 5049809.0,  # mean of four dispatches: 5,049,613 .. 5,049,921
-        "sources_sha256": "3f319bc6b82feaf8a48ffc564a46d79d89b5e51ea8583746f85edef4bf78f46c",
+        "fetch_kib": 15211901.8,  # mean of four dispatches: 15,208,823 .. 15,213,204
+        "write_kib": 5049776.6,  # mean of four dispatches: 5,049,672 .. 5,049,889
+        "sources_sha256": "b8d3fc4d25c4989f9e3edfa15bf57ad02bc70956029c9292bb553be4bb6400e8",
     },
 }
 
