@@ -345,46 +345,85 @@ __device__ __forceinline__ v4i load16(const uint8_t *base, uint32_t off) {
     return *reinterpret_cast<const v4i *>(base + off);
 }
 
-// One thread per (padded position, 16-channel group): consecutive threads
-// write consecutive 16-byte pieces of a plane.
+// A workgroup takes 64 padded positions and one 64-channel chunk of a packed
+// word.  Loads: thread (p, c16) = (tid % 64, tid / 64) reads 16 channel words
+// of position p, so each load instruction reads 64 consecutive positions of
+// one channel plane; the words go through LDS ([position][channel], rows
+// padded to 68 words).  Stores: thread (p, c16) = (tid / 4, tid % 4) writes
+// the 16-byte piece of position p, channels 16 c16.., of every residue of the
+// word: consecutive threads write consecutive pieces.
 __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const uint32_t *__restrict__ in,
                                                        uint8_t *__restrict__ planes) {
+    __shared__ __align__(16) uint32_t T[64 * 68];
     const uint32_t pair = blockIdx.y;
     const uint32_t i = L.pair_mod[pair], w = L.pair_word[pair];
     const LinMod M = L.mod[i];
     const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
-    const uint32_t ngrp = L.cp / 16;
-    const uint32_t tid = blockIdx.x * 256 + threadIdx.x;
-    if (tid >= L.nimg * L.hp * L.wp * ngrp) return;
-    const uint32_t pp = tid / ngrp, c0 = 16 * (tid % ngrp);
-    const uint32_t xp = pp % L.wp, t = pp / L.wp;
-    const uint32_t yp = t % L.hp, img = t / L.hp;
-    const int32_t y = static_cast<int32_t>(yp) - static_cast<int32_t>(L.pad);
-    const int32_t x = static_cast<int32_t>(xp) - static_cast<int32_t>(L.pad);
-    const bool live = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
-                      x < static_cast<int32_t>(L.in_cols) && c0 < L.c_in;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t npos = L.nimg * L.hp * L.wp;
+    const uint32_t pp0 = blockIdx.x * 64, cbase = 64 * blockIdx.z;
+    const uint32_t ngrp = (L.cp - cbase) / 16 < 4 ? (L.cp - cbase) / 16 : 4u;  // 16-channel groups of this chunk
     const uint32_t flip = M.m > 128 ? 0x80808080u : 0u;
-    const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
-    const uint32_t step = L.sC * 4u;
-    // padding and channels past c_in read a valid word (position (0, 0), or
-    // the last channel) and are masked below
-    const uint32_t a0 =
-        live ? (img * L.sN + static_cast<uint32_t>(y) * L.sY + static_cast<uint32_t>(x) * L.sX + c0 * L.sC) * 4u : 0u;
-    const uint32_t last = live ? L.c_in - 1 - c0 : 0u;
+    // position of (padded) index pp: inside the input, and the word offset there
+    auto at = [&](uint32_t pp, bool &inside) -> uint32_t {
+        const uint32_t xp = pp % L.wp, t = pp / L.wp;
+        const uint32_t yp = t % L.hp, img = t / L.hp;
+        const int32_t y = static_cast<int32_t>(yp) - static_cast<int32_t>(L.pad);
+        const int32_t x = static_cast<int32_t>(xp) - static_cast<int32_t>(L.pad);
+        inside = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 && x < static_cast<int32_t>(L.in_cols);
+        return inside ? (img * L.sN + static_cast<uint32_t>(y) * L.sY + static_cast<uint32_t>(x) * L.sX) * 4u : 0u;
+    };
+    {
+        const uint32_t p = tid % 64, c16 = tid / 64, pp = pp0 + p;
+        if (pp < npos && c16 < ngrp) {
+            bool inside = false;
+            const uint32_t a0 = at(pp, inside);
+            const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
+            const uint32_t step = L.sC * 4u;
+            const uint32_t c0 = cbase + 16 * c16;
+            // padding reads position (0, 0) channel 0, channels past c_in the
+            // last channel: masked below
+            const bool live = inside && c0 < L.c_in;
+            const uint32_t cb = live ? c0 : 0u, last = live ? L.c_in - 1 - c0 : 0u;
+            v4i q4[4];
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t q = static_cast<uint32_t>(4 * d + k);
+                    q4[d][k] = static_cast<int32_t>(load_word(src, a0 + (cb + (q < last ? q : last)) * step));
+                }
+#pragma unroll
+            for (int d = 0; d < 4; ++d) *reinterpret_cast<v4i *>(&T[p * 68 + 16 * c16 + 4 * d]) = q4[d];
+        }
+    }
+    __syncthreads();
+    const uint32_t p = tid / 4, c16 = tid % 4, pp = pp0 + p;
+    if (pp >= npos || c16 >= ngrp) return;  // no barrier follows
+    bool inside = false;
+    (void)at(pp, inside);
+    const uint32_t c0 = cbase + 16 * c16;
     uint32_t wd[16];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) wd[q] = load_word(src, a0 + (static_cast<uint32_t>(q) < last ? q : last) * step);
+    for (int d = 0; d < 4; ++d) {
+        const v4i v = *reinterpret_cast<const v4i *>(&T[p * 68 + 16 * c16 + 4 * d]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) wd[4 * d + k] = static_cast<uint32_t>(v[k]);
+    }
+    const uint32_t nlive = !inside || c0 >= L.c_in ? 0u : (L.c_in - c0 < 16 ? L.c_in - c0 : 16u);  // live channels
     uint8_t *dst = planes + static_cast<uint64_t>(M.lam_off + w * M.g) * L.plane_bytes + static_cast<uint64_t>(pp) * L.cp + c0;
     for (uint32_t jr = 0; jr < g; ++jr) {
         const uint32_t sh = M.b * jr;
         v4i v;
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            const uint32_t f0 = __builtin_amdgcn_ubfe(wd[4 * d], sh, M.b);
-            const uint32_t f1 = __builtin_amdgcn_ubfe(wd[4 * d + 1], sh, M.b);
-            const uint32_t f2 = __builtin_amdgcn_ubfe(wd[4 * d + 2], sh, M.b);
-            const uint32_t f3 = __builtin_amdgcn_ubfe(wd[4 * d + 3], sh, M.b);
-            v[d] = static_cast<int32_t>(live ? (f0 | (f1 << 8) | (f2 << 16) | (f3 << 24)) ^ flip : flip);
+            uint32_t f = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t q = static_cast<uint32_t>(4 * d + k);
+                f |= (q < nlive ? __builtin_amdgcn_ubfe(wd[q], sh, M.b) : 0u) << (8 * k);
+            }
+            v[d] = static_cast<int32_t>(f ^ flip);
         }
         *reinterpret_cast<v4i *>(dst + static_cast<uint64_t>(jr) * L.plane_bytes) = v;
     }
@@ -990,10 +1029,10 @@ int launch_linear(const LinPlan &L, const uint32_t *in, const uint8_t *prep, con
     if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return REDASH_E_HIP;
     if (L.lds_bytes > static_cast<uint32_t>(v)) return REDASH_E_HIP;
-    const uint64_t nthr = static_cast<uint64_t>(L.nimg) * L.hp * L.wp * (L.cp / 16);
-    if (nthr >= (1ull << 32)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL(k_linear_unpack, dim3(static_cast<uint32_t>((nthr + 255) / 256), L.npairs), dim3(256), 0, stream,
-                       L, in, work);
+    const uint64_t npos = static_cast<uint64_t>(L.nimg) * L.hp * L.wp;
+    if (npos >= (1ull << 32)) return REDASH_E_PARAM;
+    hipLaunchKernelGGL(k_linear_unpack, dim3(static_cast<uint32_t>((npos + 63) / 64), L.npairs, (L.cp + 63) / 64),
+                       dim3(256), 0, stream, L, in, work);
     if (lin_launched()) return REDASH_E_HIP;
     if (L.xt == 32) return launch_gemm_k<2, GARBLE>(L, work, prep, bias, offsets, out, stream);
     return launch_gemm_k<1, GARBLE>(L, work, prep, bias, offsets, out, stream);
