@@ -787,7 +787,7 @@ int launched() {
 }
 
 // Launches one of the evaluators for n gadgets.  Calls that one round of
-// two workgroups per CU holds when a gadget takes 4 (or 2) waves use
+// two workgroups per CU holds when a gadget takes 12, 4 (or 2) waves use
 // k_eval_split with that split; larger calls k_eval, one gadget per lane.
 template <uint32_t SPLIT>
 int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
@@ -795,8 +795,11 @@ int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval_split<kEvalBlock, SPLIT>), lds);
     if (rc) return rc;
     // block / SPLIT gadgets per workgroup, the block a multiple of 64 SPLIT
+    // (every group of SPLIT waves complete) and at most kEvalBlock
+    constexpr int most = kEvalBlock / static_cast<int>(SPLIT) / 64 * 64;
+    static_assert(most >= 64, "a workgroup holds at least one group of SPLIT waves");
     int per = 0;
-    if ((rc = block_for(P.n, kEvalBlock / static_cast<int>(SPLIT), &per))) return rc;
+    if ((rc = block_for(P.n, most, &per))) return rc;
     hipLaunchKernelGGL((k_eval_split<kEvalBlock, SPLIT>), dim3(grid_for(P.n, per)), dim3(per * static_cast<int>(SPLIT)),
                        lds, stream, P, in, tab, out, work);
     return launched();
@@ -809,6 +812,10 @@ int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t 
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         return REDASH_E_HIP;
     const uint64_t round = 2ull * static_cast<uint64_t>(cus) * kEvalBlock;  // threads of one round
+    // up to one round of two workgroups of 64 gadgets per CU: 12 waves per
+    // gadget (runs of gates sharing a digit have at most k - 1 gates, 11 on
+    // the 12-prime base: one gate per wave and run)
+    if (P.n <= 2ull * static_cast<uint64_t>(cus) * 64) return launch_split<12>(P, lds, in, tab, out, work, stream);
     if (P.n <= round / 4) return launch_split<4>(P, lds, in, tab, out, work, stream);
     if (P.n <= round / 2) return launch_split<2>(P, lds, in, tab, out, work, stream);
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds);
