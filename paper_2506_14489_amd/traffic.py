@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15211901.8,  # mean of four dispatches: 15,208,823 .. 15,213,204
-        "write_kib": 5049776.6,  # mean of four dispatches: 5,049,672 .. 5,049,889
-        "sources_sha256": "b8d3fc4d25c4989f9e3edfa15bf57ad02bc70956029c9292bb553be4bb6400e8",
+        "fetch_kib": 15212358.4,  # mean of four dispatches: 15,209,457 .. 15,213,731
+        "write_kib": 5049959.7,  # mean of four dispatches: 5,049,796 .. 5,050,142
+        "sources_sha256": "1385afff3865fa2995c8bee0f8a0f1380e7f52123a202bf0282f2268d9091193",
     },
 }
 
