@@ -309,6 +309,24 @@ def test_full_size_batched():
     _check_full(WL.BATCHED, 160)
 
 
+# The evaluator's launch thresholds on this GPU: calls of up to one round of
+# two workgroups per CU with 64, 192 or 384 gadgets per workgroup give each
+# group of 64 gadgets 12, 4 or 2 waves; larger calls take one gadget per lane.
+# Each threshold and one gadget past it (a last group of one live lane).
+LAUNCH_EDGES = [("split12-last", 64, 0), ("split4-first", 64, 1), ("split4-last", 192, 0),
+                ("split2-first", 192, 1), ("split2-last", 384, 0), ("one-per-lane-first", 384, 1)]
+
+
+@pytest.mark.parametrize("per,extra", [e[1:] for e in LAUNCH_EDGES], ids=[e[0] for e in LAUNCH_EDGES])
+def test_evaluator_launch_thresholds(per, extra):
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 2 * cus * per + extra
+    P = rns.cardinality(WL.PRIMES_12)
+    w = WL.Workload(f"edge-{n}", tuple(WL.PRIMES_12), (11,), n, 60 + per + extra, "uniform", -(P // 2),
+                    P - P // 2)
+    _check_full(w, 24)
+
+
 @pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
 def test_full_size_resnet18_layer(layer):
     _check_full(layer, 24)
