@@ -290,7 +290,7 @@ k_eval(const Plan P, const uint32_t *__restrict__ in,
 template <int BLOCK, uint32_t SPLIT>
 __global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))
 k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__restrict__ tab, uint32_t *out,
-             uint32_t *work) {
+             uint32_t *work, uint32_t first) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
@@ -302,8 +302,8 @@ k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__re
     const PermTE02 TT = perm_te02();
     const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
     const uint32_t part = wave % SPLIT, grp = wave / SPLIT;
-    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * (static_cast<uint32_t>(nthr) / SPLIT) + grp * 64u +
-                       static_cast<uint32_t>(tid) % 64u;
+    const uint64_t a = first + static_cast<uint64_t>(blockIdx.x) * (static_cast<uint32_t>(nthr) / SPLIT) +
+                       grp * 64u + static_cast<uint32_t>(tid) % 64u;
     const bool live = a < P.n;  // dead lanes still take every barrier
     const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(live ? a : 0) * 4u};
     const uint64_t tau0 = (P.a0 + a) * P.G;
@@ -786,12 +786,10 @@ int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
 
-// Launches one of the evaluators for n gadgets.  Calls that one round of
-// two workgroups per CU holds when a gadget takes 12, 4 (or 2) waves use
-// k_eval_split with that split; larger calls k_eval, one gadget per lane.
+// k_eval_split over gadgets first .. first + count - 1 (of the plan's n).
 template <uint32_t SPLIT>
 int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
-                 hipStream_t stream) {
+                 uint64_t first, uint64_t count, hipStream_t stream) {
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval_split<kEvalBlock, SPLIT>), lds);
     if (rc) return rc;
     // block / SPLIT gadgets per workgroup, the block a multiple of 64 SPLIT
@@ -799,31 +797,63 @@ int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t
     constexpr int most = kEvalBlock / static_cast<int>(SPLIT) / 64 * 64;
     static_assert(most >= 64, "a workgroup holds at least one group of SPLIT waves");
     int per = 0;
-    if ((rc = block_for(P.n, most, &per))) return rc;
-    hipLaunchKernelGGL((k_eval_split<kEvalBlock, SPLIT>), dim3(grid_for(P.n, per)), dim3(per * static_cast<int>(SPLIT)),
-                       lds, stream, P, in, tab, out, work);
+    if ((rc = block_for(count, most, &per))) return rc;
+    hipLaunchKernelGGL((k_eval_split<kEvalBlock, SPLIT>), dim3(grid_for(count, per)),
+                       dim3(per * static_cast<int>(SPLIT)), lds, stream, P, in, tab, out, work,
+                       static_cast<uint32_t>(first));
     return launched();
 }
 
+// The split evaluator for `count` gadgets that one round of two workgroups
+// per CU holds with 64, 192 or 384 gadgets per workgroup (12, 4 or 2 waves
+// per 64 gadgets); 0 when the count needs more than one such round.
+uint32_t split_for(uint64_t count, uint64_t cus) {
+    if (count <= 2 * cus * 64) return 12;
+    if (count <= 2 * cus * kEvalBlock / 4) return 4;
+    if (count <= 2 * cus * kEvalBlock / 2) return 2;
+    return 0;
+}
+
+int launch_split_any(uint32_t split, const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab,
+                     uint32_t *out, uint32_t *work, uint64_t first, uint64_t count, hipStream_t stream) {
+    switch (split) {
+        case 12: return launch_split<12>(P, lds, in, tab, out, work, first, count, stream);
+        case 4: return launch_split<4>(P, lds, in, tab, out, work, first, count, stream);
+        case 2: return launch_split<2>(P, lds, in, tab, out, work, first, count, stream);
+        default: return REDASH_E_PARAM;  // not reached
+    }
+}
+
+// Launches the evaluators for n gadgets.  A call that one round of two
+// workgroups per CU holds when a gadget takes 12, 4 or 2 waves runs on
+// k_eval_split with that split (runs of gates sharing a digit have at most
+// k - 1 gates, 11 on the 12-prime base: with 12 waves one gate per wave and
+// run).  A larger call runs on k_eval, one gadget per lane: whole rounds of
+// two full workgroups per CU, and a rest of at most a quarter round goes to
+// the split evaluator after them instead of running as a last round with few
+// waves per SIMD, whose gadgets would take the latency of their gate chain.
 int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
                 hipStream_t stream) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         return REDASH_E_HIP;
-    const uint64_t round = 2ull * static_cast<uint64_t>(cus) * kEvalBlock;  // threads of one round
-    // up to one round of two workgroups of 64 gadgets per CU: 12 waves per
-    // gadget (runs of gates sharing a digit have at most k - 1 gates, 11 on
-    // the 12-prime base: one gate per wave and run)
-    if (P.n <= 2ull * static_cast<uint64_t>(cus) * 64) return launch_split<12>(P, lds, in, tab, out, work, stream);
-    if (P.n <= round / 4) return launch_split<4>(P, lds, in, tab, out, work, stream);
-    if (P.n <= round / 2) return launch_split<2>(P, lds, in, tab, out, work, stream);
+    const uint64_t ncu = static_cast<uint64_t>(cus);
+    if (const uint32_t split = split_for(P.n, ncu))
+        return launch_split_any(split, P, lds, in, tab, out, work, 0, P.n, stream);
+    const uint64_t round = 2 * ncu * kEvalBlock;  // gadgets of one round, one per lane
+    uint64_t bulk = P.n;
+    const uint64_t rest = P.n % round;
+    if (P.n > round && rest > 0 && rest <= round / 4) bulk = P.n - rest;
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds);
     if (rc) return rc;
     int block = 0;
-    if ((rc = block_for(P.n, kEvalBlock, &block))) return rc;
-    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(P.n, block)), dim3(block), lds, stream, P, in, tab, out, work);
-    return launched();
+    if ((rc = block_for(bulk, kEvalBlock, &block))) return rc;
+    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(bulk, block)), dim3(block), lds, stream, P, in, tab, out,
+                       work);
+    if ((rc = launched())) return rc;
+    if (bulk == P.n) return REDASH_OK;
+    return launch_split_any(split_for(P.n - bulk, ncu), P, lds, in, tab, out, work, bulk, P.n - bulk, stream);
 }
 
 
