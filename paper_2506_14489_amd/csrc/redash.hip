@@ -829,9 +829,10 @@ int launch_split_any(uint32_t split, const Plan &P, uint32_t lds, const uint32_t
 // k_eval_split with that split (runs of gates sharing a digit have at most
 // k - 1 gates, 11 on the 12-prime base: with 12 waves one gate per wave and
 // run).  A larger call runs on k_eval, one gadget per lane: whole rounds of
-// two full workgroups per CU, and a rest of at most a quarter round goes to
-// the split evaluator after them instead of running as a last round with few
-// waves per SIMD, whose gadgets would take the latency of their gate chain.
+// two full workgroups per CU, and a rest that the 12-wave split holds in one
+// round goes to it after them instead of running as a last round with few
+// waves per SIMD, whose gadgets would take the latency of their gate chain
+// (a larger rest costs k_eval no more than it would cost the split).
 int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
                 hipStream_t stream) {
     int dev = 0, cus = 0;
@@ -844,7 +845,7 @@ int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t 
     const uint64_t round = 2 * ncu * kEvalBlock;  // gadgets of one round, one per lane
     uint64_t bulk = P.n;
     const uint64_t rest = P.n % round;
-    if (P.n > round && rest > 0 && rest <= round / 4) bulk = P.n - rest;
+    if (P.n > round && rest > 0 && rest <= 2 * ncu * 64) bulk = P.n - rest;
     int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds);
     if (rc) return rc;
     int block = 0;

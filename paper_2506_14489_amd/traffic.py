@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15212358.4,  # mean of four dispatches: 15,209,457 .. 15,213,731
-        "write_kib": 5049959.7,  # mean of four dispatches: 5,049,796 .. 5,050,142
-        "sources_sha256": "1385afff3865fa2995c8bee0f8a0f1380e7f52123a202bf0282f2268d9091193",
+        "fetch_kib": 15212197.9,  # mean of four dispatches: 15,209,726 .. 15,213,305
+        "write_kib": 5050334.4,  # mean of four dispatches: 5,050,211 .. 5,050,423
+        "sources_sha256": "2262ae0cabbdf144c49147aed6fd1cc5f42934e4f913f67e35bc443ab485c3bc",
     },
 }
 

@@ -312,13 +312,13 @@ def test_full_size_batched():
 # The evaluator's launch thresholds on this GPU.  Calls of up to one round of
 # two workgroups per CU with 64, 192 or 384 gadgets per workgroup give each
 # group of 64 gadgets 12, 4 or 2 waves; larger calls take one gadget per lane
-# on whole rounds of 768-gadget workgroups, and a rest of at most a quarter
-# round (192 gadgets per workgroup) goes to the split evaluator, starting at
-# the first gadget after the rounds.  Each threshold and one gadget past it.
+# on whole rounds of 768-gadget workgroups, and a rest that the 12-wave split
+# holds in one round (64 gadgets per workgroup) goes to it, starting at the
+# first gadget after the rounds.  Each threshold and one gadget past it.
 # (name, whole rounds, then gadgets per workgroup of the two per CU, extra)
 LAUNCH_EDGES = [("split12-last", 0, 64, 0), ("split4-first", 0, 64, 1), ("split4-last", 0, 192, 0),
                 ("split2-first", 0, 192, 1), ("split2-last", 0, 384, 0), ("one-per-lane-first", 0, 384, 1),
-                ("round-rest-one", 1, 0, 1), ("round-rest-quarter", 1, 192, 0), ("round-rest-past-quarter", 1, 192, 1)]
+                ("round-rest-one", 1, 0, 1), ("round-rest-split12-last", 1, 64, 0), ("round-rest-past-split12", 1, 64, 1)]
 
 
 @pytest.mark.parametrize("rounds,per,extra", [e[1:] for e in LAUNCH_EDGES], ids=[e[0] for e in LAUNCH_EDGES])
