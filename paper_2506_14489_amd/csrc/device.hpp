@@ -402,7 +402,6 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_
     const uint32_t nhi = nres - nlo;
     // low part: positions nres-1 down to nhi (least significant digit first)
     uint32_t x = lo;
-#pragma unroll 2
     for (uint32_t j = nres - 1; j > nhi; --j) {
         const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
         res |= residue(opaque(x - mul24(q, m)), j);
@@ -411,7 +410,6 @@ __device__ __forceinline__ uint32_t fast_word(uint32_t D, uint32_t nres, uint32_
     if (nlo) res |= residue(x, nhi);
     // high part: positions nhi-1 down to 0
     x = hi;
-#pragma unroll 2
     for (uint32_t j = nhi - 1; j > 0; --j) {
         const uint32_t q = mul24(x, mc.sd_M) >> mc.sd_s;
         res |= residue(opaque(x - mul24(q, m)), j);

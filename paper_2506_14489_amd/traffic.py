@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15212197.9,  # mean of four dispatches: 15,209,726 .. 15,213,305
-        "write_kib": 5050334.4,  # mean of four dispatches: 5,050,211 .. 5,050,423
-        "sources_sha256": "2262ae0cabbdf144c49147aed6fd1cc5f42934e4f913f67e35bc443ab485c3bc",
+        "fetch_kib": 15211511.8,  # mean of four dispatches: 15,208,608 .. 15,212,628
+        "write_kib": 5049873.1,  # mean of four dispatches: 5,049,740 .. 5,049,962
+        "sources_sha256": "439a7afcc1a8863f2006fbb63c9176793600b17a644fcddf8cf2e10afb67447a",
     },
 }
 
