@@ -355,13 +355,25 @@ __device__ __forceinline__ v4i load16(const uint8_t *base, uint32_t off) {
 __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const uint32_t *__restrict__ in,
                                                        uint8_t *__restrict__ planes) {
     __shared__ __align__(16) uint32_t T[64 * 68];
-    const uint32_t pair = blockIdx.y;
+    // workgroups go round-robin to the XCDs by linear index: remap so that
+    // each XCD takes runs of RUN neighbouring position blocks, the 8 XCDs
+    // working on 8 neighbouring runs, so that most lines that neighbouring
+    // blocks share (input rows are not line-aligned) are fetched into one L2
+    // (one contiguous range per XCD fetches the fewest lines but streams
+    // from HBM more slowly: 0.73 ms against 0.51)
+    const uint32_t nx = gridDim.x, ny = gridDim.y, nt = nx * ny * gridDim.z;
+    const uint32_t lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    constexpr uint32_t RUN = 16;
+    const uint32_t full = nt / (kXcds * RUN) * (kXcds * RUN);
+    const uint32_t lg = lin < full ? lin / (kXcds * RUN) * (kXcds * RUN) + (lin % kXcds) * RUN + (lin / kXcds) % RUN : lin;
+    const uint32_t bx = lg % nx, by = (lg / nx) % ny, bz = lg / (nx * ny);
+    const uint32_t pair = by;
     const uint32_t i = L.pair_mod[pair], w = L.pair_word[pair];
     const LinMod M = L.mod[i];
     const uint32_t g = (w + 1 == M.W) ? M.glast : M.g;
     const uint32_t tid = threadIdx.x;
     const uint32_t npos = L.nimg * L.hp * L.wp;
-    const uint32_t pp0 = blockIdx.x * 64, cbase = 64 * blockIdx.z;
+    const uint32_t pp0 = bx * 64, cbase = 64 * bz;
     const uint32_t ngrp = (L.cp - cbase) / 16 < 4 ? (L.cp - cbase) / 16 : 4u;  // 16-channel groups of this chunk
     const uint32_t flip = M.m > 128 ? 0x80808080u : 0u;
     // position of (padded) index pp: inside the input, and the word offset there
