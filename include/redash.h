@@ -52,7 +52,7 @@
  *    Matyas-Meyer-Oseas form with the key 00 01 .. 0f, applied to the linear
  *    orthomorphism sigma(x) = ((x_hi ^ x_lo) << 64) | x_hi of the XOR-fold
  *    of the input label's PK32 words, tweaked with
- *    T_j = gadget_id * 2^96 + 4 tau + j, tau = a * gates + g, and
+ *    T_j = gadget_id * 2^96 + ((4 tau + j) mod 2^64), tau = a * gates + g, and
  *    gadget_id = seed mod 2^32; two blocks (one when m = 2) give a 256-bit
  *    (128-bit) fraction whose first lambda_m base-m digits are the pad.
  */

@@ -12,8 +12,10 @@ touch it and fails loudly when its HIP library is missing.
                    Y = sum w X for the evaluator, Z = sum w Z - b R for the
                    garbler (Sec. 2.3 free operations)
 
-Parity unpinned by the paper: the exact label bits (hash construction, label
-length, PRG, tweaks, packing).  Those are pinned by FIPS-197 (AES), by the
-label invariants and decode results the tests check, and by the independent
-HIP implementation.
+The paper fixes no hash construction, label length, PRG, tweaks or packing;
+those follow the construction stated in ``gc_oracle.c``.  They are pinned by
+FIPS-197 (AES), by a step-by-step restatement on Python integers with
+libcrypto's AES (fold, sigma, tweak words, feed-forward, digits, PRG
+counters) and known-answer files, by the label invariants and decode results
+the tests check, and by the independent HIP implementation.
 """

@@ -26,10 +26,13 @@
  * The paper does not fix the label hash, the label length, the PRG, the
  * tweaks, the table layout or any bit convention.  The concrete choices
  * ("R-spec v1") are written out in the design notes and restated at each
- * function below.  Parity of the exact label BITS is therefore unpinned by
- * the paper: it is pinned by the invariants the tests check (every wire label
- * equals its zero-label plus value times the offset; decode equals
- * floor(x/s)), by FIPS-197 for AES, and by two independent implementations.
+ * function below.  The paper does not pin the exact label BITS; the tests
+ * pin them by the invariants (every wire label equals its zero-label plus
+ * value times the offset; decode equals floor(x/s)), by FIPS-197 for AES,
+ * and step by step against a second statement of the hash and the PRG on
+ * Python integers and libcrypto's AES (fold lanes, sigma as a linear
+ * orthomorphism, tweak words, feed-forward, digits, PRG counters), plus
+ * known-answer files derived from it.
  *
  * Plain C99 + unsigned __int128 (gcc).  Single-threaded.  No tuning.
  */
@@ -244,25 +247,27 @@ static const uint8_t *hash_round_keys(void) {
     return HASH_RK;
 }
 
-/* H_m(A, tau): A is a label over Z_q (lambda_q residues); the result is a
- * label over Z_m (lambda_m residues).
+/* The 128 n-bit value behind H_m(A, tau) (n = 1 if m == 2 else 2), with the
+ * intermediate values the tests pin one by one:
  *   x = fold(PK32(A)): word w is XORed into 32-bit lane (w mod 4)
- *   u = sigma(x) = ((x_hi ^ x_lo) << 64) | x_hi   (linear orthomorphism)
- *   n = 1 if m == 2 else 2
- *   T_j = gadget_id * 2^96 + tau * 4 + j
- *   U_j = AES_K(u ^ T_j) ^ u ^ T_j
- *   V = sum_j U_j 2^(128 j); the result is the first lambda_m base-m digits
- *   of the fraction V / 2^(128 n). */
-static void hash_label(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadget_id, uint64_t tau,
-                       uint32_t *out) {
+ *   u = sigma(x) = ((x_hi ^ x_lo) << 64) | x_hi   (linear orthomorphism;
+ *       x_lo = lanes 0-1, x_hi = lanes 2-3)
+ *   T_j = gadget_id * 2^96 + ((tau * 4 + j) mod 2^64)   (j < n; bits 64-95 zero)
+ *   U_j = AES_K(u ^ T_j) ^ u ^ T_j                (Matyas-Meyer-Oseas)
+ *   V = sum_j U_j 2^(128 j), returned as 4 n little-endian limbs. */
+static void hash_value(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadget_id, uint64_t tau,
+                       uint32_t x[4], uint32_t u[4], uint32_t V[8]) {
     const uint8_t *rk = hash_round_keys();
     uint32_t words[ORC_MAXLAMBDA];
     pk32_pack(q, A, words);
-    uint32_t x[4] = {0, 0, 0, 0};
+    for (int l = 0; l < 4; ++l) x[l] = 0;
     for (uint32_t w = 0; w < words_of(q); ++w) x[w % 4] ^= words[w];
-    uint32_t u[4] = {x[2], x[3], x[2] ^ x[0], x[3] ^ x[1]};
+    u[0] = x[2];
+    u[1] = x[3];
+    u[2] = x[2] ^ x[0];
+    u[3] = x[3] ^ x[1];
     int n = (m == 2) ? 1 : 2;
-    uint32_t V[8];
+    for (int l = 0; l < 8; ++l) V[l] = 0;
     for (int j = 0; j < n; ++j) {
         uint64_t tw = tau * 4u + (uint64_t)j;
         uint32_t T[4] = {(uint32_t)tw, (uint32_t)(tw >> 32), 0u, gadget_id};
@@ -274,6 +279,16 @@ static void hash_label(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadge
         bytes_to_lanes(ob, ct);
         for (int l = 0; l < 4; ++l) V[4 * j + l] = ct[l] ^ u[l] ^ T[l];
     }
+}
+
+/* H_m(A, tau): A is a label over Z_q (lambda_q residues); the result is a
+ * label over Z_m (lambda_m residues): the first lambda_m base-m digits of the
+ * fraction V / 2^(128 n), V from hash_value(). */
+static void hash_label(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadget_id, uint64_t tau,
+                       uint32_t *out) {
+    uint32_t x[4], u[4], V[8];
+    hash_value(q, m, A, gadget_id, tau, x, u, V);
+    int n = (m == 2) ? 1 : 2;
     uint32_t lam = lambda_of(m);
     uint32_t radix[ORC_MAXLAMBDA];
     for (uint32_t i = 0; i < lam; ++i) radix[i] = m;
@@ -282,12 +297,9 @@ static void hash_label(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadge
 
 /* Garbler PRG: K_seed = seed as 16 little-endian bytes;
  * rho(stream, idx) = AES_{K_seed}(C_0) + 2^128 AES_{K_seed}(C_1),
- * C_h = stream * 2^120 + idx * 2 + h.  A label is read off rho as fraction
- * digits; the first radix is offset_first_radix(m) when first_minus_one is
- * set (offsets). */
-static void prg_label(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx, uint32_t m,
-                      int first_minus_one, uint32_t *out) {
-    uint32_t V[8];
+ * C_h = stream * 2^120 + ((idx * 2 + h) mod 2^64), returned as 8
+ * little-endian limbs. */
+static void prg_value(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx, uint32_t V[8]) {
     for (int h = 0; h < 2; ++h) {
         uint64_t lo = idx * 2u + (uint64_t)h;
         uint32_t C[4] = {(uint32_t)lo, (uint32_t)(lo >> 32), 0u, stream << 24};
@@ -298,6 +310,14 @@ static void prg_label(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx,
         bytes_to_lanes(ob, ct);
         for (int l = 0; l < 4; ++l) V[4 * h + l] = ct[l];
     }
+}
+
+/* A label read off rho(stream, idx) as fraction digits; the first radix is
+ * offset_first_radix(m) when first_minus_one is set (offsets). */
+static void prg_label(const uint8_t rk_seed[176], uint32_t stream, uint64_t idx, uint32_t m,
+                      int first_minus_one, uint32_t *out) {
+    uint32_t V[8];
+    prg_value(rk_seed, stream, idx, V);
     uint32_t lam = lambda_of(m);
     uint32_t radix[ORC_MAXLAMBDA];
     for (uint32_t i = 0; i < lam; ++i) radix[i] = m;
@@ -508,6 +528,20 @@ void orc_pk32_unpack(uint32_t m, const uint32_t *words, uint32_t *res) { pk32_un
 /* Hash of one label given as residues; out gets lambda_m residues. */
 void orc_hash(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadget_id, uint64_t tau, uint32_t *out) {
     hash_label(q, m, A, gadget_id, tau, out);
+}
+
+/* The intermediate values of the hash (fold x, sigma u, and the 128 n-bit
+ * value V before its digits are taken), for the tests that pin each step. */
+void orc_hash_parts(uint32_t q, uint32_t m, const uint32_t *A, uint32_t gadget_id, uint64_t tau, uint32_t *x,
+                    uint32_t *u, uint32_t *V) {
+    hash_value(q, m, A, gadget_id, tau, x, u, V);
+}
+
+/* rho(stream, idx) under the seed's key, as 8 little-endian limbs. */
+void orc_prg_value(uint64_t seed, uint32_t stream, uint64_t idx, uint32_t *V) {
+    uint8_t rk[176];
+    seed_round_keys(seed, rk);
+    prg_value(rk, stream, idx, V);
 }
 
 void orc_prg_label(uint64_t seed, uint32_t stream, uint64_t idx, uint32_t m, int first_minus_one,

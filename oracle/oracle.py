@@ -68,6 +68,9 @@ def lib():
         _lib.orc_words.restype = ctypes.c_uint32
         _lib.orc_hash.argtypes = [ctypes.c_uint32, ctypes.c_uint32, u32p, ctypes.c_uint32,
                                   ctypes.c_uint64, u32p]
+        _lib.orc_hash_parts.argtypes = [ctypes.c_uint32, ctypes.c_uint32, u32p, ctypes.c_uint32,
+                                        ctypes.c_uint64, u32p, u32p, u32p]
+        _lib.orc_prg_value.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint64, u32p]
         _lib.orc_prg_label.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint64,
                                        ctypes.c_uint32, ctypes.c_int, u32p]
         _lib.orc_frac_digits.argtypes = [u32p, ctypes.c_int, u32p, ctypes.c_int, u32p]
@@ -180,6 +183,24 @@ def hash_label(q: int, m: int, A, gadget_id: int, tau: int) -> np.ndarray:
     out = np.zeros(MAXLAMBDA, np.uint32)
     lib().orc_hash(q, m, _p(a), gadget_id, tau, _p(out))
     return out[: lam(m)].copy()
+
+
+def hash_parts(q: int, m: int, A, gadget_id: int, tau: int):
+    """(x, u, V) of the hash: the fold of the packed label (4 lanes), sigma of
+    it (4 lanes) and the hash value before digit extraction (8 limbs; the top
+    4 are 0 when m = 2)."""
+    a = np.zeros(MAXLAMBDA, np.uint32)
+    a[: len(A)] = A
+    x, u, V = np.zeros(4, np.uint32), np.zeros(4, np.uint32), np.zeros(8, np.uint32)
+    lib().orc_hash_parts(q, m, _p(a), gadget_id, tau, _p(x), _p(u), _p(V))
+    return x, u, V
+
+
+def prg_value(seed: int, stream: int, idx: int) -> np.ndarray:
+    """rho(stream, idx) of the garbler PRG as 8 little-endian 32-bit limbs."""
+    V = np.zeros(8, np.uint32)
+    lib().orc_prg_value(seed, stream, idx, _p(V))
+    return V
 
 
 def prg_label(seed: int, stream: int, idx: int, m: int, first_minus_one: bool) -> np.ndarray:
