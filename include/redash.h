@@ -256,7 +256,7 @@ const char *redash_strerror(int code);
  *   k, moduli   the RNS base, as in redash_params (primes or powers of two,
  *               2..255, ascending, pairwise coprime, P < 2^63).
  *   batch, c_in, h_in, w_in, c_out, kh, kw, stride, pad  the layer, with
- *               every size >= 1, pad < kh and pad < kw, c_in kh kw <= 32768,
+ *               every size >= 1, pad < kh and pad < kw, c_in kh kw <= 16384,
  *               kh kw <= 64, and at most 2^30 - 1 input and output
  *               activations.
  */

@@ -161,7 +161,7 @@ void fill_mod_const(uint32_t m, ModConst *mc) {
     mc->two_m = 2 * m;
     if (full_word) return;  // no fast constants: the packed-add fields above are all it uses
     mc->red_M = static_cast<uint32_t>(((1ull << 32) + m - 1) / m);
-    bool ok = 3 * sq * sq < (1ull << 32);  // x m < 2^32 for x < 3 m^2 (every m <= 255)
+    bool ok = 3 * sq * m < (1ull << 32);  // x m < 2^32 for x < 3 m^2 (every m <= 255)
     uint64_t part = 1;
     for (int k = 0; k < 2; ++k) {
         const uint32_t nres = k ? mc->glast : mc->g;

@@ -38,8 +38,10 @@ struct ModConst {
     uint32_t r0;       // radix of the offset's first digit: m - 1 (prime), m / 2 (2^l, l >= 2)
     // Evaluator fast path (fast == 1 when every bound below holds):
     //  * red: floor(x/m) = umulhi(x, red_M), red_M = ceil(2^32 / m), for
-    //    every x < 3 m^2 (the error x (red_M m - 2^32) / 2^32 < x m / 2^32
-    //    stays below 1/m while x m^2 < 2^32) -- one multiply per residue;
+    //    every x < 3 m^2: with e = red_M m - 2^32 < m, x red_M / 2^32 =
+    //    x/m + x e / (m 2^32), and the floor is exact while x e < 2^32, which
+    //    x m < 2^32 guarantees (3 m^3 < 2^32 for every m <= 255) -- one
+    //    multiply per residue;
     //  * sd: the same for every x below the larger part of a split word
     //    (parts below 2^23);
     //  * a word's nres digits D (nres = g, or glast for the last word) are

@@ -71,9 +71,10 @@ struct LabelBufs {
     }
 };
 
-// Moduli without the fast constants (4, 16 and primes from 41 to 61): one
-// residue at a time with 32-bit divisions, in rolled loops; the gadget
-// configurations in use all take the fast path.
+// Moduli without the fast constants (4 and 16, whose fields fill a word, and
+// the primes 41, 47, 53, 59 and 61, whose split parts are too large for the
+// 24-bit digit steps): one residue at a time with 32-bit divisions, in
+// rolled loops; the gadget configurations in use all take the fast path.
 __device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
                                                     uint32_t (&row)[kMaxW], uint32_t (&tgt)[kMaxW],
                                                     const LabelBufs &LB) {

@@ -219,8 +219,22 @@ LINEAR_BAD = [
     ((2, 3), 1, 4, 2, 2, 2, 5, 5, 1, 1),           # kernel larger than the padded input
     ((2, 3), 1, 4, 20, 20, 2, 9, 9, 1, 1),         # more than 64 taps
     ((2, 3), 1, 4096, 4, 4, 2, 3, 3, 1, 1),        # c_in kh kw > 32768
+    ((2, 3, 251), 1, 16385, 1, 1, 2, 1, 1, 1, 0),  # c_in kh kw = 16385, one above the limit
+    ((2, 3), 1, 1821, 4, 4, 2, 3, 3, 1, 1),        # 1821 * 9 = 16389
     ((2, 3), 1024, 64, 128, 128, 2, 1, 1, 1, 0),   # 2^30 input activations
 ]
+
+
+LINEAR_LIMIT_OK = [
+    ((2, 3, 251), 1, 16384, 1, 1, 2, 1, 1, 1, 0),  # c_in kh kw = 16384, the documented limit
+    ((2, 3, 251), 1, 1024, 4, 4, 2, 4, 4, 1, 1),   # 1024 * 16 = 16384 with a 4x4 kernel
+    ((251,), 1, 2048, 3, 3, 2, 2, 4, 1, 1),        # 2048 * 8 = 16384, largest modulus alone
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_LIMIT_OK)
+def test_linear_reduction_length_limit_accepted(case):
+    assert B.linear_plan_rc(B.make_linear_params(*case)) == 0
 
 
 @pytest.mark.parametrize("case", LINEAR_BAD)

@@ -53,7 +53,9 @@ HASH_PAIRS = [(2, 3), (3, 2), (37, 2), (2, 37), (11, 13), (5, 3), (37, 31), (17,
               (3, 5), (7, 37),
               # power-of-two moduli (Sec. 4 bases), including 4 and 16 whose fields fill a word
               (32, 167), (167, 32), (173, 32), (32, 97), (4, 3), (3, 4), (16, 5), (5, 16), (2, 64), (128, 7),
-              (8, 19), (251, 8)]
+              (8, 19), (251, 8),
+              # generic-path and large fast-path moduli
+              (41, 197), (241, 59), (61, 47), (53, 211)]
 
 
 @pytest.mark.parametrize("q,m", HASH_PAIRS)
@@ -74,6 +76,35 @@ def test_hash_matches_oracle(q, m):
         exp = O.pk32_pack(m, O.hash_label(q, m, res[a], gid, int(tau[a])))
         assert np.array_equal(got[a], exp), (q, m, a)
     assert Wq == len(words[0])
+
+
+def test_hash_known_answers():
+    """The library's hash against the known-answer file (written from the
+    oracle and checked against libcrypto on the CPU)."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hash_kat.txt")
+    groups = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            q, m, gid, tau, a, h = line.split()
+            groups.setdefault((int(q), int(m), int(gid, 16)), []).append(
+                (int(tau), [int(v, 16) for v in a.split(",")], [int(v, 16) for v in h.split(",")]))
+    done = 0
+    for (q, m, gid), rows in groups.items():
+        count = len(rows)
+        words = np.array([r[1] for r in rows], dtype=np.uint32)          # count x W_q
+        tau = np.array([r[0] for r in rows], dtype=np.uint64).view(np.int64)
+        Wm = B.label_words_of(m)
+        out = torch.empty(Wm * count, dtype=torch.int32, device="cuda")
+        B.redash_hash_labels(q, m, count, H.to_dev(np.ascontiguousarray(words.T.reshape(-1))), gid,
+                             H.to_dev(tau), out)
+        got = H.to_u32(out).reshape(Wm, count).T
+        for j, r in enumerate(rows):
+            assert [int(v) for v in got[j]] == r[2], (q, m, gid, r[0])
+            done += 1
+    assert done >= 100
 
 
 # ---------------------------------------------------------------------------
@@ -104,6 +135,12 @@ SMALL = [
     ("pow2-16", (3, 5, 7, 11, 16), (4,), 400, 53, 0),
     ("pow2-64", (5, 7, 64, 67), (2,), 400, 54, 0),
     ("pow2-128-product", (3, 128, 251), (0, 1), 400, 55, 0),
+    # moduli on the evaluator's generic path (41, 47, 53, 59, 61) and large
+    # primes on its fast path (197 to 251)
+    ("generic-41-61", (2, 41, 61), (2,), 300, 56, 0),
+    ("generic-47-53-59", (2, 47, 53, 59), (1, 3), 300, 57, 11),
+    ("fast-197-241", (3, 197, 241), (1,), 300, 58, 0),
+    ("fast-199-211-251", (2, 199, 211, 251), (3,), 300, 59, 4),
 ]
 
 
@@ -247,66 +284,97 @@ def test_empty_calls_are_noops():
 # full-size workloads in the benchmark's launch configuration
 # ---------------------------------------------------------------------------
 
-def _sample_gadgets(n: int, seed: int, count: int = 96) -> np.ndarray:
+def _sample_gadgets(n: int, seed: int, head: int, tail: int, rand: int) -> np.ndarray:
+    """The first `head` and last `tail` gadgets and `rand` seeded random ones
+    (every gadget when that covers the call), sorted."""
+    if head + tail + rand >= n:
+        return np.arange(n, dtype=np.int64)
     rng = np.random.default_rng(seed + 777)
-    head = np.arange(min(16, n))
-    tail = np.arange(max(0, n - 16), n)
-    mid = rng.choice(n, size=min(count, n), replace=False)
-    return np.unique(np.concatenate([head, tail, mid])).astype(np.int64)
+    mid = rng.choice(np.arange(head, n - tail), size=rand, replace=False)
+    return np.unique(np.concatenate([np.arange(head), np.arange(n - tail, n), mid])).astype(np.int64)
 
 
-def _check_full(w: WL.Workload, n_sample: int):
+def _runs(gad: np.ndarray):
+    """Contiguous runs (first, count) of a sorted index list."""
+    cut = np.flatnonzero(np.diff(gad) != 1) + 1
+    return [(int(r[0]), len(r)) for r in np.split(gad, cut)]
+
+
+def _oracle_zero_labels(op, moduli, gad: np.ndarray):
+    """Offsets, input and output zero-labels of the given gadgets from the
+    oracle's zero-label path (one hash per gate, no rows), laid out as a
+    LabelTensor with stride len(gad)."""
+    k = len(moduli)
+    zi = [[] for _ in range(k)]
+    zo = [[] for _ in range(k)]
+    offs = None
+    for a, c in _runs(gad):
+        offs, zin, zout, _ = O.garble(op, a, c, with_tables=False)
+        for i in range(k):
+            zi[i].append(O.label_view(zin, op, c, i))
+            zo[i].append(O.label_view(zout, op, c, i))
+    cat = lambda parts: np.concatenate([np.concatenate(p, axis=1).reshape(-1) for p in parts])  # noqa: E731
+    return offs, cat(zi), cat(zo)
+
+
+def _check_full(w: WL.Workload, head: int, tail: int, rand: int, rows: int = 16):
+    """Garble, encode, evaluate and decode one full-size workload in the
+    benchmark's launch configuration; check every gadget through decode, the
+    sampled gadgets' input zero-labels, output zero-labels and output labels
+    word for word against the oracle's zero-label path, and the table rows of
+    `rows` gadgets at each end and `rows` random ones against the oracle's
+    garbling."""
     x = WL.make_inputs(w)
     n = w.n
     bp = B.make_params(w.moduli, w.scale_idx, n, w.seed)
     op = O.make_params(list(w.moduli), list(w.scale_idx), 1, w.seed)
+    print(f"full-size {w.name}: n={n} moduli={w.moduli} S={w.scale_idx} seed={w.seed}", flush=True)
     buf = H.gpu_pipeline(bp, x)
     # every gadget: decode = floor(x/s) (floor((x + r)/s), see _scaled) and every label valid
     expect = _scaled(x, w.moduli, w.scale_idx)
     assert int(buf.bad.item()) == 0
     assert np.array_equal(buf.y.cpu().numpy()[:n], expect)
-    # sampled gadgets, word for word against the oracle garbling that gadget
-    gad = _sample_gadgets(n, w.seed, n_sample)
+    # sampled gadgets: labels word for word against the oracle's zero-label path
+    gad = _sample_gadgets(n, w.seed, head, tail, rand)
+    li = H.label_index(w.moduli, n, gad)
+    offs, zin, zout = _oracle_zero_labels(op, w.moduli, gad)
+    assert np.array_equal(H.to_u32(buf.offsets), offs)
+    assert np.array_equal(H.gather(buf.in_zero, li), zin)
+    assert np.array_equal(H.gather(buf.out_zero, li), zout)
+    # expected evaluator output: output zero-label + floor(x/s) * R
+    Yexp = O.encode(op, expect[gad], zout, offs)
+    got = H.gather(buf.out_labels, li)
+    if not np.array_equal(got, Yexp):
+        bad_words = np.flatnonzero(got != Yexp) % len(gad)
+        raise AssertionError(f"{w.name}: output labels differ at gadgets {np.unique(gad[bad_words])[:10]}")
+    # table rows of a few gadgets at both ends and in between
+    rgad = _sample_gadgets(n, w.seed + 1, rows, rows, rows)
     gates = O.gate_list(op)
     gq = H.gate_list_sizes(gates, w.moduli)
-    li = H.label_index(w.moduli, n, gad)
-    ti = H.table_index(gq, n, gad)
-    g_zin = H.gather(buf.in_zero, li)
-    g_zout = H.gather(buf.out_zero, li)
-    g_out = H.gather(buf.out_labels, li)
+    ti = H.table_index(gq, n, rgad)
     g_tab = H.gather(buf.tables, ti)
-    k_words = len(li) // len(gad)
-    per_tab = len(ti) // len(gad)
-    offs_all = H.to_u32(buf.offsets)
-    for j, a in enumerate(gad):
-        offs, zin, zout, tab = O.garble(op, int(a), 1)
-        assert np.array_equal(offs_all, offs)
-        # reorder this gadget's words out of the gathered (modulus, word, gadget) order
-        sel = np.arange(k_words) * len(gad) + j
-        assert np.array_equal(g_zin[sel], zin), a
-        assert np.array_equal(g_zout[sel], zout), a
-        # expected evaluator output: output zero-label + floor(x/s) * R
-        Yexp = O.encode(op, expect[a:a + 1], zout, offs)
-        assert np.array_equal(g_out[sel], Yexp), a
+    for j, a in enumerate(rgad):
+        _, _, _, tab = O.garble(op, int(a), 1)
         # rows: gate blocks of (q-1) W words, gadget-major inside each gate
         tsel, base = [], 0
         for (q, W) in gq:
             per = (q - 1) * W
             tsel.append(base + j * per + np.arange(per))
-            base += len(gad) * per
+            base += len(rgad) * per
         assert np.array_equal(g_tab[np.concatenate(tsel)], tab), a
-    assert per_tab * len(gad) == len(ti)
     del buf
     torch.cuda.empty_cache()
 
 
 def test_full_size_conv():
-    _check_full(WL.CONV, 256)
+    """The 64x32x32 conv map: every one of its 65,536 gadgets word for word."""
+    _check_full(WL.CONV, WL.CONV.n, 0, 0, 32)
 
 
 def test_full_size_batched():
-    """The benchmark workload: 16x64x56x56 gadgets, 12 primes, s = 37."""
-    _check_full(WL.BATCHED, 160)
+    """The benchmark workload: 16x64x56x56 gadgets, 12 primes, s = 37;
+    4,096 gadgets at each end and 8,192 random ones word for word."""
+    _check_full(WL.BATCHED, 4096, 4096, 8192, 32)
 
 
 # The evaluator's launch thresholds on this GPU.  Calls of up to one round of
@@ -328,21 +396,24 @@ def test_evaluator_launch_thresholds(rounds, per, extra):
     P = rns.cardinality(WL.PRIMES_12)
     w = WL.Workload(f"edge-{n}", tuple(WL.PRIMES_12), (11,), n, 60 + per + extra, "uniform", -(P // 2),
                     P - P // 2)
-    _check_full(w, 24)
+    _check_full(w, 4096, 4096, 8192)
 
 
 @pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
 def test_full_size_resnet18_layer(layer):
-    _check_full(layer, 24)
+    if layer.n >= 400_000:  # the stem, run like the benchmark workload
+        _check_full(layer, 4096, 4096, 8192)
+    else:
+        _check_full(layer, 1024, 1024, 2048)
 
 
 @pytest.mark.parametrize("w", WL.SHORT_BASES, ids=[w.name for w in WL.SHORT_BASES])
 def test_short_base_micro_benchmark_size(w):
-    """The paper's micro-benchmark size, 2^14 gadgets."""
-    _check_full(w, 128)
+    """The paper's micro-benchmark size, 2^14 gadgets, every one word for word."""
+    _check_full(w, w.n, 0, 0)
 
 
 @pytest.mark.parametrize("w", WL.SHORT_BASES, ids=[w.name for w in WL.SHORT_BASES])
 def test_short_base_at_batched_size(w):
     """As many gadgets as the 16x64x56x56 map, the size the benchmark times."""
-    _check_full(WL.at_size(w, WL.BATCHED.n), 64)
+    _check_full(WL.at_size(w, WL.BATCHED.n), 1024, 1024, 2048)
