@@ -72,6 +72,10 @@ extern "C" {
 #define REDASH_E_NULL (-2)  /* a required pointer is NULL                          */
 #define REDASH_E_HIP (-3)   /* a HIP launch or runtime call failed                 */
 #define REDASH_E_LABEL (-4) /* reported by callers that read d_bad_count > 0       */
+#define REDASH_E_SIZE (-5)  /* the call needs more than the library's fixed buffer */
+
+/* Words of the fixed working buffer of redash_eval_scale_noalloc (64 MiB). */
+#define REDASH_NOALLOC_WORK_WORDS (16ull << 20)
 
 #define REDASH_MAX_K 15
 
@@ -197,6 +201,28 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
  */
 int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
                       uint32_t *d_out_labels, uint32_t *d_work, hipStream_t stream);
+
+/*
+ * redash_eval_scale for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, results and return codes as redash_eval_scale,
+ * without d_work: the working storage is a buffer of
+ * REDASH_NOALLOC_WORK_WORDS words inside the library, one per GPU, which
+ * each GPU holds from the loading of the library's kernels onto it until the
+ * process ends.  The
+ * call allocates and frees nothing (no hipMalloc, hipFree or allocating
+ * library routine).
+ *   Limit: n * work_words (from redash_plan) <= REDASH_NOALLOC_WORK_WORDS,
+ *   else REDASH_E_SIZE and nothing is launched (the 12-prime base scaled by
+ *   one modulus needs 54 words per gadget: up to 310,689 gadgets per call).
+ *   Sharing: every call on a GPU uses that GPU's one buffer.  Calls that can
+ *   overlap on one GPU (different streams without ordering between them, or
+ *   several host threads) race on it and give wrong labels; order them on one
+ *   stream.  Nothing in the buffer has to start at zero, and its contents
+ *   after a call are unspecified.
+ */
+int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
+                              uint32_t *d_out_labels, hipStream_t stream);
 
 /*
  * Garbler decodes the returned labels (Sec. 2.1): v_i = (Y_i[0] - O_i[0]) *

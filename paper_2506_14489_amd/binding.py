@@ -24,6 +24,8 @@ REDASH_E_PARAM = -1
 REDASH_E_NULL = -2
 REDASH_E_HIP = -3
 REDASH_E_LABEL = -4
+REDASH_E_SIZE = -5
+NOALLOC_WORK_WORDS = 16 << 20  # REDASH_NOALLOC_WORK_WORDS
 
 
 class RedashError(RuntimeError):
@@ -135,6 +137,7 @@ def lib() -> ctypes.CDLL:
         L.redash_garble_scale_given.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_encode.argtypes = [pp, vp, vp, vp, vp, vp]
         L.redash_eval_scale.argtypes = [pp, vp, vp, vp, vp, vp]
+        L.redash_eval_scale_noalloc.argtypes = [pp, vp, vp, vp, vp]
         L.redash_decode.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_hash_labels.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, vp, ctypes.c_uint32,
                                          vp, vp, vp]
@@ -145,7 +148,8 @@ def lib() -> ctypes.CDLL:
         L.redash_linear_prepare.argtypes = [lp, vp, vp, vp]
         L.redash_linear_eval.argtypes = [lp, vp, vp, vp, vp, vp]
         L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp, vp]
-        for name in ("redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale", "redash_decode",
+        for name in ("redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale",
+                     "redash_eval_scale_noalloc", "redash_decode",
                      "redash_hash_labels", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
                      "redash_linear_garble"):
             getattr(L, name).restype = ctypes.c_int
@@ -253,6 +257,18 @@ def redash_eval_scale(params, in_labels, tables, out_labels, work, stream=None):
         _ptr(tables, torch.int32, sz["table_words"], "tables"),
         _ptr(out_labels, torch.int32, sz["label_words"], "out_labels"),
         _ptr(work, torch.int32, sz["work_words"], "work"), _stream(stream)), "redash_eval_scale")
+
+
+def redash_eval_scale_noalloc(params, in_labels, tables, out_labels, stream=None):
+    """redash_eval_scale on the library's fixed working buffer (no d_work)."""
+    import torch
+
+    sz = redash_plan(params)
+    _check(lib().redash_eval_scale_noalloc(
+        ctypes.byref(params), _ptr(in_labels, torch.int32, sz["label_words"], "in_labels"),
+        _ptr(tables, torch.int32, sz["table_words"], "tables"),
+        _ptr(out_labels, torch.int32, sz["label_words"], "out_labels"), _stream(stream)),
+        "redash_eval_scale_noalloc")
 
 
 def redash_decode(params, out_labels, out_zero, offsets, y, bad_count, stream=None):

@@ -10,6 +10,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/redash.h"
 #include "device.hpp"
 #include "plan.hpp"
@@ -963,6 +965,57 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Working storage of redash_eval_scale_noalloc.  In host code the name
+// `scratch` only stands in for the device array: kernels get the device
+// address that hipGetSymbolAddress returns on each GPU (every GPU holds its
+// own copy at its own address).
+__device__ __align__(256) uint32_t scratch[REDASH_NOALLOC_WORK_WORDS];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current GPU's scratch array, looked up once per GPU
+// (with that GPU current) on its first use.
+int scratch_address(uint32_t **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return REDASH_E_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return REDASH_E_HIP;
+        g_scratch_ptr[dev] = static_cast<uint32_t *>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return REDASH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
+                              uint32_t *d_out_labels, hipStream_t stream) {
+    Plan P;
+    int rc = build_plan(p, &P);
+    if (rc) return rc;
+    if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
+    if (P.n * P.work_words > REDASH_NOALLOC_WORK_WORDS) return REDASH_E_SIZE;
+    if (P.n == 0) return REDASH_OK;
+    if (!d_in_labels || !d_tables || !d_out_labels) return REDASH_E_NULL;
+    uint32_t *work = nullptr;
+    if ((rc = scratch_address(&work))) return rc;
+    size_t max_lds = 0;
+    if ((rc = max_lds_bytes(&max_lds))) return rc;
+    const uint32_t lds = eval_lds_bytes(P.ntab);
+    if (lds > max_lds) return REDASH_E_HIP;
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, work, stream);
+}
+
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,
                   const uint32_t *d_offsets, int64_t *d_y, uint64_t *d_bad_count, hipStream_t stream) {
     Plan P;
@@ -999,6 +1052,7 @@ const char *redash_strerror(int code) {
         case REDASH_E_NULL: return "null pointer";
         case REDASH_E_HIP: return "HIP launch or runtime error";
         case REDASH_E_LABEL: return "output label failed the decode check";
+        case REDASH_E_SIZE: return "the call needs more working storage than the fixed buffer holds";
         default: return "unknown error";
     }
 }

@@ -17,7 +17,7 @@ from paper_2506_14489_amd import workloads as WL
 def test_library_exports_every_declared_symbol():
     names = B.declared_symbols()
     assert set(names) == {"redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale",
-                          "redash_decode", "redash_hash_labels", "redash_strerror", "redash_linear_plan",
+                          "redash_eval_scale_noalloc", "redash_decode", "redash_hash_labels", "redash_strerror", "redash_linear_plan",
                           "redash_linear_prepare", "redash_linear_eval", "redash_linear_garble"}
     L = B.lib()
     for n in names:
@@ -36,7 +36,7 @@ def test_params_struct_layout_matches_header():
 
 def test_strerror_texts():
     assert B.strerror(0) == "ok"
-    for code in (-1, -2, -3, -4):
+    for code in (-1, -2, -3, -4, -5):
         assert B.strerror(code) != "unknown error"
     assert B.strerror(42) == "unknown error"
 
@@ -164,6 +164,34 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_hash_labels(3, 256, 1, fake, 0, fake, fake, None) == B.REDASH_E_PARAM
     assert L.redash_hash_labels(3, 5, 1, None, 0, fake, fake, None) == B.REDASH_E_NULL
     assert L.redash_eval_scale(None, fake, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale_noalloc(ctypes.byref(bad), fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_eval_scale_noalloc(ctypes.byref(huge), fake, fake, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_eval_scale_noalloc(ctypes.byref(good), None, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale_noalloc(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale_noalloc(ctypes.byref(good), fake, fake, None, None) == B.REDASH_E_NULL
+    assert L.redash_eval_scale_noalloc(None, fake, fake, fake, None) == B.REDASH_E_NULL
+
+
+def test_noalloc_size_limit():
+    """The allocation-free evaluator takes calls whose working storage fits
+    its fixed buffer and rejects larger ones on the host, before any HIP call
+    (54 working words per gadget on the 12-prime base: at most 310,689)."""
+    L = B.lib()
+    w = WL.BATCHED
+    per = B.redash_plan(B.make_params(w.moduli, w.scale_idx, 1, w.seed))["work_words"]
+    assert per == 54
+    n_max = B.NOALLOC_WORK_WORDS // per
+    assert n_max == 310689
+    fits = B.make_params(w.moduli, w.scale_idx, n_max, w.seed)
+    over = B.make_params(w.moduli, w.scale_idx, n_max + 1, w.seed)
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced
+    assert L.redash_eval_scale_noalloc(ctypes.byref(over), fake, fake, fake, None) == B.REDASH_E_SIZE
+    # within the limit the call gets as far as its pointer checks
+    assert L.redash_eval_scale_noalloc(ctypes.byref(fits), None, fake, fake, None) == B.REDASH_E_NULL
+    # a base without working storage (one remaining modulus) has no limit below 2^30
+    two = B.make_params([2, 3], [1], (1 << 30) - 1, 0)
+    assert B.redash_plan(two)["work_words"] == 0
+    assert L.redash_eval_scale_noalloc(ctypes.byref(two), None, fake, fake, None) == B.REDASH_E_NULL
 
 
 # ---------------------------------------------------------------------------
