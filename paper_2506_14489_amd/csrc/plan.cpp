@@ -338,4 +338,156 @@ int build_plan(const redash_params *p, Plan *pl) {
     return REDASH_OK;
 }
 
+namespace {
+
+// One gate of a target's list: the digit it hashes and the gate index.
+// Digits are numbered: Phase-A digit of S[a] is a, Phase-B digit of R[b] is
+// kMaxK + b.
+struct TGate {
+    uint32_t digit, g;
+};
+
+struct Target {
+    uint32_t mod;       // modulus index
+    uint32_t from_in;   // starts from the input label (else from zero)
+    uint32_t kind;      // 0: S[a] of Phase A, 1: R[j], 2: accumulator of S[a]
+    uint32_t digit;     // the digit this target becomes (kind 0 and 1), else ~0u
+    uint32_t nA;        // its first nA gates are Phase-A gates
+    uint32_t n;
+    TGate gate[kMaxK + kMaxK];
+};
+
+}  // namespace
+
+void build_eval_plan(const Plan &P, EvalPlan *E) {
+    memset(E, 0, sizeof *E);
+    E->k = P.k;
+    E->t = P.t;
+    E->u = P.u;
+    E->G = P.G;
+    E->total_words = P.total_words;
+    E->work_words = P.work_words;
+    E->ntab = P.ntab;
+    E->gid = P.gid;
+    E->n = P.n;
+    E->a0 = P.a0;
+    for (uint32_t i = 0; i < P.k; ++i) E->mod[i] = P.mod[i];
+    // gate lookup by (phase, digit modulus, destination modulus)
+    uint32_t gidx[2][kMaxK][kMaxK];
+    uint32_t toff = 0;
+    for (uint32_t g = 0; g < P.G; ++g) {
+        const uint32_t d = P.gate[g];
+        gidx[gate_phase(d)][gate_src(d)][gate_dst(d)] = g;
+        E->egate[g] = gate_dst(d) | (gate_kind(d) << 4) | (gate_tab(d) << 5) | (gate_coeff(d) << 6) | (toff << 14);
+        toff += (P.mod[gate_src(d)].m - 1) * P.mod[gate_dst(d)].W;
+    }
+    // the targets in the order they are finished
+    Target T[3 * kMaxK];
+    uint32_t nt = 0;
+    for (uint32_t a = 1; a < P.t; ++a) {
+        Target &x = T[nt++];
+        x = Target{P.S[a], 1, 0, a, 0, 0, {}};
+        for (uint32_t b = 0; b < a; ++b) x.gate[x.n++] = TGate{b, gidx[0][P.S[b]][P.S[a]]};
+        x.nA = x.n;
+    }
+    for (uint32_t j = 0; j < P.u; ++j) {
+        Target &x = T[nt++];
+        x = Target{P.R[j], 1, 1, kMaxK + j, 0, 0, {}};
+        for (uint32_t a = 0; a < P.t; ++a) x.gate[x.n++] = TGate{a, gidx[0][P.S[a]][P.R[j]]};
+        x.nA = x.n;
+        for (uint32_t b = 0; b < j; ++b) x.gate[x.n++] = TGate{kMaxK + b, gidx[1][P.R[b]][P.R[j]]};
+    }
+    for (uint32_t a = 0; a < P.t; ++a) {
+        Target &x = T[nt++];
+        x = Target{P.S[a], 0, 2, ~0u, 0, 0, {}};
+        for (uint32_t b = 0; b < P.u; ++b) x.gate[x.n++] = TGate{kMaxK + b, gidx[1][P.R[b]][P.S[a]]};
+    }
+    // blocks: pairs of consecutive targets; with an odd count the first
+    // target (the one with the fewest gates) is alone
+    uint32_t first[kMaxBlocks], second[kMaxBlocks], nb = 0;
+    for (uint32_t next = 0; next < nt;) {
+        const bool alone = (next == 0 && nt % 2);
+        first[nb] = next;
+        second[nb++] = alone ? ~0u : next + 1;
+        next += alone ? 1 : 2;
+    }
+    uint32_t block_of[3 * kMaxK];
+    for (uint32_t b = 0; b < nb; ++b) {
+        block_of[first[b]] = b;
+        if (second[b] != ~0u) block_of[second[b]] = b;
+    }
+    // where a digit is read from (outside its own block), and whether a
+    // target must be stored for readers in later blocks
+    auto digit_loc = [&](uint32_t digit) -> uint32_t {
+        if (digit < kMaxK) return digit == 0 ? kDigIn : kDigOut;
+        return digit == kMaxK ? kDigOut : kDigWork;
+    };
+    auto digit_mod = [&](uint32_t digit) -> uint32_t { return digit < kMaxK ? P.S[digit] : P.R[digit - kMaxK]; };
+    auto read_elsewhere = [&](uint32_t ti) {
+        const uint32_t digit = T[ti].digit;
+        if (digit == ~0u) return false;
+        for (uint32_t o = 0; o < nt; ++o)
+            for (uint32_t i = 0; i < T[o].n; ++i)
+                if (T[o].gate[i].digit == digit && block_of[o] != block_of[ti]) return true;
+        return false;
+    };
+    // stores after gate i (0-based) of target ti: bit 0 output, bit 1 working
+    auto stores_after = [&](uint32_t ti, uint32_t i) -> uint32_t {
+        const Target &x = T[ti];
+        uint32_t f = 0;
+        if (x.kind == 1) {
+            if (i + 1 == x.nA) f |= 1u;  // the Phase-A value is the output label of R[j]
+            // R[0]'s digit is read from the output tensor; R[j], j >= 1, from the working storage
+            if (i + 1 == x.n && x.digit != kMaxK && read_elsewhere(ti)) f |= 2u;
+        } else if (i + 1 == x.n) {
+            if (x.kind == 2 || read_elsewhere(ti)) f |= 1u;
+        }
+        return f;
+    };
+    uint32_t ns = 0;
+    for (uint32_t b = 0; b < nb; ++b) {
+        const Target &X = T[first[b]];
+        const bool two = second[b] != ~0u;
+        const Target &Y = two ? T[second[b]] : X;
+        const uint32_t s0 = ns;
+        uint32_t i = 0, j = 0;
+        auto later_in_y = [&](uint32_t digit, uint32_t from) {
+            if (!two) return false;
+            for (uint32_t q = from; q < Y.n; ++q)
+                if (Y.gate[q].digit == digit) return true;
+            return false;
+        };
+        while (i < X.n || (two && j < Y.n)) {
+            uint32_t st = 0;
+            if (two && i < X.n && j < Y.n && X.gate[i].digit == Y.gate[j].digit) {
+                // one digit for both slots: two consecutive gates of its run
+                const uint32_t digit = X.gate[i].digit;
+                st = X.gate[i].g | (1u << 8) | (digit_loc(digit) << 10) | (digit_mod(digit) << 12);
+                st |= stores_after(first[b], i) << 16;
+                st |= stores_after(second[b], j) << 18;
+                ++i;
+                ++j;
+            } else if (i < X.n && !later_in_y(X.gate[i].digit, j)) {
+                const uint32_t digit = X.gate[i].digit;
+                st = X.gate[i].g | (digit_loc(digit) << 10) | (digit_mod(digit) << 12);
+                st |= stores_after(first[b], i) << 16;
+                ++i;
+            } else {
+                // slot 1 alone; its digit is read from slot 0 once slot 0 is final
+                const uint32_t digit = Y.gate[j].digit;
+                const uint32_t loc = (digit == X.digit && i == X.n) ? kDigSlot0 : digit_loc(digit);
+                st = Y.gate[j].g | (1u << 9) | (loc << 10) | (digit_mod(digit) << 12);
+                st |= stores_after(second[b], j) << 18;
+                ++j;
+            }
+            E->step[ns++] = st;
+        }
+        uint32_t bd = X.mod | (X.from_in << 4) | ((ns - s0) << 24) | (s0 << 16);
+        if (two) bd |= (1u << 5) | (Y.mod << 6) | (Y.from_in << 10);
+        E->block[b] = bd;
+    }
+    E->nblocks = nb;
+    E->nsteps = ns;
+}
+
 }  // namespace redash

@@ -128,6 +128,79 @@ struct Plan {
 // REDASH_E_PARAM.
 int build_plan(const redash_params *p, Plan *out);
 
+// ---------------------------------------------------------------------------
+// Target-major schedule of the one-gadget-per-lane evaluator.
+//
+// Every label that projection gates update (a "target") is kept in
+// registers from its first update to its last, so it is read once and
+// written once.  The targets, in the order the evaluator finishes them:
+// S[1..t-1] (Phase A: each becomes the digit of its division step),
+// R[0..u-1] (Phase A, then the recursion of Phase B: R[j] becomes digit j of
+// the mixed-radix conversion), then the accumulators of S[0..t-1] (Phase B).
+// A target's gates come in the order the paper applies them (its Phase-A
+// digits, then its Phase-B digits), since the division steps do not commute.
+// Consecutive targets are paired into blocks of two register slots; a step
+// hashes one digit label for the gates of both slots that take it (two
+// consecutive gates of the canonical gate list, so the tweaks and tables do
+// not change), or for one slot.  The digit label is read from the input
+// tensor (S[0]), the output tensor (S[a], a >= 1, and R[0], which are final
+// there), the working storage (R[j], j >= 1, stored once when final) or,
+// when it is the block's own first target, its registers.
+// ---------------------------------------------------------------------------
+
+// Per gate: bits 0-3 dst modulus index, 4 kind (0 sub, 1 acc), 5 the gate's
+// free operation uses its byte table, 6-13 coefficient, 14-31 word offset of
+// the gate's table block in units of n words (sum of (q-1) W_dst over the
+// earlier gates; below 2^18 for every base).
+constexpr uint32_t eg_dst(uint32_t e) { return e & 15u; }
+constexpr uint32_t eg_kind(uint32_t e) { return (e >> 4) & 1u; }
+constexpr uint32_t eg_tab(uint32_t e) { return (e >> 5) & 1u; }
+constexpr uint32_t eg_coeff(uint32_t e) { return (e >> 6) & 255u; }
+constexpr uint32_t eg_toff(uint32_t e) { return e >> 14; }
+
+// Per step: bits 0-7 the first gate g (the second, if any, is g + 1),
+// 8 two gates (slot 0 takes g, slot 1 takes g + 1), 9 the single gate goes
+// to slot 1, 10-11 where the digit label is (kDigIn, kDigOut, kDigWork,
+// kDigSlot0), 12-15 the digit's modulus index, then what is stored after the
+// step: 16 slot 0 to the output tensor, 17 slot 0 to the working storage,
+// 18 slot 1 to the output tensor, 19 slot 1 to the working storage.
+constexpr uint32_t kDigIn = 0, kDigOut = 1, kDigWork = 2, kDigSlot0 = 3;
+constexpr uint32_t st_gate(uint32_t s) { return s & 255u; }
+constexpr uint32_t st_two(uint32_t s) { return (s >> 8) & 1u; }
+constexpr uint32_t st_slot1(uint32_t s) { return (s >> 9) & 1u; }
+constexpr uint32_t st_dloc(uint32_t s) { return (s >> 10) & 3u; }
+constexpr uint32_t st_dmod(uint32_t s) { return (s >> 12) & 15u; }
+constexpr uint32_t st_store(uint32_t s) { return (s >> 16) & 15u; }  // bit 0 s0 out, 1 s0 work, 2 s1 out, 3 s1 work
+
+// Per block: bits 0-3 slot 0's modulus index, 4 slot 0 starts from the
+// input tensor (else from the all-zero label), 5 slot 1 is used, 6-9 slot
+// 1's modulus index, 10 slot 1 starts from the input tensor, 16-23 first
+// step, 24-31 number of steps.
+constexpr uint32_t bk_mod0(uint32_t b) { return b & 15u; }
+constexpr uint32_t bk_in0(uint32_t b) { return (b >> 4) & 1u; }
+constexpr uint32_t bk_two(uint32_t b) { return (b >> 5) & 1u; }
+constexpr uint32_t bk_mod1(uint32_t b) { return (b >> 6) & 15u; }
+constexpr uint32_t bk_in1(uint32_t b) { return (b >> 10) & 1u; }
+constexpr uint32_t bk_first(uint32_t b) { return (b >> 16) & 255u; }
+constexpr uint32_t bk_steps(uint32_t b) { return b >> 24; }
+constexpr int kMaxBlocks = 16;  // ceil((k + t - 1) / 2) <= 14
+
+struct EvalPlan {
+    uint32_t k, t, u, G;
+    uint32_t total_words, work_words;
+    uint32_t ntab;             // gates 0..ntab-1 have a free-operation table slot
+    uint32_t nblocks, nsteps;
+    uint32_t gid;
+    uint64_t n, a0;
+    ModConst mod[kMaxK];
+    uint32_t egate[kMaxGates];
+    uint32_t step[kMaxGates];
+    uint32_t block[kMaxBlocks];
+};
+
+// The evaluator's target-major schedule for a plan built by build_plan.
+void build_eval_plan(const Plan &P, EvalPlan *out);
+
 // A modulus the library accepts: a prime or a power of two in 2..255.
 bool modulus_ok(uint32_t m);
 

@@ -37,10 +37,14 @@ constexpr uint32_t kEvalTableBase = kTableRegionBytes + 384;  // after the 352 k
 constexpr uint32_t eval_lds_bytes(uint32_t ntab) { return kEvalTableBase + ntab * kTableBytes; }
 static_assert(kLdsKeyWords * 4 <= 384, "round keys overlap the free-operation tables");
 static_assert(2 * (kEvalTableBase + kMaxTables * kTableBytes) <= 160 * 1024, "two workgroups per CU");
+static_assert(sizeof(EvalPlan) <= 4096, "the evaluator's plan is passed as its kernel argument block");
 // Two workgroups of 768 threads share a CU (2 x 64.3 KiB of LDS): six waves
 // per SIMD, which caps the kernel at 80 VGPRs.
 constexpr int kEvalBlock = 768;
 constexpr int kEvalWaves = 6;
+// The one-gadget-per-lane evaluator k_eval: workgroup size and waves per SIMD.
+constexpr int kLaneBlock = 768;
+constexpr int kLaneWaves = 6;
 // The garbler: the same LDS image without the free-operation tables; two
 // workgroups of 512 per CU, four waves per SIMD (up to 128 VGPRs).
 constexpr int kGarbleBlock = 512;
@@ -232,51 +236,295 @@ __device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &
     static_for<NG>([&](auto j) { static_for<8>([&](auto l) { V[j][l] = Vn[j][l]; }); });
 }
 
+// ---------------------------------------------------------------------------
+// The one-gadget-per-lane evaluator, target-major (EvalPlan): a block's two
+// target labels stay in registers from their first gate to their last, so
+// each is read and written once; a step hashes one digit label for one gate
+// of each slot (four AES blocks interleaved) or for one slot.  Updates always
+// act on slot 0: slot 1 is brought there by swapping the two slots.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void swap_slots(uint32_t (&T)[2][kMaxW]) {
+    static_for<kMaxW>([&](auto w) {
+        const uint32_t v = T[0][w];
+        T[0][w] = T[1][w];
+        T[1][w] = v;
+    });
+}
+
+// Register labels are right-aligned: a label of W words sits in positions
+// kMaxW - W .. kMaxW - 1 of its array (W is 4, 5 or 6), so its last word --
+// the one with its own digit count -- is always at position kMaxW - 1 and
+// every word is at a constant position: the word loops below are unrolled
+// with a uniform test per position, and no register moves.
+__device__ __forceinline__ uint32_t label_off(const ModConst &mc) { return kMaxW - mc.W; }
+
+__device__ __forceinline__ void load_label(uint32_t (&T)[kMaxW], const LabelBufs &LB, uint32_t loc, const ModConst &mc,
+                                           bool from_input) {
+    static_for<kMaxW>([&](auto p) { T[p] = 0; });
+    if (from_input) {
+        const uint32_t off = label_off(mc);
+        const uint32_t *b = LB.base(loc, mc);
+        static_for<kMaxW>([&](auto p) {
+            if (p >= static_cast<int>(off)) T[p] = LB.get(b, p - off);
+        });
+    }
+}
+
+__device__ __forceinline__ void store_label(const uint32_t (&T)[kMaxW], const LabelBufs &LB, uint32_t to_work,
+                                            const ModConst &mc) {
+    const uint32_t off = label_off(mc);
+    uint32_t *b = LB.dest(to_work, mc);
+    static_for<kMaxW>([&](auto p) {
+        if (p >= static_cast<int>(off)) LB.put(b, p - off, T[p]);
+    });
+}
+
+// XOR-fold of a right-aligned register label with OFF = kMaxW - W: word w
+// goes into lane w mod 4.
+template <int OFF>
+__device__ __forceinline__ void fold_regs(const uint32_t (&T)[kMaxW], uint32_t (&x)[4]) {
+    static_for<kMaxW - OFF>([&](auto w) { x[w & 3] ^= T[w + OFF]; });
+}
+
+// Generic moduli (see eval_update_generic): all kMaxW positions in a rolled
+// loop that rotates the label and the row by one word per position (kMaxW
+// rotations put both back in place).
+__device__ __forceinline__ void reg_update_generic(uint32_t e, const ModConst &mm, uint32_t (&V)[8],
+                                                   uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW]) {
+    const uint32_t coeff = eg_coeff(e), off = label_off(mm);
+#pragma unroll 1
+    for (uint32_t p = 0; p < static_cast<uint32_t>(kMaxW); ++p) {
+        const uint32_t l = next_word(T);
+        const uint32_t rw = next_word(row);
+        uint32_t res = l;
+        if (p >= off) {
+            const bool last = (p + 1 == static_cast<uint32_t>(kMaxW));
+            const uint32_t nres = last ? mm.glast : mm.g;
+            uint32_t D = frac_carry_any(V, last ? mm.pw_last : mm.pw_g);
+            res = 0;
+            for (uint32_t j = nres; j-- > 0;) {
+                uint32_t pd;
+                if (j) {
+                    const uint32_t qd = div_m(D, mm);
+                    pd = D - qd * mm.m;
+                    D = qd;
+                } else {
+                    pd = D;
+                }
+                const uint32_t ev = add_mod(pd, field(rw, j, mm), mm.m);
+                const uint32_t lj = field(l, j, mm);
+                const uint32_t r = eg_kind(e) == 0 ? mul_mod(coeff, sub_mod(lj, ev, mm.m), mm)
+                                                   : add_mod(lj, mul_mod(coeff, ev, mm), mm.m);
+                res |= r << (mm.b * j);
+            }
+        }
+        T[kMaxW - 1] = res;
+        row[kMaxW - 1] = rw;
+    }
+}
+
+// The full words (positions kMaxW - W .. kMaxW - 2) with the word shape
+// (residues per word, bits per residue) known at compile time: the shape is
+// dispatched once per gate, not once per word.
+template <bool ACC, bool TAB, int NR, int BB>
+__device__ __forceinline__ void reg_full_words(const ModConst &mm, uint32_t coeff, uint32_t (&V)[8],
+                                               const uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW], uint32_t tk) {
+    const uint32_t off = label_off(mm);
+    static_for<kMaxW - 1>([&](auto p) {
+        if (p >= static_cast<int>(off)) {
+            const uint32_t D = frac_mul_carry(V, mm.pw_g);
+            T[p] = fast_word_c<ACC, NR, BB, TAB>(D, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f, mm.fc_lo_f, row[p],
+                                                 T[p], coeff, mm, tk);
+        }
+    });
+}
+
+template <bool ACC, bool TAB>
+__device__ __forceinline__ void reg_update_fast(uint32_t e, const ModConst &mm, uint32_t (&V)[8],
+                                                const uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW], uint32_t tk) {
+    const uint32_t coeff = eg_coeff(e);
+    // full words: g = floor(32 / b) residues of b bits
+    switch (mm.fd ? mm.g | (mm.b << 8) : 0u) {
+#define REDASH_FULL(NR, BB) \
+    case (NR) | ((BB) << 8): reg_full_words<ACC, TAB, NR, BB>(mm, coeff, V, row, T, tk); break;
+        REDASH_FULL(16, 2) REDASH_FULL(10, 3) REDASH_FULL(8, 4) REDASH_FULL(6, 5) REDASH_FULL(5, 6)
+        REDASH_FULL(4, 7) REDASH_FULL(4, 8)
+#undef REDASH_FULL
+        default: {
+            const uint32_t off = label_off(mm);
+            static_for<kMaxW - 1>([&](auto p) {
+                if (p >= static_cast<int>(off)) {
+                    const uint32_t D = frac_mul_carry(V, mm.pw_g);
+                    T[p] = fast_word<ACC>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, row[p], T[p], coeff,
+                                          mm);
+                }
+            });
+        }
+    }
+    const uint32_t D = frac_mul_carry(V, mm.pw_last);
+    T[kMaxW - 1] = fast_word_any<ACC, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l,
+                                           mm.fc_lo_l, row[kMaxW - 1], T[kMaxW - 1], coeff, mm, tk);
+}
+
+// Gate g's free operation on the register label T (see eval_update).
+__device__ __forceinline__ void reg_update(uint32_t g, uint32_t e, const ModConst &mm, uint32_t (&V)[8],
+                                           uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW]) {
+    if (mm.m == 2) {  // W = 4: positions 2..5
+        const bool flip = eg_kind(e) == 0 || (eg_coeff(e) & 1u);  // sub: q^{-1} = 1 mod 2
+        if (flip) {
+            static_for<4>([&](auto w) { T[w + 2] ^= bits_word(V, w) ^ row[w + 2]; });
+        }
+    } else if (eg_tab(e)) {
+        const uint32_t tk = kEvalTableBase + g * kTableBytes + (eg_kind(e) ? 0u : mm.two_m);
+        if (eg_kind(e)) {
+            reg_update_fast<true, true>(e, mm, V, row, T, tk);
+        } else {
+            reg_update_fast<false, true>(e, mm, V, row, T, tk);
+        }
+    } else if (mm.fast) {
+        if (eg_kind(e)) {
+            reg_update_fast<true, false>(e, mm, V, row, T, 0);
+        } else {
+            reg_update_fast<false, false>(e, mm, V, row, T, 0);
+        }
+    } else {
+        reg_update_generic(e, mm, V, row, T);
+    }
+}
+
+// The free-operation tables of an EvalPlan (as stage_free_op_tables).
+__device__ __forceinline__ void stage_free_op_tables_e(const EvalPlan &P, uint32_t *lds, int tid, uint32_t nwaves) {
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
+    const uint32_t lane = static_cast<uint32_t>(tid) % 64u;
+    for (uint32_t g = wave; g < P.ntab; g += nwaves) {
+        const uint32_t e = P.egate[g];
+        if (!eg_tab(e) || lane >= kTableBytes / 4) continue;
+        const uint32_t m = P.mod[eg_dst(e)].m, c = eg_coeff(e);
+        uint32_t w = 0;
+        for (uint32_t k = 0; k < 4; ++k) {
+            const uint32_t v = 4 * lane + k;
+            w |= ((c * (v % m)) % m) << (8 * k);
+        }
+        lds[(kEvalTableBase + g * kTableBytes) / 4 + lane] = w;
+    }
+}
+
+// One step's NG gates g, g+1 (NG = 2) or g: requests their rows (the colour
+// is known before hashing), then runs the 2 NG AES blocks interleaved.
+//
+// The gadget index a (below 2^30) is a 32-bit register: the row offset
+// a (q-1) W + (c-1) W and the tweak (a0 + a) G + g are each one
+// 32 x 32 + 64-bit multiply-add from it, instead of 64-bit values kept live
+// across the whole gadget.
+__device__ __forceinline__ uint64_t mad64(uint32_t x, uint32_t y, uint64_t z) {
+    return static_cast<uint64_t>(x) * y + z;
+}
+
+template <int NG>
+__device__ __forceinline__ void step_hash(const EvalPlan &P, uint32_t g, uint32_t q, const uint32_t (&x)[4],
+                                          uint32_t colour, const PermTE02 &TT, const uint32_t *K, uint32_t a,
+                                          const uint32_t *__restrict__ tab, uint32_t (&V)[2][8],
+                                          uint32_t (&row)[2][kMaxW]) {
+    static_for<NG>([&](auto j) {
+        const uint32_t e = P.egate[g + j];
+        const uint32_t Wd = P.mod[eg_dst(e)].W;
+        static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
+        if (colour != 0) {  // right-aligned like the labels
+            const uint32_t *rp = tab + static_cast<uint64_t>(eg_toff(e)) * P.n +
+                                 mad64(opaque(a), (q - 1) * Wd, static_cast<uint64_t>(colour - 1) * Wd);
+            const int off = kMaxW - static_cast<int>(Wd);
+            static_for<kMaxW>([&](auto p) {
+                if (p >= off) row[j][p] = rp[p - off];
+            });
+        }
+    });
+    uint32_t Vn[NG][8];
+    const uint64_t tau = mad64(opaque(a), P.G, P.a0 * P.G + g);
+    hash_fraction_n<NG>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau, P.gid, Vn);
+    static_for<NG>([&](auto j) { static_for<8>([&](auto l) { V[j][l] = Vn[j][l]; }); });
+}
+
 template <int BLOCK>
-__global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))
-k_eval(const Plan P, const uint32_t *__restrict__ in,
-                                                const uint32_t *__restrict__ tab, uint32_t *out, uint32_t *work) {
+__global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kLaneWaves, kLaneWaves)))
+k_eval(const EvalPlan P, const uint32_t *__restrict__ in, const uint32_t *__restrict__ tab, uint32_t *out,
+       uint32_t *work) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;  // BLOCK or fewer (a multiple of 64)
     stage_perm_te02(lds, tid, nthr);
     stage_hash_key(K, tid, nthr);
-    stage_free_op_tables(P, lds, tid, static_cast<uint32_t>(nthr) / 64u);
+    stage_free_op_tables_e(P, lds, tid, static_cast<uint32_t>(nthr) / 64u);
     __syncthreads();
     const PermTE02 TT = perm_te02();
-    const uint64_t a = static_cast<uint64_t>(blockIdx.x) * nthr + tid;
+    const uint32_t a = blockIdx.x * static_cast<uint32_t>(nthr) + static_cast<uint32_t>(tid);  // n < 2^30
     if (a >= P.n) return;  // no barrier follows
-    const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(a) * 4u};
+    const LabelBufs LB{in, out, work, P.n, a * 4u};
 
-    const uint64_t tau0 = (P.a0 + a) * P.G;
-    uint64_t toff = 0;
-    for (uint32_t g = 0; g < P.G;) {
-        const uint32_t len = gate_chunk(P.gate[g]);
-        uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW], tgt[kMaxChunk][kMaxW];
-        if (kMaxChunk >= 4 && len == 4) {
-            hash_chunk<(kMaxChunk >= 4 ? 4 : 1)>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
-        } else if (len == 2) {
-            hash_chunk<2>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
-        } else {
-            hash_chunk<1>(P, g, toff, TT, K, LB, a, tau0, tab, V, row, tgt);
-        }
-        // One copy of the update code for every chunk size: the chunk's
-        // gates go through a queue (entry 0 is processed, the rest move down).
-#pragma unroll 1
-        for (uint32_t j = 0; j < len; ++j) {
-            const uint32_t dj = P.gate[g + j];
-            const ModConst mm = P.mod[gate_dst(dj)];
-            eval_update(g + j, dj, mm, V[0], row[0], tgt[0], LB);
-            static_for<kMaxChunk - 1>([&](auto k) {
-                static_for<8>([&](auto l) { V[k][l] = V[k + 1][l]; });
-                static_for<kMaxW>([&](auto w) {
-                    row[k][w] = row[k + 1][w];
-                    tgt[k][w] = tgt[k + 1][w];
+    for (uint32_t b = 0; b < P.nblocks; ++b) {
+        const uint32_t bd = P.block[b];
+        uint32_t T[2][kMaxW];
+        load_label(T[0], LB, kLocIn, P.mod[bk_mod0(bd)], bk_in0(bd) != 0);
+        load_label(T[1], LB, kLocIn, P.mod[bk_mod1(bd)], bk_two(bd) && bk_in1(bd));
+        const uint32_t s_end = bk_first(bd) + bk_steps(bd);
+        for (uint32_t s = bk_first(bd); s < s_end; ++s) {
+            const uint32_t sd = P.step[s];
+            const bool two = st_two(sd) != 0;
+            const bool alone1 = !two && st_slot1(sd);
+            if (alone1) swap_slots(T);  // slot 1's gate acts on slot 0's registers
+            // The digit label: folded into 128 bits for the hash, colour =
+            // residue 0.  A residue >= q only occurs in a malformed input
+            // label; it selects the implicit zero row, the output is garbage
+            // and decode flags it.
+            const ModConst mq = P.mod[st_dmod(sd)];
+            const uint32_t q = mq.m;
+            uint32_t x[4] = {0, 0, 0, 0}, w0;
+            if (st_dloc(sd) == kDigSlot0) {  // the block's first target, now in T[1]
+                switch (label_off(mq)) {
+                    case 0: fold_regs<0>(T[1], x); w0 = T[1][0]; break;
+                    case 1: fold_regs<1>(T[1], x); w0 = T[1][1]; break;
+                    default: fold_regs<2>(T[1], x); w0 = T[1][2]; break;
+                }
+            } else {
+                const uint32_t *dig = LB.base(st_dloc(sd), mq);
+                w0 = LB.get(dig, 0);
+                x[0] = w0;
+                static_for<kMaxW - 1>([&](auto w1) {
+                    constexpr int w = decltype(w1)::value + 1;
+                    if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
                 });
-            });
+            }
+            uint32_t colour = w0 & mq.mask;
+            if (colour >= q) colour = 0;
+            const uint32_t g = st_gate(sd);
+            uint32_t V[2][8], row[2][kMaxW];
+            if (two) {
+                step_hash<2>(P, g, q, x, colour, TT, K, a, tab, V, row);
+            } else {
+                step_hash<1>(P, g, q, x, colour, TT, K, a, tab, V, row);
+            }
+            // one copy of the update code: gate j acts on slot 0, then the
+            // slots (and the gate's pad and row) move along
+            const uint32_t ng = two ? 2u : 1u;
+#pragma unroll 1
+            for (uint32_t j = 0; j < ng; ++j) {
+                const uint32_t e = P.egate[g + j];
+                const ModConst mm = P.mod[eg_dst(e)];
+                reg_update(g + j, e, mm, V[0], row[0], T[0]);
+                if (two) {
+                    swap_slots(T);
+                    static_for<8>([&](auto l) { V[0][l] = V[1][l]; });
+                    static_for<kMaxW>([&](auto w) { row[0][w] = row[1][w]; });
+                }
+            }
+            if (alone1) swap_slots(T);
+            const uint32_t f = st_store(sd);
+            if (f & 3u) store_label(T[0], LB, (f >> 1) & 1u, P.mod[bk_mod0(bd)]);
+            if ((f & 3u) == 3u) store_label(T[0], LB, 0, P.mod[bk_mod0(bd)]);
+            if (f & 12u) store_label(T[1], LB, (f >> 3) & 1u, P.mod[bk_mod1(bd)]);
+            if ((f & 12u) == 12u) store_label(T[1], LB, 0, P.mod[bk_mod1(bd)]);
         }
-        g += len;
     }
 }
 
@@ -845,15 +1093,17 @@ int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t 
     const uint64_t ncu = static_cast<uint64_t>(cus);
     if (const uint32_t split = split_for(P.n, ncu))
         return launch_split_any(split, P, lds, in, tab, out, work, 0, P.n, stream);
-    const uint64_t round = 2 * ncu * kEvalBlock;  // gadgets of one round, one per lane
+    const uint64_t round = 2 * ncu * kLaneBlock;  // gadgets of one round, one per lane
     uint64_t bulk = P.n;
     const uint64_t rest = P.n % round;
     if (P.n > round && rest > 0 && rest <= 2 * ncu * 64) bulk = P.n - rest;
-    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kEvalBlock>), lds);
+    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kLaneBlock>), lds);
     if (rc) return rc;
     int block = 0;
-    if ((rc = block_for(bulk, kEvalBlock, &block))) return rc;
-    hipLaunchKernelGGL(k_eval<kEvalBlock>, dim3(grid_for(bulk, block)), dim3(block), lds, stream, P, in, tab, out,
+    if ((rc = block_for(bulk, kLaneBlock, &block))) return rc;
+    EvalPlan E;
+    build_eval_plan(P, &E);
+    hipLaunchKernelGGL(k_eval<kLaneBlock>, dim3(grid_for(bulk, block)), dim3(block), lds, stream, E, in, tab, out,
                        work);
     if ((rc = launched())) return rc;
     if (bulk == P.n) return REDASH_OK;

@@ -14,6 +14,7 @@
 // construction, umulhi(x, 2^(32-e)) = x >> e; it is checked on a sample.)
 #include <stdint.h>
 #include <stdio.h>
+#include <string.h>
 
 #include "../paper_2506_14489_amd/csrc/plan.hpp"
 
@@ -166,7 +167,160 @@ static void check_modulus(uint32_t m) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// The evaluator's target-major schedule (build_eval_plan), run on values
+// instead of labels: a label over Z_m is replaced by the residue it carries,
+// a projection gate q -> m maps digit value v to v mod m, a sub gate is
+// L <- c (L - E), an acc gate Acc <- Acc + c E.  Every label is read from the
+// place the schedule names (input, output, working storage or slot 0) and
+// stored where it says, into buffers that start poisoned, exactly as the
+// kernel does.  For every x the outputs must be floor(x_up / s) mod m_i with
+// x_up = (x + floor(P/2)) mod P (the ShiftUp is the garbler's; the value the
+// evaluator's labels carry), the Phase-B values the mixed-radix digits, and
+// every gate must be used exactly once, pairs on consecutive gates.
+// ---------------------------------------------------------------------------
+static const uint32_t kPoison = 0xdeadbeefu;
+
+static void check_schedule(const uint32_t *moduli, uint32_t k, const uint32_t *S, uint32_t t, uint64_t seed) {
+    redash_params p;
+    memset(&p, 0, sizeof p);
+    p.k = k;
+    p.t = t;
+    for (uint32_t i = 0; i < k; ++i) p.moduli[i] = moduli[i];
+    for (uint32_t a = 0; a < t; ++a) p.scale_idx[a] = S[a];
+    p.n = 1;
+    Plan P;
+    CHECK(build_plan(&p, &P) == REDASH_OK, "plan k=%u t=%u", k, t);
+    static EvalPlan E;
+    build_eval_plan(P, &E);
+    CHECK(sizeof(EvalPlan) <= 4096, "EvalPlan of %zu bytes exceeds the kernel-argument limit", sizeof(EvalPlan));
+    // every gate exactly once
+    uint32_t used[kMaxGates] = {};
+    for (uint32_t st = 0; st < E.nsteps; ++st) {
+        const uint32_t s0 = E.step[st];
+        used[st_gate(s0)]++;
+        if (st_two(s0)) used[st_gate(s0) + 1]++;
+    }
+    for (uint32_t g = 0; g < P.G; ++g) CHECK(used[g] == 1, "k=%u t=%u gate %u used %u times", k, t, g, used[g]);
+    CHECK(E.nblocks <= static_cast<uint32_t>(kMaxBlocks), "blocks %u", E.nblocks);
+    // table offsets: running sum of (q-1) W_dst
+    uint32_t toff = 0;
+    for (uint32_t g = 0; g < P.G; ++g) {
+        CHECK(eg_toff(E.egate[g]) == toff, "toff gate %u", g);
+        CHECK(eg_dst(E.egate[g]) == gate_dst(P.gate[g]) && eg_kind(E.egate[g]) == gate_kind(P.gate[g]) &&
+                  eg_coeff(E.egate[g]) == gate_coeff(P.gate[g]) && eg_tab(E.egate[g]) == gate_tab(P.gate[g]),
+              "egate %u", g);
+        toff += (P.mod[gate_src(P.gate[g])].m - 1) * P.mod[gate_dst(P.gate[g])].W;
+    }
+    uint64_t Pv = 1, sv = 1;
+    for (uint32_t i = 0; i < k; ++i) Pv *= moduli[i];
+    for (uint32_t a = 0; a < t; ++a) sv *= moduli[S[a]];
+    uint64_t r = seed * 0x9e3779b97f4a7c15ull + 1;
+    for (int trial = 0; trial < 64; ++trial) {
+        r ^= r << 13;
+        r ^= r >> 7;
+        r ^= r << 17;
+        const uint64_t x = (trial == 0) ? 0 : (trial == 1) ? Pv - 1 : r % Pv;  // x_up in [0, P)
+        const uint64_t y = x / sv;
+        uint32_t in[kMaxK], out[kMaxK], work[kMaxK];
+        for (uint32_t i = 0; i < k; ++i) {
+            in[i] = static_cast<uint32_t>(x % moduli[i]);
+            out[i] = kPoison;
+            work[i] = kPoison;
+        }
+        for (uint32_t b = 0; b < E.nblocks; ++b) {
+            const uint32_t bd = E.block[b];
+            uint32_t slot[2] = {bk_in0(bd) ? in[bk_mod0(bd)] : 0u, 0u};
+            uint32_t smod[2] = {bk_mod0(bd), bk_two(bd) ? bk_mod1(bd) : 99u};
+            if (bk_two(bd)) slot[1] = bk_in1(bd) ? in[bk_mod1(bd)] : 0u;
+            for (uint32_t st = bk_first(bd); st < bk_first(bd) + bk_steps(bd); ++st) {
+                const uint32_t sd = E.step[st];
+                const uint32_t dm = st_dmod(sd);
+                uint32_t v = kPoison;
+                switch (st_dloc(sd)) {
+                    case kDigIn: v = in[dm]; break;
+                    case kDigOut: v = out[dm]; break;
+                    case kDigWork: v = work[dm]; break;
+                    default: v = (smod[0] == dm) ? slot[0] : kPoison; break;
+                }
+                CHECK(v < moduli[dm], "k=%u t=%u step %u reads an unset digit label (loc %u)", k, t, st, st_dloc(sd));
+                if (v >= moduli[dm]) return;
+                const uint32_t ng = st_two(sd) ? 2 : 1;
+                for (uint32_t j = 0; j < ng; ++j) {
+                    const uint32_t g = st_gate(sd) + j;
+                    const uint32_t sl = st_two(sd) ? j : st_slot1(sd);
+                    const uint32_t e = E.egate[g];
+                    CHECK(gate_src(P.gate[g]) == dm, "step %u gate %u digit modulus", st, g);
+                    CHECK(eg_dst(e) == smod[sl], "step %u gate %u goes to slot %u's modulus", st, g, sl);
+                    const uint32_t m = moduli[eg_dst(e)];
+                    const uint64_t E1 = v % m, c = eg_coeff(e);
+                    slot[sl] = eg_kind(e) ? static_cast<uint32_t>((slot[sl] + c * E1) % m)
+                                          : static_cast<uint32_t>((c * ((slot[sl] + m - E1) % m)) % m);
+                }
+                const uint32_t f = st_store(sd);
+                if (f & 1u) out[smod[0]] = slot[0];
+                if (f & 2u) work[smod[0]] = slot[0];
+                if (f & 4u) out[smod[1]] = slot[1];
+                if (f & 8u) work[smod[1]] = slot[1];
+            }
+        }
+        for (uint32_t i = 0; i < k; ++i)
+            CHECK(out[i] == y % moduli[i], "k=%u t=%u x_up=%llu modulus %u: %u, floor(x_up/s) mod m = %llu", k, t,
+                  static_cast<unsigned long long>(x), moduli[i], out[i],
+                  static_cast<unsigned long long>(y % moduli[i]));
+    }
+}
+
+static void check_schedules() {
+    static const uint32_t primes[15] = {2, 3, 5, 7, 11, 13, 17, 19, 23, 29, 31, 37, 41, 43, 47};
+    long before = checked;
+    // the workloads' bases
+    {
+        const uint32_t S1[] = {4};
+        check_schedule(primes, 5, S1, 1, 1);
+        const uint32_t S2[] = {7};
+        check_schedule(primes, 8, S2, 1, 2);
+        const uint32_t S3[] = {8, 9};
+        check_schedule(primes, 10, S3, 2, 3);
+        const uint32_t S4[] = {11};
+        check_schedule(primes, 12, S4, 1, 4);
+        const uint32_t S5[] = {10, 11};
+        check_schedule(primes, 12, S5, 2, 5);
+        const uint32_t S6[] = {9};
+        check_schedule(primes, 12, S6, 1, 6);
+        const uint32_t f[] = {32, 167, 173}, F[] = {32, 97, 107}, S0[] = {0};
+        check_schedule(f, 3, S0, 1, 7);
+        check_schedule(F, 3, S0, 1, 8);
+        const uint32_t c8[] = {3, 5, 7, 8, 11, 13, 17, 19}, S8[] = {3};
+        check_schedule(c8, 8, S8, 1, 9);
+    }
+    // every scale set of small bases, and random ones of up to 15 primes
+    for (uint32_t k = 2; k <= 6; ++k)
+        for (uint32_t mask = 1; mask + 1 < (1u << k); ++mask) {
+            uint32_t S[16], t = 0;
+            for (uint32_t i = 0; i < k; ++i)
+                if (mask & (1u << i)) S[t++] = i;
+            check_schedule(primes, k, S, t, mask * 31 + k);
+        }
+    uint64_t r = 12345;
+    for (int trial = 0; trial < 400; ++trial) {
+        r = r * 6364136223846793005ull + 1442695040888963407ull;
+        uint32_t k = 2 + static_cast<uint32_t>((r >> 33) % 14);  // 2..15
+        uint64_t P = 1;
+        for (uint32_t i = 0; i < k; ++i) P *= primes[i];
+        if (P >= (1ull << 63)) k = 14;
+        uint32_t S[16], t = 0;
+        for (uint32_t i = 0; i < k; ++i)
+            if ((r >> (i + 3)) & 1u) S[t++] = i;
+        if (t == 0) S[t++] = k - 1;
+        if (t == k) --t;
+        check_schedule(primes, k, S, t, r);
+    }
+    printf("schedules: %ld checks\n", checked - before);
+}
+
 int main() {
+    check_schedules();
     int accepted = 0, fast = 0;
     for (uint32_t m = 0; m <= 300; ++m) {
         const bool ok = modulus_ok(m);
