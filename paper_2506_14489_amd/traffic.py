@@ -29,9 +29,9 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 15211511.8,  # mean of four dispatches: 15,208,608 .. 15,212,628
-        "write_kib": 5049873.1,  # mean of four dispatches: 5,049,740 .. 5,049,962
-        "sources_sha256": "439a7afcc1a8863f2006fbb63c9176793600b17a644fcddf8cf2e10afb67447a",
+        "fetch_kib": 13309405.2,  # mean of four dispatches: 13,306,211 .. 13,311,067
+        "write_kib": 2271030.5,  # mean of four dispatches: 2,270,958 .. 2,271,093
+        "sources_sha256": "b49fe3564c4ea1cc9d5a7682cdf6b329346501f426a8e588100ff4ff5e037895",
     },
 }
 
