@@ -35,17 +35,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, x, sample: int, target_s: float):
+def oracle_rate(w, x, sample: int, target_s: float):
     """The CPU oracle's evaluation, single-threaded, on the first `sample`
-    gadgets of the workload (garbled by the oracle, untimed), repeated until
-    about target_s seconds have been timed."""
+    gadgets of workload w (garbled by the oracle, untimed), repeated until
+    about target_s seconds have been timed; checked by decode afterwards.
+    Returns (gadgets/s, passes, seconds timed)."""
     from oracle import oracle as O
 
     op = O.make_params(list(w.moduli), list(w.scale_idx), sample, w.seed)
     t0 = time.time()
     offs, zin, zout, tab = O.garble(op, 0, sample)
     X = O.encode(op, x[:sample], zin, offs)
-    log(f"cpu baseline: oracle garbled {sample} gadgets in {time.time() - t0:.1f} s")
+    log(f"cpu baseline: oracle garbled {sample} gadgets of {w.name} in {time.time() - t0:.1f} s")
     reps, elapsed = 0, 0.0
     while elapsed < target_s:
         t1 = time.perf_counter()
@@ -54,8 +55,18 @@ def cpu_baseline(w, x, sample: int, target_s: float):
         reps += 1
     y, bad = O.decode(op, Y, zout, offs)
     assert bad.sum() == 0 and np.array_equal(y, expected_values(w, x[:sample]))
-    return {
-        "value": round(sample * reps / elapsed, 1),
+    return sample * reps / elapsed, reps, elapsed
+
+
+def cpu_baseline(w, x, sample: int, target_s: float, slices: bool = True):
+    """The oracle's evaluation rate on the benchmark workload (a slice of its
+    first gadgets; gadgets are independent, so the rate carries over), and on
+    slices of the other workloads: the tiny and dense ones whole, the first
+    gadgets of the conv map and of three ResNet-18 layers (the stem, a layer-4
+    conv scaled by 31 x 37, the fc layer)."""
+    rate, reps, elapsed = oracle_rate(w, x, sample, target_s)
+    out = {
+        "value": round(rate, 1),
         "unit": "gadgets/s",
         "cores": 1,
         "kind": "oracle",
@@ -63,6 +74,19 @@ def cpu_baseline(w, x, sample: int, target_s: float):
                   f"(oracle-garbled tables), {reps} passes, {elapsed:.1f} s timed; plain C, one thread; "
                   f"host has {len(os.sched_getaffinity(0))} cores available",
     }
+    if slices:
+        from paper_2506_14489_amd import workloads as WL
+
+        plan = [(WL.TINY, 1024), (WL.DENSE, 4096), (WL.CONV, 2048),
+                (WL.by_name("resnet18.stem"), 1024), (WL.by_name("resnet18.l4.1.b"), 1024),
+                (WL.by_name("resnet18.fc"), 1000)]
+        out["slices"] = []
+        for sw, count in plan:
+            sx = WL.make_inputs(sw)
+            r, k, t = oracle_rate(sw, sx, count, max(target_s / 6, 1.0))
+            out["slices"].append({"workload": sw.name, "gadgets": count, "of": sw.n, "value": round(r, 1),
+                                  "unit": "gadgets/s", "passes": k, "seconds": round(t, 2)})
+    return out
 
 
 def expected_values(w, x):
@@ -254,6 +278,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-slices", action="store_true", help="time the oracle on the benchmark workload only")
     ap.add_argument("--no-check", action="store_true", help="skip the decode check after timing")
     ap.add_argument("--garble-steps", type=int, default=3,
                     help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
@@ -456,7 +481,8 @@ def main():
     if not args.no_resnet18:
         result["resnet18"] = time_resnet18(max(args.steps // 2, 1), args.warmup, dev)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds,
+                                              slices=not args.no_cpu_slices)
     print(json.dumps(result), flush=True)
 
 

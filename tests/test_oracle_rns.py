@@ -205,6 +205,28 @@ def test_gadget_rounding_brute_force(base, S):
         assert rns.plain_scale(x, base, S) == (x + r) // s, (x, base, S)
 
 
+@pytest.mark.parametrize("base,S", ROUNDING_CASES)
+def test_no_shift_gives_floor_on_the_whole_signed_range(base, S):
+    """The alternative reading weighed against the kept one: a ShiftUp U that
+    is a multiple of s (U = s floor(floor(P/2)/s), ShiftDown U/s) makes the
+    gadget's floor((x_up)/s) - U/s exactly floor(x/s) -- but only where
+    x + U stays in [0, P): the r = floor(P/2) mod s most negative inputs of
+    the signed range wrap.  And no shift at all keeps the whole signed range
+    in [0, P) except U = floor(P/2): so when r > 0 a gadget either rounds
+    (the kept reading) or wraps r inputs."""
+    P = rns.cardinality(base)
+    s = rns.cardinality([base[i] for i in S])
+    r = rns.rounding_offset(base, S)
+    lo, hi = -(P // 2), P - P // 2 - 1
+    assert [U for U in range(P) if lo + U >= 0 and hi + U < P] == [P // 2]
+    U = s * ((P // 2) // s)
+    bad = [x for x in range(lo, hi + 1) if ((x + U) % P) // s - U // s != x // s]
+    assert bad == list(range(lo, lo + r))
+    # the kept reading: exact on every x of the range, floor((x + r)/s)
+    if r:
+        assert any((x + r) // s != x // s for x in range(lo, hi + 1))
+
+
 def test_round_half_up_for_half_offset():
     """With r = s/2 (a 2^l modulus scaled by, Sec. 4's bases) the gadget rounds
     x/s to the nearest integer, halves upward."""
