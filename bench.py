@@ -249,6 +249,32 @@ def time_resnet18(steps: int, warmup: int, dev):
     }
 
 
+def aes_rate(dev, bitsliced: bool = False, count: int = 1 << 28, reps: int = 5) -> float:
+    """AES blocks/s of a bare AES kernel (counter mode under the hash key):
+    the evaluator's two-table LDS round code, four blocks per lane, or the
+    bitsliced AES, 32 blocks per lane."""
+    import torch
+
+    from paper_2506_14489_amd import binding as B
+
+    run = B.redash_aes_ctr_bitsliced if bitsliced else B.redash_aes_ctr
+    out = torch.empty(4 * count, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    run(count, 0, out, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        run(count, 0, out, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del out
+    torch.cuda.empty_cache()
+    log(f"aes ({'bitsliced' if bitsliced else 'round tables'}): {count} blocks in {ms:.3f} ms, "
+        f"{count / (ms / 1e3):.3e} blocks/s")
+    return count / (ms / 1e3)
+
+
 def copy_bandwidth(dev, mib: int = 2048, reps: int = 5) -> float:
     """GB/s of a device-to-device copy (bytes read + bytes written)."""
     import torch
@@ -408,6 +434,8 @@ def main():
     gadgets_per_s = n / (ms_step / 1e3)
     copy_gbs = copy_bandwidth(dev)
     log(f"device-to-device copy: {copy_gbs:.1f} GB/s (read + write)")
+    aes_peak = aes_rate(dev)
+    aes_bs = aes_rate(dev, bitsliced=True)
     bytes_g = cost.bytes_per_gadget(w.moduli, w.scale_idx)
     ops_g = cost.ops_per_gadget(w.moduli, w.scale_idx)
     lds_g = cost.lds_bytes_per_gadget(w.moduli, w.scale_idx)
@@ -466,6 +494,14 @@ def main():
             "bytes_per_gadget": lds_g,
         },
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
+        "aes_roofline": {"achieved": round(aes_g * gadgets_per_s, 1), "peak": round(aes_peak, 1),
+                         "unit": "AES blocks/s", "frac": round(aes_g * gadgets_per_s / aes_peak, 4),
+                         "kernel": "k_eval",
+                         "peak_kernel": "k_aes_ctr: the evaluator's AES alone (two-table LDS rounds, "
+                                        "four blocks per lane, counter mode)",
+                         "bitsliced_blocks_per_s": round(aes_bs, 1),
+                         "bitsliced_kernel": "k_aes_ctr_bs: bitsliced AES, 32 blocks per lane, Boyar-Peralta "
+                                             "S-box, counter mode"},
         "ms_median_per_call": round(ms_median, 4),
         "check": check,
         "garble": garble,

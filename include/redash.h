@@ -240,7 +240,7 @@ int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const ui
 
 /*
  * The projection-gate hash alone (Sec. 2.3; construction in the conventions
- * above), for tests and for measuring the AES throughput of the device.
+ * above), for tests.
  *   q, m        input and output modulus (2..255, prime or a power of two).
  *   count       number of labels.
  *   d_labels    W_q * count words, SoA: word w of label a at w * count + a.
@@ -250,6 +250,26 @@ int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const ui
  */
 int redash_hash_labels(uint32_t q, uint32_t m, uint64_t count, const uint32_t *d_labels,
                        uint32_t gadget_id, const uint64_t *d_tau, uint32_t *d_out, hipStream_t stream);
+
+/*
+ * The AES of the projection-gate hash alone, for measuring the device's AES
+ * rate with the evaluator's round-table code (Sec. 2.3 leaves the hash to the
+ * implementation; the conventions above fix AES-128 under K = 00 01 .. 0f):
+ * counter mode, d_out[4i .. 4i+3] = AES_K(c0 + i) for i < count, the counter
+ * block being the 128-bit little-endian integer c0 + i and each output block
+ * four little-endian words.
+ *   count   number of blocks, at most 2^40 (else REDASH_E_PARAM).
+ *   d_out   4 * count words, written.
+ */
+int redash_aes_ctr(uint64_t count, uint64_t c0, uint32_t *d_out, hipStream_t stream);
+
+/*
+ * The same counter-mode output as redash_aes_ctr from a bitsliced AES-128 (32
+ * blocks per 32-bit lane word, the S-box as the Boyar-Peralta circuit, no
+ * table lookups), to compare the two formulations' rates on the device.
+ * Same arguments, layout and return codes.
+ */
+int redash_aes_ctr_bitsliced(uint64_t count, uint64_t c0, uint32_t *d_out, hipStream_t stream);
 
 /* Static text for a return code. */
 const char *redash_strerror(int code);

@@ -141,6 +141,8 @@ def lib() -> ctypes.CDLL:
         L.redash_decode.argtypes = [pp, vp, vp, vp, vp, vp, vp]
         L.redash_hash_labels.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, vp, ctypes.c_uint32,
                                          vp, vp, vp]
+        L.redash_aes_ctr.argtypes = [ctypes.c_uint64, ctypes.c_uint64, vp, vp]
+        L.redash_aes_ctr_bitsliced.argtypes = [ctypes.c_uint64, ctypes.c_uint64, vp, vp]
         L.redash_strerror.argtypes = [ctypes.c_int]
         L.redash_strerror.restype = ctypes.c_char_p
         lp = ctypes.POINTER(LinearParams)
@@ -150,7 +152,7 @@ def lib() -> ctypes.CDLL:
         L.redash_linear_garble.argtypes = [lp, vp, vp, vp, vp, vp, vp, vp]
         for name in ("redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale",
                      "redash_eval_scale_noalloc", "redash_decode",
-                     "redash_hash_labels", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
+                     "redash_hash_labels", "redash_aes_ctr", "redash_aes_ctr_bitsliced", "redash_linear_plan", "redash_linear_prepare", "redash_linear_eval",
                      "redash_linear_garble"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -290,6 +292,22 @@ def redash_hash_labels(q, m, count, labels, gadget_id, tau, out, stream=None):
         int(q), int(m), int(count), _ptr(labels, torch.int32, wq * count, "labels"), int(gadget_id) & 0xFFFFFFFF,
         _ptr(tau, torch.int64, count, "tau"), _ptr(out, torch.int32, wm * count, "out"), _stream(stream)),
         "redash_hash_labels")
+
+
+def redash_aes_ctr(count, c0, out, stream=None):
+    """AES-128 under the hash key in counter mode (the device's AES rate)."""
+    import torch
+
+    _check(lib().redash_aes_ctr(int(count), int(c0), _ptr(out, torch.int32, 4 * count, "out"), _stream(stream)),
+           "redash_aes_ctr")
+
+
+def redash_aes_ctr_bitsliced(count, c0, out, stream=None):
+    """redash_aes_ctr from the bitsliced AES (the device's AES rate without tables)."""
+    import torch
+
+    _check(lib().redash_aes_ctr_bitsliced(int(count), int(c0), _ptr(out, torch.int32, 4 * count, "out"),
+                                          _stream(stream)), "redash_aes_ctr_bitsliced")
 
 
 def redash_linear_plan(params: LinearParams) -> dict:

@@ -14,8 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libredash.so")
-SOURCES = [os.path.join(CSRC, "redash.hip"), os.path.join(CSRC, "linear.hip"), os.path.join(CSRC, "plan.cpp")]
-HEADERS = [os.path.join(CSRC, f) for f in ("aes_tables.hpp", "device.hpp", "plan.hpp")] + [
+SOURCES = [os.path.join(CSRC, "redash.hip"), os.path.join(CSRC, "linear.hip"), os.path.join(CSRC, "aes_rate.hip"),
+           os.path.join(CSRC, "plan.cpp")]
+HEADERS = [os.path.join(CSRC, f) for f in ("aes_tables.hpp", "aes_bitslice.hpp", "device.hpp", "plan.hpp")] + [
     os.path.join(ROOT, "include", "redash.h")
 ]
 

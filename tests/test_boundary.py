@@ -17,7 +17,7 @@ from paper_2506_14489_amd import workloads as WL
 def test_library_exports_every_declared_symbol():
     names = B.declared_symbols()
     assert set(names) == {"redash_plan", "redash_garble_scale", "redash_garble_scale_given", "redash_encode", "redash_eval_scale",
-                          "redash_eval_scale_noalloc", "redash_decode", "redash_hash_labels", "redash_strerror", "redash_linear_plan",
+                          "redash_eval_scale_noalloc", "redash_decode", "redash_hash_labels", "redash_aes_ctr", "redash_aes_ctr_bitsliced", "redash_strerror", "redash_linear_plan",
                           "redash_linear_prepare", "redash_linear_eval", "redash_linear_garble"}
     L = B.lib()
     for n in names:
@@ -170,6 +170,12 @@ def test_entry_points_validate_before_any_device_work():
     assert L.redash_eval_scale_noalloc(ctypes.byref(good), fake, None, fake, None) == B.REDASH_E_NULL
     assert L.redash_eval_scale_noalloc(ctypes.byref(good), fake, fake, None, None) == B.REDASH_E_NULL
     assert L.redash_eval_scale_noalloc(None, fake, fake, fake, None) == B.REDASH_E_NULL
+    assert L.redash_aes_ctr(0, 0, None, None) == B.REDASH_OK
+    assert L.redash_aes_ctr(5, 0, None, None) == B.REDASH_E_NULL
+    assert L.redash_aes_ctr((1 << 40) + 1, 0, fake, None) == B.REDASH_E_PARAM
+    assert L.redash_aes_ctr_bitsliced(0, 0, None, None) == B.REDASH_OK
+    assert L.redash_aes_ctr_bitsliced(5, 0, None, None) == B.REDASH_E_NULL
+    assert L.redash_aes_ctr_bitsliced((1 << 40) + 1, 0, fake, None) == B.REDASH_E_PARAM
 
 
 def test_noalloc_size_limit():

@@ -107,6 +107,23 @@ def test_hash_known_answers():
     assert done >= 100
 
 
+@pytest.mark.parametrize("bitsliced", [False, True])
+def test_aes_ctr_matches_oracle(bitsliced):
+    """The bare AES kernels (counter mode under the hash key; round tables,
+    and bitsliced) against the oracle's FIPS-197 AES, including ragged tails
+    and a counter that carries into bit 64."""
+    key = bytes(range(16))
+    run = B.redash_aes_ctr_bitsliced if bitsliced else B.redash_aes_ctr
+    for count, c0 in ((1000, 0), (4099, 2 ** 64 - 2050), (7, 12345), (70000, 2 ** 63 + 5)):
+        out = torch.empty(4 * count, dtype=torch.int32, device="cuda")
+        run(count, c0, out)
+        got = H.to_u32(out).reshape(count, 4)
+        for i in list(range(min(count, 300))) + list(range(max(count - 300, 0), count)):
+            block = ((c0 + i) % 2 ** 128).to_bytes(16, "little")
+            want = np.frombuffer(O.aes128(key, block), dtype="<u4")
+            assert np.array_equal(got[i], want), (count, c0, i)
+
+
 # ---------------------------------------------------------------------------
 # small cases: garble, encode, eval, decode, word for word
 # ---------------------------------------------------------------------------

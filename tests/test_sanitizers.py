@@ -5,7 +5,10 @@
   extreme arguments) on eight small bases and checks every decode.
 * tests/plan_check.cpp checks every per-modulus constant of the library's
   host plan (plan.cpp) over the operand range the kernels use it on, for
-  every modulus the library accepts.
+  every modulus the library accepts, and runs the evaluator's target-major
+  schedule on values for many bases.
+* tests/aes_bitslice_check.cpp checks the bitsliced AES (S-box circuit,
+  rounds, transpose) against GF(2^8) arithmetic and a byte-level AES.
 
 Both are built with gcc/g++ (host code only; no GPU code is built here).
 """
@@ -55,3 +58,12 @@ def test_plan_constants_under_sanitizers(tmp_path):
     # 4, 16 and 41..61 take the evaluator's fast path
     assert "accepted 60 moduli, 52 on the fast path" in out, out
     assert "generic: 4 16 41 47 53 59 61\n" in out, out
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or not os.path.isdir("/opt/rocm/include"),
+                    reason="needs g++ and the HIP headers")
+def test_bitsliced_aes_under_sanitizers(tmp_path):
+    exe = str(tmp_path / "aes_bitslice_check")
+    out = _run(["g++", "-std=c++17", *SAN, "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                os.path.join(HERE, "aes_bitslice_check.cpp"), "-o", exe], exe, tmp_path)
+    assert "aes bitslice check: 0 failures" in out, out
