@@ -322,19 +322,6 @@ int build_plan(const redash_params *p, Plan *pl) {
         if (g < kMaxTables && md.m > 2 && md.m <= kTableMaxModulus && md.fast) d |= 1u << 15;
     }
     pl->ntab = G < kMaxTables ? G : kMaxTables;
-    // Chunks: split every run of gates with one digit label into pieces of
-    // kMaxChunk gates (4 or 2), then 2s and 1s.
-    for (uint32_t g = 0; g < G;) {
-        uint32_t run = 1;
-        while (g + run < G && gate_src(pl->gate[g + run]) == gate_src(pl->gate[g])) ++run;
-        for (uint32_t done = 0; done < run;) {
-            const uint32_t left = run - done;
-            const uint32_t len = (left >= 4 && kMaxChunk >= 4) ? 4 : (left >= 2 ? 2 : 1);
-            pl->gate[g + done] |= len << 24;
-            done += len;
-        }
-        g += run;
-    }
     return REDASH_OK;
 }
 

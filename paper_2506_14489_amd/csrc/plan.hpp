@@ -76,12 +76,9 @@ struct ModConst {
 //   bits 0-3 src modulus index, 4-7 dst modulus index, 8 kind (0 sub, 1 acc),
 //   9 phase (0 A, 1 B), 10-11 where the destination label's current value
 //   is, 12 where its new value goes, 13-14 where the digit label is, 15 the
-//   gate's free operation uses a byte table (see below), 16-23 coefficient,
-//   24-26 chunk length.
-// A chunk is a run of up to kMaxChunk (a power of two) consecutive gates with
-// the same digit label (hence distinct destinations): the evaluator hashes
-// them together.  The chunk length is stored on the chunk's first gate and
-// is 0 elsewhere.
+//   gate's free operation uses a byte table (see below), 16-23 coefficient.
+// The locations are those of the gate-by-gate order (the garbler and the
+// split evaluator); the one-gadget-per-lane evaluator uses EvalPlan.
 constexpr uint32_t gate_src(uint32_t d) { return d & 15u; }
 constexpr uint32_t gate_dst(uint32_t d) { return (d >> 4) & 15u; }
 constexpr uint32_t gate_kind(uint32_t d) { return (d >> 8) & 1u; }
@@ -91,8 +88,6 @@ constexpr uint32_t gate_tdst(uint32_t d) { return (d >> 12) & 1u; }
 constexpr uint32_t gate_dsrc(uint32_t d) { return (d >> 13) & 3u; }
 constexpr uint32_t gate_tab(uint32_t d) { return (d >> 15) & 1u; }
 constexpr uint32_t gate_coeff(uint32_t d) { return (d >> 16) & 255u; }
-constexpr uint32_t gate_chunk(uint32_t d) { return (d >> 24) & 7u; }
-constexpr int kMaxChunk = 2;
 
 // Free-operation tables: gate g < ntab whose output modulus m satisfies
 // 2 < m <= kTableMaxModulus (and has the fast constants) gets 128 bytes of

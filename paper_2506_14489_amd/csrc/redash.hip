@@ -77,95 +77,6 @@ struct LabelBufs {
     }
 };
 
-// Moduli without the fast constants (4 and 16, whose fields fill a word, and
-// the primes 41, 47, 53, 59 and 61, whose split parts are too large for the
-// 24-bit digit steps): one residue at a time with 32-bit divisions, in
-// rolled loops; the gadget configurations in use all take the fast path.
-__device__ __forceinline__ void eval_update_generic(uint32_t d, const ModConst &mm, uint32_t (&V)[8],
-                                                    uint32_t (&row)[kMaxW], uint32_t (&tgt)[kMaxW],
-                                                    const LabelBufs &LB) {
-    const uint32_t coeff = gate_coeff(d);
-    uint32_t *dst = LB.dest(gate_tdst(d), mm);
-    for (uint32_t w = 0; w < mm.W; ++w) {
-        const bool last = (w + 1 == mm.W);
-        const uint32_t nres = last ? mm.glast : mm.g;
-        uint32_t D = frac_carry_any(V, last ? mm.pw_last : mm.pw_g);
-        const uint32_t rw = next_word(row);
-        const uint32_t l = next_word(tgt);
-        uint32_t res = 0;
-        // Digits come out least significant first: position nres-1 down to 0.
-        for (uint32_t j = nres; j-- > 0;) {
-            uint32_t pd;
-            if (j) {
-                const uint32_t qd = div_m(D, mm);
-                pd = D - qd * mm.m;
-                D = qd;
-            } else {
-                pd = D;
-            }
-            const uint32_t e = add_mod(pd, field(rw, j, mm), mm.m);
-            const uint32_t lj = field(l, j, mm);
-            const uint32_t r = gate_kind(d) == 0 ? mul_mod(coeff, sub_mod(lj, e, mm.m), mm)
-                                                 : add_mod(lj, mul_mod(coeff, e, mm), mm.m);
-            res |= r << (mm.b * j);
-        }
-        LB.put(dst, w, res);
-    }
-}
-
-// The fast path over all words of the destination label: full words in a
-// loop, the last word peeled, each with its own constants.
-template <bool TAB>
-__device__ __forceinline__ void eval_fast(uint32_t d, const ModConst &mm, uint32_t (&V)[8], uint32_t (&row)[kMaxW],
-                                          uint32_t (&tgt)[kMaxW], uint32_t *dst, const LabelBufs &LB, uint32_t tk) {
-    const uint32_t coeff = gate_coeff(d);
-    const bool acc = gate_kind(d) != 0;
-#pragma unroll 1
-    for (uint32_t w = 0; w + 1 < mm.W; ++w) {
-        const uint32_t l = next_word(tgt);
-        const uint32_t D = frac_mul_carry(V, mm.pw_g);
-        const uint32_t rw = next_word(row);
-        LB.put(dst, w,
-               acc ? fast_word_any<true, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f,
-                                              mm.fc_lo_f, rw, l, coeff, mm, tk)
-                   : fast_word_any<false, TAB>(D, mm.g, mm.nlo_f, mm.lo_M_f, mm.lo_s_f, mm.pw_lo_f, mm.fc_hi_f,
-                                               mm.fc_lo_f, rw, l, coeff, mm, tk));
-    }
-    const uint32_t l = tgt[0];
-    const uint32_t D = frac_mul_carry(V, mm.pw_last);
-    const uint32_t rw = row[0];
-    LB.put(dst, mm.W - 1,
-           acc ? fast_word_any<true, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l,
-                                          mm.fc_lo_l, rw, l, coeff, mm, tk)
-               : fast_word_any<false, TAB>(D, mm.glast, mm.nlo_l, mm.lo_M_l, mm.lo_s_l, mm.pw_lo_l, mm.fc_hi_l,
-                                           mm.fc_lo_l, rw, l, coeff, mm, tk));
-}
-
-// Applies gate g's free operation to its destination label (in tgt):
-// E = row + pad, then L <- c (L - E) (sub: division step and the recursion
-// of Eq. rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination
-// onto a scaling modulus), and stores the new label.
-__device__ __forceinline__ void eval_update(uint32_t g, uint32_t d, const ModConst &mm, uint32_t (&V)[8],
-                                            uint32_t (&row)[kMaxW], uint32_t (&tgt)[kMaxW], const LabelBufs &LB) {
-    uint32_t *dst = LB.dest(gate_tdst(d), mm);
-    if (mm.m == 2) {
-        const bool flip = gate_kind(d) == 0 || (gate_coeff(d) & 1u);  // sub: q^{-1} = 1 mod 2
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const uint32_t E = bits_word(V, w) ^ row[w];
-            LB.put(dst, w, flip ? tgt[w] ^ E : tgt[w]);
-        }
-    } else if (gate_tab(d)) {
-        // table address, plus 2m for a sub gate (its index is l + 2m - p - r)
-        const uint32_t tk = kEvalTableBase + g * kTableBytes + (gate_kind(d) ? 0u : mm.two_m);
-        eval_fast<true>(d, mm, V, row, tgt, dst, LB, tk);
-    } else if (mm.fast) {
-        eval_fast<false>(d, mm, V, row, tgt, dst, LB, 0);
-    } else {
-        eval_update_generic(d, mm, V, row, tgt, LB);
-    }
-}
-
 // Fills the free-operation tables (gates 0..ntab-1 that have one): byte v of
 // gate g's table is c (v mod m) mod m.  Wave w fills gates w, w + waves, ...
 __device__ __forceinline__ void stage_free_op_tables(const Plan &P, uint32_t *lds, int tid, uint32_t nwaves) {
@@ -182,58 +93,6 @@ __device__ __forceinline__ void stage_free_op_tables(const Plan &P, uint32_t *ld
         }
         lds[(kEvalTableBase + g * kTableBytes) / 4 + lane] = w;
     }
-}
-
-// Hashes the NG gates g..g+NG-1, which share one digit label: reads the
-// digit label, requests every gate's row (the colour is known before
-// hashing) and destination label, then runs the 2 NG AES blocks
-// interleaved.  Fills V, row and tgt for the NG gates.
-template <int NG>
-__device__ __forceinline__ void hash_chunk(const Plan &P, uint32_t g, uint64_t &toff, const PermTE02 &TT,
-                                           const uint32_t *K, const LabelBufs &LB, uint64_t a, uint64_t tau0,
-                                           const uint32_t *__restrict__ tab, uint32_t (&V)[kMaxChunk][8],
-                                           uint32_t (&row)[kMaxChunk][kMaxW], uint32_t (&tgt)[kMaxChunk][kMaxW]) {
-    const uint64_t n = P.n;
-    // Local copies of the modulus constants: the compiler keeps their fields
-    // in scalar registers (a pointer into the argument block could end up in
-    // vector registers and make every loop bound derived from it divergent).
-    const uint32_t d0 = P.gate[g];
-    const ModConst mq = P.mod[gate_src(d0)];
-    const uint32_t q = mq.m;
-    const uint32_t *dig = LB.base(gate_dsrc(d0), mq);
-    uint32_t x[4] = {LB.get(dig, 0), 0, 0, 0};
-    static_for<kMaxW - 1>([&](auto w1) {
-        constexpr int w = decltype(w1)::value + 1;
-        if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
-    });
-    // A residue >= q only occurs in a malformed input label; it selects the
-    // implicit zero row, the output is garbage and decode flags it.
-    uint32_t colour = LB.get(dig, 0) & mq.mask;
-    if (colour >= q) colour = 0;
-    static_for<NG>([&](auto j) {
-        const uint32_t dj = P.gate[g + j];
-        const ModConst &md = P.mod[gate_dst(dj)];
-        const uint32_t Wd = md.W;
-        static_for<kMaxW>([&](auto w) { row[j][w] = 0; });
-        if (colour != 0) {
-            const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * Wd;
-            static_for<kMaxW>([&](auto w) {
-                if (w < static_cast<int>(Wd)) row[j][w] = rp[w];
-            });
-        }
-        toff += n * (q - 1) * Wd;
-        static_for<kMaxW>([&](auto w) { tgt[j][w] = 0; });
-        const uint32_t tsrc = gate_tsrc(dj);
-        if (tsrc != kLocZero) {
-            const uint32_t *tp = LB.base(tsrc, md);
-            static_for<kMaxW>([&](auto w) {
-                if (w < static_cast<int>(Wd)) tgt[j][w] = LB.get(tp, w);
-            });
-        }
-    });
-    uint32_t Vn[NG][8];
-    hash_fraction_n<NG>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g, P.gid, Vn);
-    static_for<NG>([&](auto j) { static_for<8>([&](auto l) { V[j][l] = Vn[j][l]; }); });
 }
 
 // ---------------------------------------------------------------------------
@@ -287,9 +146,12 @@ __device__ __forceinline__ void fold_regs(const uint32_t (&T)[kMaxW], uint32_t (
     static_for<kMaxW - OFF>([&](auto w) { x[w & 3] ^= T[w + OFF]; });
 }
 
-// Generic moduli (see eval_update_generic): all kMaxW positions in a rolled
-// loop that rotates the label and the row by one word per position (kMaxW
-// rotations put both back in place).
+// Moduli without the fast constants (4 and 16, whose fields fill a word, and
+// the primes 41, 47, 53, 59 and 61, whose split parts are too large for the
+// 24-bit digit steps): one residue at a time with 32-bit divisions, over all
+// kMaxW positions in a rolled loop that rotates the label and the row by one
+// word per position (kMaxW rotations put both back in place).  The gadget
+// configurations in use all take the fast path.
 __device__ __forceinline__ void reg_update_generic(uint32_t e, const ModConst &mm, uint32_t (&V)[8],
                                                    uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW]) {
     const uint32_t coeff = eg_coeff(e), off = label_off(mm);
@@ -367,7 +229,12 @@ __device__ __forceinline__ void reg_update_fast(uint32_t e, const ModConst &mm, 
                                            mm.fc_lo_l, row[kMaxW - 1], T[kMaxW - 1], coeff, mm, tk);
 }
 
-// Gate g's free operation on the register label T (see eval_update).
+// Applies gate g's free operation to the register label T: E = row + pad,
+// then L <- c (L - E) (sub: division step and the recursion of Eq.
+// rns_to_mrs) or L <- L + c E (acc: the mixed-radix recombination onto a
+// scaling modulus).  For an output modulus m <= 42 the product c (v mod m)
+// mod m comes from the gate's byte table in LDS: a sub gate's new residue is
+// T[l + 2m - p - r], an acc gate's is l + T[p + r] reduced once.
 __device__ __forceinline__ void reg_update(uint32_t g, uint32_t e, const ModConst &mm, uint32_t (&V)[8],
                                            uint32_t (&row)[kMaxW], uint32_t (&T)[kMaxW]) {
     if (mm.m == 2) {  // W = 4: positions 2..5
@@ -565,14 +432,40 @@ k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__re
         while (g + r < P.G && gate_src(P.gate[g + r]) == src) ++r;
         for (uint32_t i = 0; i < r; ++i) {
             const uint32_t d = P.gate[g + i];
+            const ModConst mq = P.mod[src];
+            const uint32_t q = mq.m;
             if (i % SPLIT == part && live) {
-                uint64_t t = toff;
-                uint32_t V[kMaxChunk][8], row[kMaxChunk][kMaxW], tgt[kMaxChunk][kMaxW];
-                hash_chunk<1>(P, g + i, t, TT, K, LB, a, tau0, tab, V, row, tgt);
+                // the digit label: fold and colour (see k_eval)
+                const uint32_t *dig = LB.base(gate_dsrc(d), mq);
+                const uint32_t w0 = LB.get(dig, 0);
+                uint32_t x[4] = {w0, 0, 0, 0};
+                static_for<kMaxW - 1>([&](auto w1) {
+                    constexpr int w = decltype(w1)::value + 1;
+                    if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
+                });
+                uint32_t colour = w0 & mq.mask;
+                if (colour >= q) colour = 0;
                 const ModConst mm = P.mod[gate_dst(d)];
-                eval_update(g + i, d, mm, V[0], row[0], tgt[0], LB);
+                const uint32_t Wd = mm.W;
+                // the row (right-aligned, as the register labels)
+                uint32_t row[kMaxW];
+                static_for<kMaxW>([&](auto p) { row[p] = 0; });
+                if (colour != 0) {
+                    const uint32_t *rp = tab + toff + (a * (q - 1) + (colour - 1)) * Wd;
+                    const int off = kMaxW - static_cast<int>(Wd);
+                    static_for<kMaxW>([&](auto p) {
+                        if (p >= off) row[p] = rp[p - off];
+                    });
+                }
+                uint32_t T[kMaxW];
+                load_label(T, LB, gate_tsrc(d), mm, gate_tsrc(d) != kLocZero);
+                uint32_t Vn[1][8];
+                hash_fraction_n<1>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g + i, P.gid, Vn);
+                const uint32_t e = gate_dst(d) | (gate_kind(d) << 4) | (gate_tab(d) << 5) | (gate_coeff(d) << 6);
+                reg_update(g + i, e, mm, Vn[0], row, T);
+                store_label(T, LB, gate_tdst(d), mm);
             }
-            toff += P.n * (P.mod[gate_src(d)].m - 1) * P.mod[gate_dst(d)].W;
+            toff += P.n * (q - 1) * P.mod[gate_dst(d)].W;
         }
         __syncthreads();
         g += r;
