@@ -444,6 +444,7 @@ def main():
     achieved_gbs = bytes_g * n / (ms_step / 1e3) / 1e9
     # HBM bytes per launch from the rocprofv3 counters (None once the kernel changed)
     traffic_b = traffic.traffic_bytes(w.name)
+    valu_i = traffic.valu_instructions(w.name)
     result = {
         "metric": METRIC,
         "value": round(gadgets_per_s, 1),
@@ -493,6 +494,11 @@ def main():
             "frac": round(lds_g * n / (ms_step / 1e3) / 1e9 / LDS_PEAK_GBS, 4),
             "bytes_per_gadget": lds_g,
         },
+        # measured VALU issue: SQ_INSTS_VALU x 4 cycles per wave64 instruction on a 16-lane SIMD,
+        # against 1,024 SIMDs x 2.4 GHz over the launch (None once the kernel changed)
+        "valu_issue": {"instructions_per_launch": valu_i,
+                       "frac": None if valu_i is None else round(valu_i * 4 / (1024 * 2.4e9 * ms_step / 1e3), 4),
+                       "source": "rocprofv3 SQ_INSTS_VALU"},
         "aes_blocks_per_s": round(aes_g * gadgets_per_s, 1),
         "aes_roofline": {"achieved": round(aes_g * gadgets_per_s, 1), "peak": round(aes_peak, 1),
                          "unit": "AES blocks/s", "frac": round(aes_g * gadgets_per_s / aes_peak, 4),

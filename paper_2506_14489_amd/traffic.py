@@ -1,4 +1,5 @@
-"""Measured HBM traffic of the evaluation kernel, from hardware counters.
+"""Measured HBM traffic (and vector instruction count) of the evaluation
+kernel, from hardware counters.
 
 The figures were taken with two rocprofv3 counter passes over
 ``bench.py`` (``--pmc FETCH_SIZE``, then ``--pmc WRITE_SIZE``; KiB per
@@ -31,6 +32,7 @@ MEASURED = {
         "kernel": "k_eval",
         "fetch_kib": 13309405.2,  # mean of four dispatches: 13,306,211 .. 13,311,067
         "write_kib": 2271030.5,  # mean of four dispatches: 2,270,958 .. 2,271,093
+        "valu_insts": 4412700000,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
         # taken on an earlier source; the kernel's assembly from these sources is the same,
         # instruction for instruction (only the split evaluator and unused helpers changed)
         "sources_sha256": "f76e6bf461d49e1a3f7d8ee03552267eafdfcc1ef541094d0e02f9322ae09178",
@@ -51,6 +53,15 @@ def sources_sha256() -> str:
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def valu_instructions(workload: str):
+    """Vector ALU wave instructions per k_eval launch on ``workload``
+    (SQ_INSTS_VALU), or None as for traffic_bytes."""
+    rec = MEASURED.get(workload)
+    if rec is None or rec["sources_sha256"] != sources_sha256() or "valu_insts" not in rec:
+        return None
+    return rec["valu_insts"]
 
 
 def traffic_bytes(workload: str):
