@@ -127,15 +127,24 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     Y = torch.empty(sz["out_label_words"], dtype=torch.int32, device=dev)
     Z = torch.empty_like(Y)
     B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
-    for _ in range(warmup):
-        B.redash_linear_eval(lp, X, prep, work, Y, stream)
     gc.collect()
+    t_w, done = time.perf_counter(), 0  # as time_workload: at least `warmup` calls and 50 ms
+    while done < warmup or time.perf_counter() - t_w < 0.05:
+        B.redash_linear_eval(lp, X, prep, work, Y, stream)
+        done += 1
+        if done % 8 == 0:
+            torch.cuda.synchronize()
+    # An event recorded behind a still-running kernel is stamped when that kernel
+    # starts (measured: 10 calls timed that way take 11 calls' time), so the
+    # warm-up calls are waited for before the first event.
+    torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     for _ in range(steps):
         B.redash_linear_eval(lp, X, prep, work, Y, stream)
     ev1.record(stream)
+    torch.cuda.synchronize()
     g0 = torch.cuda.Event(enable_timing=True)
     g1 = torch.cuda.Event(enable_timing=True)
     g0.record(stream)
@@ -188,9 +197,22 @@ def time_workload(w, steps: int, warmup: int, dev, values: str = "values uniform
     stream = torch.cuda.current_stream()
     B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work, stream)
     B.redash_encode(params, torch.from_numpy(x).to(dev), buf.in_zero, buf.offsets, buf.in_labels, stream)
-    for _ in range(warmup):
+    gc.collect()
+    # Warm-up: at least `warmup` calls and at least 50 ms of them.  After the CPU
+    # has built a layer's inputs the GPU has been idle and a short call gets
+    # faster over its first ~30 repetitions (measured: a 200,704-gadget layer
+    # from 0.81 to 0.74 ms per call), so a fixed count of a few calls would time
+    # small layers on a GPU that has not come back up to speed.
+    t_w, done = time.perf_counter(), 0
+    while done < warmup or time.perf_counter() - t_w < 0.05:
         B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
-    gc.collect()  # no collector pause while the calls are queued
+        done += 1
+        if done % 8 == 0:
+            torch.cuda.synchronize()
+    # An event recorded behind a still-running kernel is stamped when that kernel
+    # starts (measured: 10 calls timed that way take 11 calls' time), so the
+    # warm-up calls are waited for before the first event.
+    torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
@@ -261,6 +283,7 @@ def aes_rate(dev, bitsliced: bool = False, count: int = 1 << 28, reps: int = 5) 
     out = torch.empty(4 * count, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream()
     run(count, 0, out, stream)
+    torch.cuda.synchronize()  # (see time_workload: no event behind a running kernel)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(reps):
@@ -282,6 +305,7 @@ def copy_bandwidth(dev, mib: int = 2048, reps: int = 5) -> float:
     src = torch.ones(mib * (1 << 20) // 4, dtype=torch.int32, device=dev)
     dst = torch.empty_like(src)
     dst.copy_(src)
+    torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
@@ -394,9 +418,9 @@ def main():
         }
         log(f"garble: {g_ms:.3f} ms per call")
 
+    gc.collect()
     for _ in range(args.warmup):
         B.redash_eval_scale(params, buf.in_labels, buf.tables, buf.out_labels, buf.work, stream)
-    gc.collect()
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
