@@ -416,6 +416,31 @@ def test_evaluator_launch_thresholds(rounds, per, extra):
     _check_full(w, 4096, 4096, 8192)
 
 
+# Bases beyond the workloads' on the one-gadget-per-lane evaluator (its target-major
+# schedule differs with k, t and the moduli: product scaling, 15 moduli, odd P,
+# powers of two among the remaining moduli, moduli on the generic and the
+# no-table fast paths): one gadget past the two-wave split's last call size.
+K_EVAL_BASES = [
+    ("k15-product", tuple(rns.first_primes(15)), (13, 14)),
+    ("conv-base", tuple(WL.PRIMES_12[:10]), (8, 9)),
+    ("generic-47-53-59", (2, 47, 53, 59), (1, 3)),
+    ("large-moduli", (2, 97, 251), (2,)),
+    ("pow2-128-product", (3, 128, 251), (0, 1)),
+    ("pow2-4-remaining", (4, 5, 7), (1,)),
+    ("odd-P", (3, 5, 7, 11, 13), (0, 4)),
+    ("k2", (2, 3), (1,)),
+]
+
+
+@pytest.mark.parametrize("name,moduli,S", K_EVAL_BASES, ids=[b[0] for b in K_EVAL_BASES])
+def test_one_gadget_per_lane_on_varied_bases(name, moduli, S):
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 2 * cus * 384 + 1
+    P = rns.cardinality(moduli)
+    w = WL.Workload(f"lane-{name}", tuple(moduli), tuple(S), n, 70 + len(moduli), "uniform", -(P // 2), P - P // 2)
+    _check_full(w, 2048, 2048, 2048, 8)
+
+
 @pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
 def test_full_size_resnet18_layer(layer):
     if layer.n >= 400_000:  # the stem, run like the benchmark workload
