@@ -958,6 +958,53 @@ uint32_t split_for(uint64_t count, uint64_t cus) {
     return 0;
 }
 
+// A second stream per device (default priority, non-blocking) and the two
+// events that fork work onto it from the caller's stream and join it back.
+// Created on first use and kept until the process ends.
+struct AuxStream {
+    hipStream_t s;
+    hipEvent_t fork, join;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_aux_mu;
+AuxStream g_aux[kMaxDevices] = {};
+
+// Runs bulk(stream) and, beside it, tail(second stream); the caller's stream
+// then waits for both.  Under stream capture (the second stream would join
+// the caller's graph) the tail follows the bulk on the caller's stream.
+template <class Bulk, class Tail>
+int fork_tail(hipStream_t stream, const Bulk &bulk, const Tail &tail) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return REDASH_E_HIP;
+    if (cs != hipStreamCaptureStatusNone) {
+        const int rc = bulk(stream);
+        return rc ? rc : tail(stream);
+    }
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return REDASH_E_HIP;
+    std::lock_guard<std::mutex> lock(g_aux_mu);  // one fork-join sequence at a time on the shared events
+    AuxStream &A = g_aux[dev];
+    if (!A.s) {
+        AuxStream n{};
+        if (hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking) != hipSuccess) return REDASH_E_HIP;
+        if (hipEventCreateWithFlags(&n.fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&n.join, hipEventDisableTiming) != hipSuccess) {
+            if (n.fork) (void)hipEventDestroy(n.fork);
+            (void)hipStreamDestroy(n.s);
+            return REDASH_E_HIP;
+        }
+        A = n;
+    }
+    if (hipEventRecord(A.fork, stream) != hipSuccess || hipStreamWaitEvent(A.s, A.fork, 0) != hipSuccess)
+        return REDASH_E_HIP;
+    int rc = bulk(stream);
+    if (!rc) rc = tail(A.s);
+    // joined even after a failed launch: the caller's stream never runs ahead of queued work
+    if (hipEventRecord(A.join, A.s) != hipSuccess || hipStreamWaitEvent(stream, A.join, 0) != hipSuccess)
+        return REDASH_E_HIP;
+    return rc;
+}
+
 int launch_split_any(uint32_t split, const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab,
                      uint32_t *out, uint32_t *work, uint64_t first, uint64_t count, hipStream_t stream) {
     switch (split) {
@@ -977,13 +1024,29 @@ int launch_split_any(uint32_t split, const Plan &P, uint32_t lds, const uint32_t
 // round goes to it after them instead of running as a last round with few
 // waves per SIMD, whose gadgets would take the latency of their gate chain
 // (a larger rest costs k_eval no more than it would cost the split).
+//
+// With `fork`, a call just above one full round of the 4- or 2-wave split
+// (two 768-thread workgroups per CU: 98,304 or 196,608 gadgets on 256 CUs)
+// runs that round on the split and the rest, at most one 64-gadget workgroup
+// per CU, on the 12-wave split beside it on a second stream: the rest's
+// workgroups take the CUs the round frees first, instead of adding a
+// wave to some SIMDs for the whole call.
 int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
-                hipStream_t stream) {
+                hipStream_t stream, bool fork) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         return REDASH_E_HIP;
     const uint64_t ncu = static_cast<uint64_t>(cus);
+    for (const uint32_t split : {4u, 2u}) {
+        const uint64_t full = 2 * ncu * (kEvalBlock / split);
+        if (fork && P.n > full && P.n - full <= ncu * 64) {
+            return fork_tail(
+                stream,
+                [&](hipStream_t s) { return launch_split_any(split, P, lds, in, tab, out, work, 0, full, s); },
+                [&](hipStream_t s) { return launch_split<12>(P, lds, in, tab, out, work, full, P.n - full, s); });
+        }
+    }
     if (const uint32_t split = split_for(P.n, ncu))
         return launch_split_any(split, P, lds, in, tab, out, work, 0, P.n, stream);
     const uint64_t round = 2 * ncu * kLaneBlock;  // gadgets of one round, one per lane
@@ -1105,7 +1168,7 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
-    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream);
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream, true);
 }
 
 }  // extern "C"
@@ -1118,7 +1181,6 @@ namespace {
 // own copy at its own address).
 __device__ __align__(256) uint32_t scratch[REDASH_NOALLOC_WORK_WORDS];
 
-constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
 uint32_t *g_scratch_ptr[kMaxDevices] = {};
 
@@ -1156,7 +1218,7 @@ int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_label
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
-    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, work, stream);
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, work, stream, false);
 }
 
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,

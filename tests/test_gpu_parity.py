@@ -396,24 +396,88 @@ def test_full_size_batched():
 
 # The evaluator's launch thresholds on this GPU.  Calls of up to one round of
 # two workgroups per CU with 64, 192 or 384 gadgets per workgroup give each
-# group of 64 gadgets 12, 4 or 2 waves; larger calls take one gadget per lane
-# on whole rounds of 768-gadget workgroups, and a rest that the 12-wave split
-# holds in one round (64 gadgets per workgroup) goes to it, starting at the
-# first gadget after the rounds.  Each threshold and one gadget past it.
-# (name, whole rounds, then gadgets per workgroup of the two per CU, extra)
-LAUNCH_EDGES = [("split12-last", 0, 64, 0), ("split4-first", 0, 64, 1), ("split4-last", 0, 192, 0),
-                ("split2-first", 0, 192, 1), ("split2-last", 0, 384, 0), ("one-per-lane-first", 0, 384, 1),
-                ("round-rest-one", 1, 0, 1), ("round-rest-split12-last", 1, 64, 0), ("round-rest-past-split12", 1, 64, 1)]
+# group of 64 gadgets 12, 4 or 2 waves; a call above one full round of the 4-
+# or 2-wave split by at most 64 gadgets per CU runs that round on the split and
+# the rest on the 12-wave split on a second stream beside it; larger calls take
+# one gadget per lane on whole rounds of 768-gadget workgroups, and a rest that
+# the 12-wave split holds in one round (64 gadgets per workgroup) goes to it,
+# starting at the first gadget after the rounds.  Each threshold and one gadget
+# past it.  (name, whole rounds, gadgets per workgroup of the two per CU,
+# gadgets per CU, extra): n = 2 cus (768 rounds + per) + cus per_cu + extra.
+LAUNCH_EDGES = [("split12-last", 0, 64, 0, 0), ("split4-first", 0, 64, 0, 1), ("split4-last", 0, 192, 0, 0),
+                ("split4-round-rest-first", 0, 192, 0, 1), ("split4-round-rest-last", 0, 192, 64, 0),
+                ("split2-first", 0, 192, 64, 1), ("split2-last", 0, 384, 0, 0),
+                ("split2-round-rest-first", 0, 384, 0, 1), ("split2-round-rest-last", 0, 384, 64, 0),
+                ("one-per-lane-first", 0, 384, 64, 1), ("round-rest-one", 1, 0, 0, 1),
+                ("round-rest-split12-last", 1, 64, 0, 0), ("round-rest-past-split12", 1, 64, 0, 1)]
 
 
-@pytest.mark.parametrize("rounds,per,extra", [e[1:] for e in LAUNCH_EDGES], ids=[e[0] for e in LAUNCH_EDGES])
-def test_evaluator_launch_thresholds(rounds, per, extra):
+@pytest.mark.parametrize("rounds,per,per_cu,extra", [e[1:] for e in LAUNCH_EDGES], ids=[e[0] for e in LAUNCH_EDGES])
+def test_evaluator_launch_thresholds(rounds, per, per_cu, extra):
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    n = 2 * cus * (768 * rounds + per) + extra
+    n = 2 * cus * (768 * rounds + per) + cus * per_cu + extra
     P = rns.cardinality(WL.PRIMES_12)
-    w = WL.Workload(f"edge-{n}", tuple(WL.PRIMES_12), (11,), n, 60 + per + extra, "uniform", -(P // 2),
+    w = WL.Workload(f"edge-{n}", tuple(WL.PRIMES_12), (11,), n, 60 + per + per_cu + extra, "uniform", -(P // 2),
                     P - P // 2)
     _check_full(w, 4096, 4096, 8192)
+
+
+def _round_and_rest_call(seed: int):
+    """A layer-1-sized call (one full round of the 2-wave split and 4,096
+    gadgets on the second stream), garbled and encoded."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 2 * cus * 384 + 4096
+    w = WL.by_name("resnet18.l1.1.a")
+    bp = B.make_params(w.moduli, w.scale_idx, n, seed)
+    x = np.resize(WL.make_inputs(w), n)
+    buf = B.Buffers(bp, "cuda")
+    B.redash_garble_scale(bp, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work)
+    B.redash_encode(bp, torch.from_numpy(x).cuda(), buf.in_zero, buf.offsets, buf.in_labels)
+    torch.cuda.synchronize()
+    return w, bp, x, buf
+
+
+def test_round_and_rest_follow_the_callers_stream():
+    """On a stream of the caller's other than the null stream, work queued
+    after the call (decode) sees every gadget of both launches, and a second
+    call into fresh output buffers right behind the first gives the same labels."""
+    w, bp, x, buf = _round_and_rest_call(81)
+    s = torch.cuda.Stream()
+    out2 = torch.full_like(buf.out_labels, -1)
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        buf.out_labels.fill_(-1)
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels, buf.work, s)
+        B.redash_decode(bp, buf.out_labels, buf.out_zero, buf.offsets, buf.y, buf.bad, s)
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, out2, buf.work, s)
+    s.synchronize()
+    assert int(buf.bad.item()) == 0
+    assert np.array_equal(buf.y.cpu().numpy()[:len(x)], _scaled(x, w.moduli, w.scale_idx))
+    assert torch.equal(out2, buf.out_labels)
+
+
+def test_round_and_rest_under_graph_capture():
+    """Captured in a graph (the rest then follows the round on the capturing
+    stream): three replays, with eager calls and synchronizations between
+    them, each equal to the eager call."""
+    w, bp, x, buf = _round_and_rest_call(82)
+    B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels, buf.work)
+    torch.cuda.synchronize()
+    ref = buf.out_labels.clone()
+    out_g = torch.full_like(buf.out_labels, -1)
+    work_g = torch.empty_like(buf.work)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, capture_error_mode="thread_local"):
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, out_g, work_g)
+    for _ in range(3):
+        out_g.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels, buf.work)
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, ref)
+        assert torch.equal(buf.out_labels, ref)
+    del g
 
 
 # Bases beyond the workloads' on the one-gadget-per-lane evaluator (its target-major
