@@ -20,8 +20,7 @@
  *  - Pointers named d_* are DEVICE pointers on the current HIP device.  The
  *    caller allocates and owns every buffer, sized from redash_plan(); the
  *    library never allocates or frees device memory and keeps no state
- *    between calls beyond read-only constants and, per device, the stream
- *    and two events redash_eval_scale creates on first need (see there).
+ *    between calls beyond read-only constants.
  *  - Calls are asynchronous on `stream` (0 = the null stream); they return
  *    after the launches are queued.  Buffers must stay valid until the stream
  *    reaches the work.  Calls that write the same buffers must be ordered by
@@ -197,15 +196,6 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
  *                return unspecified; may be NULL when work_words is 0.
  * Output labels carry floor(x/s) (see redash_params) under the garbler's
  * output zero-labels.
- * Streams: a call a little above one full round of the 4- or 2-wave split
- * evaluator (n - 2 cus 192 or n - 2 cus 384 in 1 .. 64 cus, cus = compute
- * units) runs that round on `stream` and the rest beside it on a second
- * stream of the library's (one per device, default priority, non-blocking,
- * created by the first such call and kept until the process ends); `stream`
- * then waits for the second stream, so work queued after the call sees every
- * output, as after a single-stream call.  Under stream capture the rest
- * follows the round on `stream`.  Calls from several host threads are
- * serialised while they queue this fork and join.
  * REDASH_E_PARAM also when n >= 2^30 (a gadget's byte offset must fit in
  * 32 bits).
  */
@@ -221,8 +211,7 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
  * each GPU holds from the loading of the library's kernels onto it until the
  * process ends.  The
  * call allocates and frees nothing (no hipMalloc, hipFree or allocating
- * library routine), creates no stream or event, and queues all of its work
- * on `stream` (no second stream at any size).
+ * library routine).
  *   Limit: n * work_words (from redash_plan) <= REDASH_NOALLOC_WORK_WORDS,
  *   else REDASH_E_SIZE and nothing is launched (the 12-prime base scaled by
  *   one modulus needs 54 words per gadget: up to 310,689 gadgets per call).

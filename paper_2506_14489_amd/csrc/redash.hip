@@ -397,31 +397,48 @@ k_eval(const EvalPlan P, const uint32_t *__restrict__ in, const uint32_t *__rest
 
 // ---------------------------------------------------------------------------
 // The evaluator for calls too small to fill the GPU one gadget per lane.
-// A group of SPLIT waves shares 64 gadgets (one per lane); within a run of
+// A group of `split` waves shares 64 gadgets (one per lane); within a run of
 // gates that share a digit label (distinct destinations, no dependence among
-// them) wave j of the group takes gates j, j + SPLIT, ...; a workgroup
+// them) wave j of the group takes gates j, j + split, ...; a workgroup
 // barrier after each run makes the updated labels (in global memory; the
 // waves of a workgroup share one write-through L1) visible to every wave
 // before the next run reads them.  The gate a wave works on stays uniform.
 // Same LDS image as k_eval.
+//
+// One launch may hold two kinds of workgroup: 0 .. nb0-1 give each group
+// split0 waves, the others split1; the gadgets are first, first + 1, ... in
+// workgroup order (blockDim / split0 per workgroup of the first kind, then
+// blockDim / split1 per workgroup of the second).  The workgroups are
+// dispatched in order, so the second kind takes the CUs the first frees.
 // ---------------------------------------------------------------------------
-template <int BLOCK, uint32_t SPLIT>
+struct SplitLaunch {
+    uint32_t first;   // the launch's first gadget
+    uint32_t nb0;     // workgroups of the first kind
+    uint32_t split0;  // waves per 64 gadgets in them (2, 4 or 12)
+    uint32_t split1;  // waves per 64 gadgets in the others
+};
+
+template <int BLOCK>
 __global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))
 k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__restrict__ tab, uint32_t *out,
-             uint32_t *work, uint32_t first) {
+             uint32_t *work, const SplitLaunch L) {
     extern __shared__ uint32_t lds[];
     uint32_t *K = lds + kTableRegionBytes / 4;
     const int tid = threadIdx.x;
-    const int nthr = blockDim.x;  // a multiple of 64 SPLIT, at most BLOCK
+    const int nthr = blockDim.x;  // a multiple of 64 split0 and of 64 split1, at most BLOCK
     stage_perm_te02(lds, tid, nthr);
     stage_hash_key(K, tid, nthr);
     stage_free_op_tables(P, lds, tid, static_cast<uint32_t>(nthr) / 64u);
     __syncthreads();
     const PermTE02 TT = perm_te02();
     const uint32_t wave = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(tid) / 64u);
-    const uint32_t part = wave % SPLIT, grp = wave / SPLIT;
-    const uint64_t a = first + static_cast<uint64_t>(blockIdx.x) * (static_cast<uint32_t>(nthr) / SPLIT) +
-                       grp * 64u + static_cast<uint32_t>(tid) % 64u;
+    const uint32_t wg = blockIdx.x;
+    const bool kind1 = wg >= L.nb0;
+    const uint32_t split = kind1 ? L.split1 : L.split0;
+    const uint32_t part = wave % split, grp = wave / split;
+    const uint32_t per0 = static_cast<uint32_t>(nthr) / L.split0;
+    const uint32_t start = kind1 ? L.nb0 * per0 + (wg - L.nb0) * (static_cast<uint32_t>(nthr) / L.split1) : wg * per0;
+    const uint64_t a = static_cast<uint64_t>(L.first) + start + grp * 64u + static_cast<uint32_t>(tid) % 64u;
     const bool live = a < P.n;  // dead lanes still take every barrier
     const LabelBufs LB{in, out, work, P.n, static_cast<uint32_t>(live ? a : 0) * 4u};
     const uint64_t tau0 = (P.a0 + a) * P.G;
@@ -434,7 +451,7 @@ k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__re
             const uint32_t d = P.gate[g + i];
             const ModConst mq = P.mod[src];
             const uint32_t q = mq.m;
-            if (i % SPLIT == part && live) {
+            if (i % split == part && live) {
                 // the digit label: fold and colour (see k_eval)
                 const uint32_t *dig = LB.base(gate_dsrc(d), mq);
                 const uint32_t w0 = LB.get(dig, 0);
@@ -930,22 +947,29 @@ int launched() {
     return hipGetLastError() == hipSuccess ? REDASH_OK : REDASH_E_HIP;
 }
 
-// k_eval_split over gadgets first .. first + count - 1 (of the plan's n).
-template <uint32_t SPLIT>
-int launch_split(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
-                 uint64_t first, uint64_t count, hipStream_t stream) {
-    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval_split<kEvalBlock, SPLIT>), lds);
+// Launches k_eval_split (it may use more than 64 KiB of LDS).
+int launch_split_kernel(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
+                        uint32_t *work, const SplitLaunch &L, unsigned grid, int threads, hipStream_t stream) {
+    const int rc = allow_lds(reinterpret_cast<const void *>(&k_eval_split<kEvalBlock>), lds);
     if (rc) return rc;
-    // block / SPLIT gadgets per workgroup, the block a multiple of 64 SPLIT
-    // (every group of SPLIT waves complete) and at most kEvalBlock
-    constexpr int most = kEvalBlock / static_cast<int>(SPLIT) / 64 * 64;
-    static_assert(most >= 64, "a workgroup holds at least one group of SPLIT waves");
-    int per = 0;
-    if ((rc = block_for(count, most, &per))) return rc;
-    hipLaunchKernelGGL((k_eval_split<kEvalBlock, SPLIT>), dim3(grid_for(count, per)),
-                       dim3(per * static_cast<int>(SPLIT)), lds, stream, P, in, tab, out, work,
-                       static_cast<uint32_t>(first));
+    hipLaunchKernelGGL(k_eval_split<kEvalBlock>, dim3(grid), dim3(threads), lds, stream, P, in, tab, out, work, L);
     return launched();
+}
+
+// Gadgets per workgroup of the split evaluator at full size: a multiple of 64
+// with per * split <= kEvalBlock (768, 384, 192 and 64 for 1, 2, 4 and 12 waves).
+constexpr uint32_t split_most(uint32_t split) { return kEvalBlock / split / 64 * 64; }
+
+// k_eval_split over gadgets first .. first + count - 1 (of the plan's n), each
+// group of 64 gadgets on `split` waves (12, 4 or 2).
+int launch_split(uint32_t split, const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out,
+                 uint32_t *work, uint64_t first, uint64_t count, hipStream_t stream) {
+    int per = 0;
+    const int rc = block_for(count, static_cast<int>(split_most(split)), &per);
+    if (rc) return rc;
+    const SplitLaunch L{static_cast<uint32_t>(first), grid_for(count, per), split, split};
+    return launch_split_kernel(P, lds, in, tab, out, work, L, grid_for(count, per), per * static_cast<int>(split),
+                               stream);
 }
 
 // The split evaluator for `count` gadgets that one round of two workgroups
@@ -958,97 +982,39 @@ uint32_t split_for(uint64_t count, uint64_t cus) {
     return 0;
 }
 
-// A second stream per device (default priority, non-blocking) and the two
-// events that fork work onto it from the caller's stream and join it back.
-// Created on first use and kept until the process ends.
-struct AuxStream {
-    hipStream_t s;
-    hipEvent_t fork, join;
-};
-constexpr int kMaxDevices = 64;
-std::mutex g_aux_mu;
-AuxStream g_aux[kMaxDevices] = {};
-
-// Runs bulk(stream) and, beside it, tail(second stream); the caller's stream
-// then waits for both.  Under stream capture (the second stream would join
-// the caller's graph) the tail follows the bulk on the caller's stream.
-template <class Bulk, class Tail>
-int fork_tail(hipStream_t stream, const Bulk &bulk, const Tail &tail) {
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return REDASH_E_HIP;
-    if (cs != hipStreamCaptureStatusNone) {
-        const int rc = bulk(stream);
-        return rc ? rc : tail(stream);
-    }
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return REDASH_E_HIP;
-    std::lock_guard<std::mutex> lock(g_aux_mu);  // one fork-join sequence at a time on the shared events
-    AuxStream &A = g_aux[dev];
-    if (!A.s) {
-        AuxStream n{};
-        if (hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking) != hipSuccess) return REDASH_E_HIP;
-        if (hipEventCreateWithFlags(&n.fork, hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&n.join, hipEventDisableTiming) != hipSuccess) {
-            if (n.fork) (void)hipEventDestroy(n.fork);
-            (void)hipStreamDestroy(n.s);
-            return REDASH_E_HIP;
-        }
-        A = n;
-    }
-    if (hipEventRecord(A.fork, stream) != hipSuccess || hipStreamWaitEvent(A.s, A.fork, 0) != hipSuccess)
-        return REDASH_E_HIP;
-    int rc = bulk(stream);
-    if (!rc) rc = tail(A.s);
-    // joined even after a failed launch: the caller's stream never runs ahead of queued work
-    if (hipEventRecord(A.join, A.s) != hipSuccess || hipStreamWaitEvent(stream, A.join, 0) != hipSuccess)
-        return REDASH_E_HIP;
-    return rc;
-}
-
-int launch_split_any(uint32_t split, const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab,
-                     uint32_t *out, uint32_t *work, uint64_t first, uint64_t count, hipStream_t stream) {
-    switch (split) {
-        case 12: return launch_split<12>(P, lds, in, tab, out, work, first, count, stream);
-        case 4: return launch_split<4>(P, lds, in, tab, out, work, first, count, stream);
-        case 2: return launch_split<2>(P, lds, in, tab, out, work, first, count, stream);
-        default: return REDASH_E_PARAM;  // not reached
-    }
-}
-
 // Launches the evaluators for n gadgets.  A call that one round of two
 // workgroups per CU holds when a gadget takes 12, 4 or 2 waves runs on
 // k_eval_split with that split (runs of gates sharing a digit have at most
 // k - 1 gates, 11 on the 12-prime base: with 12 waves one gate per wave and
-// run).  A larger call runs on k_eval, one gadget per lane: whole rounds of
-// two full workgroups per CU, and a rest that the 12-wave split holds in one
-// round goes to it after them instead of running as a last round with few
-// waves per SIMD, whose gadgets would take the latency of their gate chain
-// (a larger rest costs k_eval no more than it would cost the split).
-//
-// With `fork`, a call just above one full round of the 4- or 2-wave split
-// (two 768-thread workgroups per CU: 98,304 or 196,608 gadgets on 256 CUs)
-// runs that round on the split and the rest, at most one 64-gadget workgroup
-// per CU, on the 12-wave split beside it on a second stream: the rest's
-// workgroups take the CUs the round frees first, instead of adding a
-// wave to some SIMDs for the whole call.
+// run).  A call a little above one full round of the 4- or 2-wave split
+// (98,304 or 196,608 gadgets on 256 CUs, plus at most 64 gadgets per CU) runs
+// that round and its rest as one launch, the rest's workgroups on 12 waves per
+// 64 gadgets after the round's: they take the CUs the round frees first,
+// instead of adding a wave to some SIMDs for the whole call.  A larger call
+// runs on k_eval, one gadget per lane: whole rounds of two full workgroups per
+// CU, and a rest that the 12-wave split holds in one round goes to it after
+// them instead of running as a last round with few waves per SIMD, whose
+// gadgets would take the latency of their gate chain (a larger rest costs
+// k_eval no more than it would cost the split).
 int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
-                hipStream_t stream, bool fork) {
+                hipStream_t stream) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         return REDASH_E_HIP;
     const uint64_t ncu = static_cast<uint64_t>(cus);
     for (const uint32_t split : {4u, 2u}) {
-        const uint64_t full = 2 * ncu * (kEvalBlock / split);
-        if (fork && P.n > full && P.n - full <= ncu * 64) {
-            return fork_tail(
-                stream,
-                [&](hipStream_t s) { return launch_split_any(split, P, lds, in, tab, out, work, 0, full, s); },
-                [&](hipStream_t s) { return launch_split<12>(P, lds, in, tab, out, work, full, P.n - full, s); });
+        const uint32_t per0 = split_most(split);
+        const uint64_t full = 2 * ncu * per0;
+        if (P.n > full && P.n - full <= ncu * 64) {
+            const uint32_t nb0 = static_cast<uint32_t>(2 * ncu);
+            const unsigned grid = nb0 + grid_for(P.n - full, 64);
+            return launch_split_kernel(P, lds, in, tab, out, work, SplitLaunch{0, nb0, split, 12}, grid, kEvalBlock,
+                                       stream);
         }
     }
     if (const uint32_t split = split_for(P.n, ncu))
-        return launch_split_any(split, P, lds, in, tab, out, work, 0, P.n, stream);
+        return launch_split(split, P, lds, in, tab, out, work, 0, P.n, stream);
     const uint64_t round = 2 * ncu * kLaneBlock;  // gadgets of one round, one per lane
     uint64_t bulk = P.n;
     const uint64_t rest = P.n % round;
@@ -1063,7 +1029,7 @@ int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t 
                        work);
     if ((rc = launched())) return rc;
     if (bulk == P.n) return REDASH_OK;
-    return launch_split_any(split_for(P.n - bulk, ncu), P, lds, in, tab, out, work, bulk, P.n - bulk, stream);
+    return launch_split(split_for(P.n - bulk, ncu), P, lds, in, tab, out, work, bulk, P.n - bulk, stream);
 }
 
 
@@ -1168,7 +1134,7 @@ int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
-    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream, true);
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, d_work, stream);
 }
 
 }  // extern "C"
@@ -1181,6 +1147,7 @@ namespace {
 // own copy at its own address).
 __device__ __align__(256) uint32_t scratch[REDASH_NOALLOC_WORK_WORDS];
 
+constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
 uint32_t *g_scratch_ptr[kMaxDevices] = {};
 
@@ -1218,7 +1185,7 @@ int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_label
     if ((rc = max_lds_bytes(&max_lds))) return rc;
     const uint32_t lds = eval_lds_bytes(P.ntab);
     if (lds > max_lds) return REDASH_E_HIP;
-    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, work, stream, false);
+    return launch_eval(P, lds, d_in_labels, d_tables, d_out_labels, work, stream);
 }
 
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,

@@ -36,7 +36,7 @@ MEASURED = {
         # taken on an earlier source; the device code built from these sources is the same,
         # instruction for instruction (since then: the split evaluator, unused helpers, and
         # host-side launch code)
-        "sources_sha256": "dfcb5699eb20d7f6bcd414894665e8b135bac77feff7b698834ce2de852851d2",
+        "sources_sha256": "2910fbb81009a79331ecdfcb4ee103316468d7de1b9bad44b243c9ed32a06a71",
     },
 }
 

@@ -398,7 +398,7 @@ def test_full_size_batched():
 # two workgroups per CU with 64, 192 or 384 gadgets per workgroup give each
 # group of 64 gadgets 12, 4 or 2 waves; a call above one full round of the 4-
 # or 2-wave split by at most 64 gadgets per CU runs that round on the split and
-# the rest on the 12-wave split on a second stream beside it; larger calls take
+# the rest on 12 waves per 64 gadgets in the same launch; larger calls take
 # one gadget per lane on whole rounds of 768-gadget workgroups, and a rest that
 # the 12-wave split holds in one round (64 gadgets per workgroup) goes to it,
 # starting at the first gadget after the rounds.  Each threshold and one gadget
@@ -423,8 +423,8 @@ def test_evaluator_launch_thresholds(rounds, per, per_cu, extra):
 
 
 def _round_and_rest_call(seed: int):
-    """A layer-1-sized call (one full round of the 2-wave split and 4,096
-    gadgets on the second stream), garbled and encoded."""
+    """A layer-1-sized call (one full round of the 2-wave split and a rest of
+    4,096 gadgets on 12 waves per 64 in the same launch), garbled and encoded."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     n = 2 * cus * 384 + 4096
     w = WL.by_name("resnet18.l1.1.a")
@@ -439,8 +439,9 @@ def _round_and_rest_call(seed: int):
 
 def test_round_and_rest_follow_the_callers_stream():
     """On a stream of the caller's other than the null stream, work queued
-    after the call (decode) sees every gadget of both launches, and a second
-    call into fresh output buffers right behind the first gives the same labels."""
+    after the call (decode) sees every gadget of the round and the rest, and a
+    second call into fresh output buffers right behind the first gives the
+    same labels."""
     w, bp, x, buf = _round_and_rest_call(81)
     s = torch.cuda.Stream()
     out2 = torch.full_like(buf.out_labels, -1)
@@ -457,9 +458,8 @@ def test_round_and_rest_follow_the_callers_stream():
 
 
 def test_round_and_rest_under_graph_capture():
-    """Captured in a graph (the rest then follows the round on the capturing
-    stream): three replays, with eager calls and synchronizations between
-    them, each equal to the eager call."""
+    """Captured in a graph: three replays, with eager calls and
+    synchronizations between them, each equal to the eager call."""
     w, bp, x, buf = _round_and_rest_call(82)
     B.redash_eval_scale(bp, buf.in_labels, buf.tables, buf.out_labels, buf.work)
     torch.cuda.synchronize()
