@@ -341,10 +341,11 @@ int redash_linear_prepare(const redash_linear_params *p, const int32_t *d_weight
  * Evaluator, online: Y = sum w X, every residue of every modulus (Sec. 2.3).
  *   d_in_labels   in_label_words (read only).
  *   d_prepared    from redash_linear_prepare with the same params.
- *   d_work        work_bytes of working storage: every input residue as a
- *                 byte, one zero-padded channel-last plane per (modulus,
- *                 residue).  Contents on entry are ignored and on return
- *                 unspecified.
+ *   d_work        work_bytes of working storage: the input residues in
+ *                 zero-padded channel-last byte planes (one residue per
+ *                 byte, or 8, 4 or 2 residues of a modulus m <= 16 in 1-,
+ *                 2- or 4-bit fields).  Contents on entry are ignored and on
+ *                 return unspecified.
  *   d_out_labels  out_label_words, written; may not alias d_in_labels.
  */
 int redash_linear_eval(const redash_linear_params *p, const uint32_t *d_in_labels, const uint8_t *d_prepared,

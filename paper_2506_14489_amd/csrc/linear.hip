@@ -55,7 +55,14 @@ constexpr int kXcds = 8;               // MI355X: workgroups go round-robin to 8
 struct LinMod {
     uint32_t m, b, g, W, glast;
     uint32_t woff;     // word offset of this modulus's block (in units of n)
-    uint32_t lam_off;  // planes of the earlier moduli: sum of their lambda
+    // Residue planes: a plane byte holds f = 8 / bp residues of bp bits
+    // (m <= 16: m = 2 eight of one bit, 3 and 4 four of two bits, 5..16 two
+    // of four bits) or one residue byte (m > 16).  Plane pn(w, j) = w ppw +
+    // j / f of this modulus holds field j mod f of residues j of packed word w.
+    uint32_t pl_off;   // planes of the earlier moduli
+    uint32_t bp, lgf;  // bits per field in a plane byte, log2 f
+    uint32_t ppw;      // planes per full packed word: ceil(g / f)
+    uint32_t rep;      // a bp-bit mask in every byte (f > 1)
     // floor(u / m) = umulhi(u, divM) >> divS for every u the epilogue sees
     uint32_t divM, divS;
     uint32_t off;      // a multiple of m above |sum w v|: keeps u >= 0
@@ -84,7 +91,7 @@ struct LinPlan {
     uint64_t n_in, n_out;         // activations
     uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
-    uint32_t total_lam;           // planes: sum of lambda over the base
+    uint32_t total_planes;        // residue planes over the base
     uint8_t pair_mod[kLinMaxPairs], pair_word[kLinMaxPairs];
     LinMod mod[kMaxK];
 };
@@ -223,7 +230,7 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     L->plane_bytes = static_cast<uint64_t>(L->nimg) * L->hp * L->wp * L->cp;
     if (L->plane_bytes >= (1ull << 32)) return REDASH_E_PARAM;  // 32-bit offsets within a plane
 
-    uint32_t woff = 0, lam_off = 0, np = 0;
+    uint32_t woff = 0, pl_off = 0, np = 0;
     for (uint32_t i = 0; i < p->k; ++i) {
         ModConst mc;
         fill_mod_const(p->moduli[i], &mc);
@@ -234,9 +241,14 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         lm.W = mc.W;
         lm.glast = mc.glast;
         lm.woff = woff;
-        lm.lam_off = lam_off;
+        lm.pl_off = pl_off;
+        lm.bp = mc.b == 1 ? 1u : mc.b == 2 ? 2u : mc.b <= 4 ? 4u : 8u;
+        const uint32_t f = 8 / lm.bp;
+        lm.lgf = f == 8 ? 3u : f == 4 ? 2u : f == 2 ? 1u : 0u;
+        lm.ppw = (mc.g + f - 1) / f;
+        lm.rep = f > 1 ? ((1u << lm.bp) - 1u) * 0x01010101u : 0xffffffffu;
         woff += mc.W;
-        lam_off += mc.lam;
+        pl_off += (mc.W - 1) * lm.ppw + (mc.glast + f - 1) / f;
         // |sum w v| <= K floor(m/2) (m - 1) =: B (signed weights, residues v < m);
         // u = sum w v + off (+ (-b mod m) R_j, below m^2) lies in [0, 2B + m^2),
         // below 2^31 for K <= 16384, and u / m < 2^23 (a signed 24-bit product)
@@ -261,14 +273,14 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         }
     }
     L->npairs = np;
-    L->total_lam = lam_off;
+    L->total_planes = pl_off;
     L->rowsum_off = static_cast<uint64_t>(L->k) * L->ncc * L->o_pad * L->kc;
     return REDASH_OK;
 }
 
 uint64_t prepared_bytes(const LinPlan &L) { return L.rowsum_off + 4ull * L.k * L.o_pad; }
 
-uint64_t work_bytes(const LinPlan &L) { return static_cast<uint64_t>(L.total_lam) * L.plane_bytes; }
+uint64_t work_bytes(const LinPlan &L) { return static_cast<uint64_t>(L.total_planes) * L.plane_bytes; }
 
 uint32_t total_words(const LinPlan &L) {
     uint32_t t = 0;
@@ -324,11 +336,12 @@ __global__ void __launch_bounds__(256) k_linear_rowsums(const LinPlan L, const i
 }
 
 // ---------------------------------------------------------------------------
-// Residue planes.  Plane q = lam_off_i + r (residue r of modulus i) holds
-// plane_bytes bytes: position (img, yp, xp) of the zero-padded input at
-// ((img hp + yp) wp + xp) cp, its cp channel bytes after it.  A byte is the
-// residue v (m <= 128) or v XOR 0x80 (m > 128); padding holds the byte of
-// v = 0, channels past c_in meet zero weights.
+// Residue planes.  Plane pl_off_i + pn(w, j) (see LinMod) holds plane_bytes
+// bytes: position (img, yp, xp) of the zero-padded input at
+// ((img hp + yp) wp + xp) cp, its cp channel bytes after it.  A byte holds f
+// residues of a modulus m <= 16 in bp-bit fields, or one residue v (16 < m <=
+// 128) or v XOR 0x80 (m > 128); padding holds the byte of v = 0, channels
+// past c_in meet zero weights.
 // ---------------------------------------------------------------------------
 
 // A word at byte offset `off` (below 2^32) of a uniform base: the offset stays
@@ -423,22 +436,42 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
         for (int k = 0; k < 4; ++k) wd[4 * d + k] = static_cast<uint32_t>(v[k]);
     }
     const uint32_t nlive = !inside || c0 >= L.c_in ? 0u : (L.c_in - c0 < 16 ? L.c_in - c0 : 16u);  // live channels
-    uint8_t *dst = planes + static_cast<uint64_t>(M.lam_off + w * M.g) * L.plane_bytes + static_cast<uint64_t>(pp) * L.cp + c0;
-    for (uint32_t jr = 0; jr < g; ++jr) {
-        const uint32_t sh = M.b * jr;
+    uint8_t *dst = planes + static_cast<uint64_t>(M.pl_off + w * M.ppw) * L.plane_bytes + static_cast<uint64_t>(pp) * L.cp + c0;
+    const uint32_t nplanes = (g + (1u << M.lgf) - 1) >> M.lgf;
+    for (uint32_t h = 0; h < nplanes; ++h) {
         v4i v;
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            uint32_t f = 0;
+            uint32_t y = 0;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const uint32_t q = static_cast<uint32_t>(4 * d + k);
-                f |= (q < nlive ? __builtin_amdgcn_ubfe(wd[q], sh, M.b) : 0u) << (8 * k);
+                uint32_t x;
+                if (M.lgf == 0) {
+                    x = __builtin_amdgcn_ubfe(wd[q], M.b * h, M.b);  // one residue
+                } else if (M.bp == M.b) {
+                    x = __builtin_amdgcn_ubfe(wd[q], 8 * h, 8);  // f adjacent fields, as in the word
+                } else {
+                    // b = 3: residues 2h and 2h + 1 into 4-bit fields
+                    x = __builtin_amdgcn_ubfe(wd[q], 6 * h, 3) | (__builtin_amdgcn_ubfe(wd[q], 6 * h + 3, 3) << 4);
+                }
+                y |= (q < nlive ? x : 0u) << (8 * k);
             }
-            v[d] = static_cast<int32_t>(f ^ flip);
+            v[d] = static_cast<int32_t>(y ^ flip);
         }
-        *reinterpret_cast<v4i *>(dst + static_cast<uint64_t>(jr) * L.plane_bytes) = v;
+        *reinterpret_cast<v4i *>(dst + static_cast<uint64_t>(h) * L.plane_bytes) = v;
     }
+}
+
+// Residue j's values from a 16-byte piece of its plane: field j mod f of
+// every byte (f > 1), or the bytes themselves.
+__device__ __forceinline__ v4i plane_field(const v4i &v, const LinMod &M, uint32_t j) {
+    if (M.lgf == 0) return v;
+    const uint32_t sh = M.bp * (j & ((1u << M.lgf) - 1u));
+    v4i r;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) r[d] = static_cast<int32_t>((static_cast<uint32_t>(v[d]) >> sh) & M.rep);
+    return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -549,7 +582,8 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const uint32_t j = st.j0 + q < g ? st.j0 + q : 0u;
-            const uint8_t *plane = planes + static_cast<uint64_t>(M.lam_off + st.w * M.g + j) * L.plane_bytes;
+            const uint8_t *plane =
+                planes + static_cast<uint64_t>(M.pl_off + st.w * M.ppw + (j >> M.lgf)) * L.plane_bytes;
 #pragma unroll
             for (int t = 0; t < 2; ++t) pf[t][q] = load16(plane, pval[t] ? poff[t] + st.cc * L.ck : 0u);
         }
@@ -605,7 +639,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
             if (j0 + q < g) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
-                    if (pval[t]) *reinterpret_cast<v4i *>(Bl + q * L.halo + loff[t]) = pf[t][q];
+                    if (pval[t]) *reinterpret_cast<v4i *>(Bl + q * L.halo + loff[t]) = plane_field(pf[t][q], M, j0 + q);
             }
         // pf is free: the next stage
         if (ahead.w < M.W) load_stage(pf, ahead);
@@ -809,26 +843,29 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) colb[cb] = (cb * 16 + lane % 16) * L.stride * L.xstride;
 
-    // residue rr = w g + j of the modulus (field j of packed word w) is
-    // plane lam_off + rr; the halo of residue rr + 1 is staged after the
-    // operations of residue rr, its pieces loaded one residue ahead
+    // residue (w, j) (field j of packed word w) is in plane pn(w, j) of the
+    // modulus; the halo of the next residue is staged after the operations
+    // of this one from registers that hold its plane's pieces, and a plane
+    // is loaded into them one residue before its first residue is staged
     auto g_of = [&](uint32_t w) { return (w + 1 == M.W) ? M.glast : M.g; };
-    const uint32_t lam = (M.W - 1) * M.g + M.glast;
+    auto pn = [&](uint32_t w, uint32_t j) { return w * M.ppw + (j >> M.lgf); };
     v4i pf[PL];
-    auto load = [&](uint32_t rr) {
-        const uint8_t *plane = planes + static_cast<uint64_t>(M.lam_off + rr) * L.plane_bytes;
+    auto load = [&](uint32_t pl) {
+        const uint8_t *plane = planes + static_cast<uint64_t>(M.pl_off + pl) * L.plane_bytes;
 #pragma unroll
         for (int s = 0; s < PL; ++s) pf[s] = load16(plane, lane + 64 * s < pieces ? poff[s] : 0u);
     };
-    auto stage = [&]() {
+    auto stage = [&](uint32_t j) {
 #pragma unroll
         for (int s = 0; s < PL; ++s)
-            if (lane + 64 * s < pieces) *reinterpret_cast<v4i *>(Bw + loff(s)) = pf[s];
+            if (lane + 64 * s < pieces) *reinterpret_cast<v4i *>(Bw + loff(s)) = plane_field(pf[s], M, j);
     };
     load(0);
-    stage();
-    if (1 < lam) load(1);
-    uint32_t rr = 0;  // the residue being computed
+    stage(0);
+    // (nw, nj): the next residue to stage; its plane is in pf once staged
+    uint32_t nw = 0, nj = 1;
+    if (nj == g_of(0)) nw = 1, nj = 0;
+    if (nw < M.W && pn(nw, nj) != 0) load(pn(nw, nj));
 
     uint32_t part[4][NCB][4];
     v4i acc[4][NCB];
@@ -916,12 +953,16 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                 }
             }
             // the next residue's halo over this one (after this wave's reads,
-            // in LDS order), then the one after into the registers
-            if (rr + 1 < lam) {
-                stage();
-                if (rr + 2 < lam) load(rr + 2);
+            // in LDS order), then the plane of the one after into the
+            // registers if it is a new plane
+            if (nw < M.W) {
+                stage(nj);
+                uint32_t mw = nw, mj = nj + 1;
+                if (mj == g_of(mw)) mw += 1, mj = 0;
+                if (mw < M.W && pn(mw, mj) != pn(nw, nj)) load(pn(mw, mj));
+                nw = mw;
+                nj = mj;
             }
-            ++rr;
             // epilogue: residue of u mod m into field j
             const uint32_t sh = M.b * j;
             auto epilogue = [&](auto shifts) {

@@ -236,9 +236,28 @@ def test_linear_plan_sizes(case):
     assert sz["out_label_words"] == n * c_out * ho * wo * W
     assert sz["offset_words"] == W
     assert sz["prepared_bytes"] >= len(moduli) * c_out * c_in * kh * kw
-    # one byte per residue per (zero-padded) input position and channel
-    lam_total = sum(OL.label_lambda(m) for m in moduli)
-    assert sz["work_bytes"] >= lam_total * n * c_in * h * w
+    # residue planes of one byte per (zero-padded) input position and
+    # channel: one residue per byte, or f = 8 / bp residues of bp bits for
+    # m <= 16 (bp = 1, 2, 4), grouped within each packed word
+    def planes(m):
+        b = (m - 1).bit_length()
+        lam, g = OL.label_lambda(m), 32 // b
+        W = -(-lam // g)
+        bp = 1 if b == 1 else 2 if b == 2 else 4 if b <= 4 else 8
+        f = 8 // bp
+        return (W - 1) * -(-g // f) + -(-(lam - (W - 1) * g) // f)
+
+    assert sz["work_bytes"] >= sum(planes(m) for m in moduli) * n * c_in * h * w
+
+
+def test_linear_work_of_the_batched_layer():
+    """The 3x3 64 -> 64 layer of the batched map over the first 12 primes:
+    295 residue planes (16 + 21 + 28 + 23 + 19 + 18 for 2..13, packed 8, 4 and
+    2 per byte; 32 + 31 + 29 + 27 + 26 + 25 for 17..37, one per byte) of the
+    zero-padded 16 x 58 x 58 input, 64 channel bytes per position."""
+    sz = B.redash_linear_plan(B.make_linear_params((2, 3, 5, 7, 11, 13, 17, 19, 23, 29, 31, 37), 16, 64, 56, 56,
+                                                   64, 3, 3, 1, 1))
+    assert sz["work_bytes"] == 295 * 16 * 58 * 58 * 64
 
 
 LINEAR_BAD = [
