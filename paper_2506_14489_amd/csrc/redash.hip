@@ -417,6 +417,8 @@ struct SplitLaunch {
     uint32_t split0;  // waves per 64 gadgets in them (2, 4 or 12)
     uint32_t split1;  // waves per 64 gadgets in the others
 };
+static_assert(sizeof(Plan) + 4 * sizeof(void *) + sizeof(SplitLaunch) <= 4096,
+              "the split evaluator's arguments fit the kernel argument block");
 
 template <int BLOCK>
 __global__ void __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(kEvalWaves, kEvalWaves)))

@@ -36,7 +36,7 @@ MEASURED = {
         # taken on an earlier source; the device code built from these sources is the same,
         # instruction for instruction (since then: the split evaluator, unused helpers, and
         # host-side launch code)
-        "sources_sha256": "2910fbb81009a79331ecdfcb4ee103316468d7de1b9bad44b243c9ed32a06a71",
+        "sources_sha256": "0209461897a5675a4b69c4277b91465fd13e14e5e84afa805ee0256a9b69febc",
     },
 }
 
