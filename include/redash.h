@@ -20,7 +20,10 @@
  *  - Pointers named d_* are DEVICE pointers on the current HIP device.  The
  *    caller allocates and owns every buffer, sized from redash_plan(); the
  *    library never allocates or frees device memory and keeps no state
- *    between calls beyond read-only constants.
+ *    between calls beyond read-only constants, host-side caches (per host
+ *    thread, the plan of the last redash_params it passed; per device, its
+ *    compute-unit count and LDS limit) and the fixed buffer of
+ *    redash_eval_scale_noalloc.
  *  - Calls are asynchronous on `stream` (0 = the null stream); they return
  *    after the launches are queued.  Buffers must stay valid until the stream
  *    reaches the work.  Calls that write the same buffers must be ordered by

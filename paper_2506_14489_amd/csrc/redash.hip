@@ -910,16 +910,86 @@ __global__ void __launch_bounds__(BLOCK) k_hash(const ModConst mq, const ModCons
 // ---------------------------------------------------------------------------
 namespace {
 
+constexpr int kMaxDevices = 64;
+
+// Per device: its compute units and the largest LDS allocation a block may
+// request, read on the first call that runs on it (they do not change while
+// the process runs).
+struct DeviceInfo {
+    int cus, max_lds;
+};
+std::mutex g_dev_mu;
+DeviceInfo g_dev[kMaxDevices] = {};
+
+int device_info(DeviceInfo *out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return REDASH_E_HIP;
+    std::lock_guard<std::mutex> lock(g_dev_mu);
+    DeviceInfo &d = g_dev[dev];
+    if (d.cus <= 0) {
+        int cus = 0, lds = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            return REDASH_E_HIP;
+        if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            return REDASH_E_HIP;
+        d = DeviceInfo{cus, lds};
+    }
+    *out = d;
+    return REDASH_OK;
+}
+
+// The plan of the parameters this host thread passed last, and its
+// evaluator schedule once a call needed it: a layer evaluated call after call
+// with the same parameters builds them once.  (redash_params has no padding:
+// equal bytes are equal parameters; unused entries that differ only cost a
+// rebuild.)
+struct PlanCache {
+    bool valid, has_eval;
+    redash_params p;
+    Plan P;
+    EvalPlan E;
+};
+thread_local PlanCache t_plan;
+
+int cached_plan(const redash_params *p, const Plan **out) {
+    if (!p) return REDASH_E_NULL;
+    PlanCache &c = t_plan;
+    if (!c.valid || memcmp(&c.p, p, sizeof *p) != 0) {
+        c.valid = false;
+        const int rc = build_plan(p, &c.P);
+        if (rc) return rc;
+        c.p = *p;
+        c.valid = true;
+        c.has_eval = false;
+    }
+    *out = &c.P;
+    return REDASH_OK;
+}
+
+// The evaluator schedule of P (the cached plan's, kept with it).
+const EvalPlan &eval_plan(const Plan &P) {
+    PlanCache &c = t_plan;
+    if (&P != &c.P) {  // not reached: every entry point takes its plan from the cache
+        static thread_local EvalPlan E;
+        build_eval_plan(P, &E);
+        return E;
+    }
+    if (!c.has_eval) {
+        build_eval_plan(c.P, &c.E);
+        c.has_eval = true;
+    }
+    return c.E;
+}
+
 // Threads per workgroup for n gadgets: the smallest multiple of 64 that keeps
 // the grid within one round of two workgroups per CU (the LDS image allows two),
 // at most `most`.  Small launches thus spread over every CU instead of filling
 // a few with long-running waves; large ones use `most`.
 int block_for(uint64_t n, int most, int *out) {
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        return REDASH_E_HIP;
-    const uint64_t slots = 2ull * static_cast<uint64_t>(cus);
+    DeviceInfo d;
+    const int rc = device_info(&d);
+    if (rc) return rc;
+    const uint64_t slots = 2ull * static_cast<uint64_t>(d.cus);
     const uint64_t b = 64 * ((n + 64 * slots - 1) / (64 * slots));
     *out = b < 64 ? 64 : (b > static_cast<uint64_t>(most) ? most : static_cast<int>(b));
     return REDASH_OK;
@@ -927,10 +997,10 @@ int block_for(uint64_t n, int most, int *out) {
 
 // Largest LDS allocation a block may request on the current device.
 int max_lds_bytes(size_t *out) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return REDASH_E_HIP;
-    *out = static_cast<size_t>(v);
+    DeviceInfo d;
+    const int rc = device_info(&d);
+    if (rc) return rc;
+    *out = static_cast<size_t>(d.max_lds);
     return REDASH_OK;
 }
 
@@ -1000,11 +1070,10 @@ uint32_t split_for(uint64_t count, uint64_t cus) {
 // k_eval no more than it would cost the split).
 int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t *tab, uint32_t *out, uint32_t *work,
                 hipStream_t stream) {
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return REDASH_E_HIP;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        return REDASH_E_HIP;
-    const uint64_t ncu = static_cast<uint64_t>(cus);
+    DeviceInfo d;
+    int rc = device_info(&d);
+    if (rc) return rc;
+    const uint64_t ncu = static_cast<uint64_t>(d.cus);
     for (const uint32_t split : {4u, 2u}) {
         const uint32_t per0 = split_most(split);
         const uint64_t full = 2 * ncu * per0;
@@ -1021,12 +1090,10 @@ int launch_eval(const Plan &P, uint32_t lds, const uint32_t *in, const uint32_t 
     uint64_t bulk = P.n;
     const uint64_t rest = P.n % round;
     if (P.n > round && rest > 0 && rest <= 2 * ncu * 64) bulk = P.n - rest;
-    int rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kLaneBlock>), lds);
-    if (rc) return rc;
+    if ((rc = allow_lds(reinterpret_cast<const void *>(&k_eval<kLaneBlock>), lds))) return rc;
     int block = 0;
     if ((rc = block_for(bulk, kLaneBlock, &block))) return rc;
-    EvalPlan E;
-    build_eval_plan(P, &E);
+    const EvalPlan &E = eval_plan(P);
     hipLaunchKernelGGL(k_eval<kLaneBlock>, dim3(grid_for(bulk, block)), dim3(block), lds, stream, E, in, tab, out,
                        work);
     if ((rc = launched())) return rc;
@@ -1052,9 +1119,10 @@ extern "C" {
 
 int redash_plan(const redash_params *p, redash_sizes *out) {
     if (!p || !out) return REDASH_E_NULL;
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     out->label_words = P.n * P.total_words;
     uint64_t tw = 0;
     for (uint32_t g = 0; g < P.G; ++g) {
@@ -1075,9 +1143,10 @@ namespace {
 template <bool GIVEN>
 int garble_scale(const redash_params *p, uint32_t *d_offsets, const uint32_t *d_in_zero, uint32_t *d_in_zero_w,
                  uint32_t *d_out_zero, uint32_t *d_tables, uint32_t *d_work, hipStream_t stream) {
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
     if (!d_offsets) return REDASH_E_NULL;
     if (P.n > 0 && (!d_in_zero || !d_out_zero || !d_tables || (P.work_words && !d_work))) return REDASH_E_NULL;
@@ -1113,9 +1182,10 @@ int redash_garble_scale_given(const redash_params *p, uint32_t *d_offsets, const
 
 int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_in_zero, const uint32_t *d_offsets,
                   uint32_t *d_in_labels, hipStream_t stream) {
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     if (!d_offsets) return REDASH_E_NULL;
     if (P.n == 0) return REDASH_OK;
     if (!d_x || !d_in_zero || !d_in_labels) return REDASH_E_NULL;
@@ -1126,9 +1196,10 @@ int redash_encode(const redash_params *p, const int64_t *d_x, const uint32_t *d_
 
 int redash_eval_scale(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
                       uint32_t *d_out_labels, uint32_t *d_work, hipStream_t stream) {
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
     if (P.n == 0) return REDASH_OK;
     if (!d_in_labels || !d_tables || !d_out_labels || (P.work_words && !d_work)) return REDASH_E_NULL;
@@ -1149,7 +1220,6 @@ namespace {
 // own copy at its own address).
 __device__ __align__(256) uint32_t scratch[REDASH_NOALLOC_WORK_WORDS];
 
-constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
 uint32_t *g_scratch_ptr[kMaxDevices] = {};
 
@@ -1174,9 +1244,10 @@ extern "C" {
 
 int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_labels, const uint32_t *d_tables,
                               uint32_t *d_out_labels, hipStream_t stream) {
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     if (P.n >= (1ull << 30)) return REDASH_E_PARAM;  // 4 a must fit in 32 bits
     if (P.n * P.work_words > REDASH_NOALLOC_WORK_WORDS) return REDASH_E_SIZE;
     if (P.n == 0) return REDASH_OK;
@@ -1192,9 +1263,10 @@ int redash_eval_scale_noalloc(const redash_params *p, const uint32_t *d_in_label
 
 int redash_decode(const redash_params *p, const uint32_t *d_out_labels, const uint32_t *d_out_zero,
                   const uint32_t *d_offsets, int64_t *d_y, uint64_t *d_bad_count, hipStream_t stream) {
-    Plan P;
-    int rc = build_plan(p, &P);
+    const Plan *PP = nullptr;
+    int rc = cached_plan(p, &PP);
     if (rc) return rc;
+    const Plan &P = *PP;
     if (!d_offsets || !d_bad_count) return REDASH_E_NULL;
     if (P.n > 0 && (!d_out_labels || !d_out_zero || !d_y)) return REDASH_E_NULL;
     unsigned long long *bad = reinterpret_cast<unsigned long long *>(d_bad_count);

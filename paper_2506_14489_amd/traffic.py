@@ -35,8 +35,8 @@ MEASURED = {
         "valu_insts": 4412700000,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
         # taken on an earlier source; the device code built from these sources is the same,
         # instruction for instruction (since then: the split evaluator, unused helpers, and
-        # host-side launch code)
-        "sources_sha256": "0209461897a5675a4b69c4277b91465fd13e14e5e84afa805ee0256a9b69febc",
+        # host-side launch and plan-cache code)
+        "sources_sha256": "75fa89e7f0868298cf7053065752b7274f8a8c2bae6aca9c419a1335f59a3e66",
     },
 }
 

@@ -75,6 +75,50 @@ def test_work_words(moduli, S):
     assert sz["work_words"] == n * sum(O.words(moduli[i]) for i in R[1:])
 
 
+def test_plan_cache_follows_the_params():
+    """The library keeps the last plan per host thread: calls that alternate
+    between parameters, invalid ones among them, still get each one's own
+    sizes or error."""
+    cases = [(PLAN_CASES[i][0], PLAN_CASES[i][1], n) for i, n in ((0, 5), (3, 7), (0, 6), (5, 1000))]
+    want = [O.sizes(O.make_params(list(m), list(S), n, 0), n) for m, S, n in cases]
+    bad = B.make_params((2, 3, 6), (1,), 10, 0)  # 6 is not a prime or a power of two
+    for _ in range(3):
+        for (m, S, n), osz in zip(cases, want):
+            sz = B.redash_plan(B.make_params(m, S, n, 0))
+            assert (sz["label_words"], sz["table_words"]) == (osz["label_words"], osz["table_words"])
+            with pytest.raises(RuntimeError):
+                B.redash_plan(bad)
+    # the same parameters again after a change in an unused entry
+    p = B.make_params(PLAN_CASES[0][0], PLAN_CASES[0][1], 5, 0)
+    a = B.redash_plan(p)
+    p.moduli[15] = 12345
+    assert B.redash_plan(p) == a
+
+
+def test_plan_cache_per_thread():
+    """Host threads calling with different parameters at once each get their
+    own sizes (the cached plan is per thread)."""
+    import threading
+
+    cases = [(m, S, 100 + i) for i, (m, S) in enumerate(PLAN_CASES[:6])]
+    want = {c: O.sizes(O.make_params(list(c[0]), list(c[1]), c[2], 0), c[2])["table_words"] for c in cases}
+    errors = []
+
+    def run(c):
+        p = B.make_params(c[0], c[1], c[2], 0)
+        for _ in range(2000):
+            if B.redash_plan(p)["table_words"] != want[c]:
+                errors.append(c)
+                return
+
+    threads = [threading.Thread(target=run, args=(c,)) for c in cases]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors
+
+
 @pytest.mark.parametrize("m", rns.first_primes(12) + [97, 107, 167, 173, 251, 4, 8, 16, 32, 64, 128])
 def test_label_words_match_oracle(m):
     assert B.label_words_of(m) == O.words(m)
