@@ -161,6 +161,57 @@ SMALL = [
 ]
 
 
+def _random_bases(count: int, seed: int):
+    """Seeded random bases the library accepts: k from 2 to 15 moduli drawn
+    from the primes and powers of two up to 255 (at most one of them even),
+    P < 2^63, a random non-empty proper scaling set."""
+    rng = np.random.default_rng(seed)
+    accepted = [m for m in range(2, 256) if rns.is_prime(m) or (m & (m - 1)) == 0]
+    out = []
+    while len(out) < count:
+        k = int(rng.integers(2, 16))
+        base = sorted(int(m) for m in rng.choice(accepted, size=k, replace=False))
+        if sum(1 for m in base if m % 2 == 0) > 1 or rns.cardinality(base) >= 2 ** 63:
+            continue
+        t = int(rng.integers(1, k))
+        S = tuple(sorted(int(i) for i in rng.choice(k, size=t, replace=False)))
+        n = int(rng.integers(1, 400))
+        out.append((f"rand{len(out)}-k{k}-t{t}", tuple(base), S, n, 900 + len(out), int(rng.integers(0, 1 << 20))))
+    return out
+
+
+RANDOM_BASES = _random_bases(24, 2026)
+
+
+@pytest.mark.parametrize("case", RANDOM_BASES, ids=[c[0] for c in RANDOM_BASES])
+def test_random_bases_match_oracle(case):
+    """Garbled tables, offsets and zero-labels, and the evaluator's output
+    labels on the oracle's tables, word for word on seeded random bases;
+    every output decodes to the scaled value."""
+    name, moduli, S, n, seed, a0 = case
+    print(f"random base {name}: moduli={moduli} S={S} n={n} a0={a0}", flush=True)
+    bp, op = _params_pair(moduli, S, n, seed, a0)
+    offs, zin, zout, tab = O.garble(op, a0, n)
+    buf = B.Buffers(bp)
+    B.redash_garble_scale(bp, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.to_u32(buf.offsets), offs)
+    assert np.array_equal(H.to_u32(buf.in_zero), zin)
+    assert np.array_equal(H.to_u32(buf.out_zero), zout)
+    assert np.array_equal(H.to_u32(buf.tables)[: len(tab)], tab)
+    x = _small_inputs(moduli, n, seed)
+    X = O.encode(op, x, zin, offs)
+    Y = O.evaluate(op, a0, n, X, tab)
+    out = torch.empty(len(X), dtype=torch.int32, device="cuda")
+    work = torch.empty(max(B.redash_plan(bp)["work_words"], 1), dtype=torch.int32, device="cuda")
+    B.redash_eval_scale(bp, H.to_dev(X), H.to_dev(tab), out, work)
+    torch.cuda.synchronize()
+    got = H.to_u32(out)
+    assert np.array_equal(got, Y)
+    y, bad = O.decode(op, got, zout, offs)
+    assert bad.sum() == 0 and np.array_equal(y, _scaled(x, moduli, S))
+
+
 def _small_inputs(moduli, n, seed):
     P = rns.cardinality(moduli)
     rng = np.random.default_rng(seed + 1000)
@@ -502,6 +553,20 @@ def test_one_gadget_per_lane_on_varied_bases(name, moduli, S):
     n = 2 * cus * 384 + 1
     P = rns.cardinality(moduli)
     w = WL.Workload(f"lane-{name}", tuple(moduli), tuple(S), n, 70 + len(moduli), "uniform", -(P // 2), P - P // 2)
+    _check_full(w, 2048, 2048, 2048, 8)
+
+
+RANDOM_LANE_BASES = [c[:3] for c in _random_bases(4, 7207)]
+
+
+@pytest.mark.parametrize("name,moduli,S", RANDOM_LANE_BASES, ids=[b[0] for b in RANDOM_LANE_BASES])
+def test_one_gadget_per_lane_on_random_bases(name, moduli, S):
+    """Seeded random bases on the one-gadget-per-lane evaluator (one gadget
+    past the sizes that run on the split evaluator)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 2 * cus * 384 + cus * 64 + 1
+    P = rns.cardinality(moduli)
+    w = WL.Workload(f"lane-{name}", tuple(moduli), tuple(S), n, 80 + len(moduli), "uniform", -(P // 2), P - P // 2)
     _check_full(w, 2048, 2048, 2048, 8)
 
 
