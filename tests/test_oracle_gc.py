@@ -11,9 +11,11 @@
   right label for every input value; colours are distinct.
 * Result (Sec. 3.2): decode gives floor(x/s) for every input of small bases.
 
-Parity of the label bits themselves is unpinned by the paper (it fixes no
-hash, PRG or encoding); those are the design choices of the oracle and the
-HIP library, which are implemented twice without shared code.
+The paper fixes no hash, PRG or encoding: those are this design's
+construction, pinned bit for bit by a second statement on Python integers
+with libcrypto's AES (fold, sigma, tweak words, feed-forward, digits, PRG
+counters) and by known-answer files in tests/test_oracle_spec.py; the HIP
+library implements them once more without shared code.
 """
 
 import ctypes
