@@ -79,7 +79,7 @@ struct LinPlan {
     uint32_t xt, xtiles;          // output positions per tile, tiles per row
     uint32_t ck, kc, taps, ncc;   // channel chunk, K bytes per chunk (64-padded), kh kw, chunks
     uint32_t lg_ck;
-    uint32_t kw_magic;            // floor(t / kw) = umulhi(t, kw_magic) for every tap t < 64
+    uint32_t kw_magic;            // floor(t / kw) = (t kw_magic) >> 16 for every tap t < 64
     uint32_t o_pad, ogroups;      // c_out rounded up to 64, its groups of 64
     uint32_t astride;             // LDS bytes per staged weight row
     uint32_t ostride;             // words per output-channel row of the merged output words
@@ -185,8 +185,11 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     L->cp = L->ncc * ck;
     L->hp = L->in_rows + 2 * p->pad;
     L->wp = L->in_cols + 2 * p->pad;
-    // with M = ceil(2^32 / kw), umulhi(t, M) = floor(t / kw) whenever t kw < 2^32
-    L->kw_magic = static_cast<uint32_t>(((1ull << 32) + p->kw - 1) / p->kw);
+    // M = ceil(2^16 / kw) <= 2^16: with e = M kw - 2^16 < kw, (t M) >> 16 =
+    // floor(t/kw + t e / (kw 2^16)), and t e / 2^16 < 64 kw / 2^16 < 1 keeps
+    // the error below 1/kw for every tap t < 64 and kw <= 64 (t M < 2^22: a
+    // 24-bit multiply).  (2^32 / kw would not fit 32 bits for kw = 1.)
+    L->kw_magic = ((1u << 16) + p->kw - 1) / p->kw;
     L->o_pad = round_up(p->c_out, kLinOTile);
     L->ogroups = L->o_pad / kLinOTile;
     // 16-byte LDS reads of 16 rows (or columns) at a stride of S bytes, four
@@ -678,7 +681,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
                     const uint32_t kidx = kk * 64 + kg;
                     uint32_t tap = kidx >> L.lg_ck;
                     if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
-                    const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+                    const uint32_t dy = __umul24(tap, L.kw_magic) >> 16, dx = tap - dy * L.kw;
                     const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
 #pragma unroll
                     for (int cb = 0; cb < NCB; ++cb) {
@@ -941,7 +944,7 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                     const uint32_t kidx = kk * 64 + kg;
                     uint32_t tap = kidx >> L.lg_ck;
                     if (tap >= L.taps) tap = 0;  // K padding: the weights there are 0
-                    const uint32_t dy = __umulhi(tap, L.kw_magic), dx = tap - dy * L.kw;
+                    const uint32_t dy = __umul24(tap, L.kw_magic) >> 16, dx = tap - dy * L.kw;
                     const uint32_t boff = dy * rowb + dx * L.xstride + (kidx & (L.ck - 1u));
 #pragma unroll
                     for (int cb = 0; cb < NCB; ++cb) {

@@ -57,12 +57,50 @@ SMALL = [
     ("conv3x3-64ch-stride2", (2, 3, 5, 7), (2, 64, 9, 20), 6, 3, 3, 2, 1),
     ("conv3x3-64ch-m251-three-groups", (2, 251), (1, 64, 5, 9), 130, 3, 3, 1, 1),
     ("conv3x3-64ch-whole-tiles", (5, 7, 64), (1, 64, 3, 64), 64, 3, 3, 1, 1),
+    # kernels one column wide and taller than one row (the tap's row and column
+    # from one division by kw = 1), and one row high
+    ("conv-3x1", (2, 3, 5, 7), (1, 20, 9, 7), 6, 3, 1, 1, 0),
+    ("conv-5x1-two-chunks", (3, 4, 5, 13), (2, 119, 9, 6), 5, 5, 1, 1, 0),
+    ("conv-2x1-stride3-two-chunks", (3, 4, 5, 13), (2, 119, 9, 6), 5, 2, 1, 3, 0),
+    ("conv-1x3", (2, 3, 5, 7, 11), (1, 33, 5, 12), 9, 1, 3, 1, 0),
 ]
 
 
-@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def _random_linear(count: int, seed: int):
+    """Seeded random layers: bases of 1 to 6 moduli drawn mostly from the
+    small ones (2, 3, 4, 5, 7, 8, 11, 13, 16, whose residues share plane
+    bytes) and some larger, at most one of them even; random shapes, kernels,
+    strides and padding that the plan accepts."""
+    rng = np.random.default_rng(seed)
+    small = [2, 3, 4, 5, 7, 8, 11, 13, 16]
+    large = [17, 19, 23, 29, 31, 32, 37, 41, 64, 97, 127, 128, 251]
+    out = []
+    while len(out) < count:
+        k = int(rng.integers(1, 7))
+        pool = small if rng.random() < 0.7 else small + large
+        base = sorted(int(m) for m in rng.choice(pool, size=min(k, len(pool)), replace=False))
+        if sum(1 for m in base if m % 2 == 0) > 1:
+            continue
+        kh, kw = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        shape = (int(rng.integers(1, 3)), int(rng.integers(1, 131)), int(rng.integers(kh, 13)),
+                 int(rng.integers(kw, 13)))
+        c_out = int(rng.integers(1, 81))
+        stride = int(rng.integers(1, 4))
+        pad = int(rng.integers(0, min(kh, kw)))
+        lp = B.make_linear_params(tuple(base), *shape, c_out, kh, kw, stride, pad)
+        if B.linear_plan_rc(lp) != 0:
+            continue
+        out.append((f"rand{len(out)}-{'-'.join(map(str, base))}", tuple(base), shape, c_out, kh, kw, stride, pad))
+    return out
+
+
+RANDOM_LINEAR = _random_linear(16, 4242)
+
+
+@pytest.mark.parametrize("case", SMALL + RANDOM_LINEAR, ids=[c[0] for c in SMALL + RANDOM_LINEAR])
 def test_linear_matches_oracle(case):
     name, moduli, shape, c_out, kh, kw, stride, pad = case
+    print(f"linear {name}: moduli={moduli} shape={shape} c_out={c_out} k={kh}x{kw} s={stride} p={pad}", flush=True)
     n, c_in, h, w = shape
     rng = np.random.default_rng(zlib.crc32(name.encode()))
     lp = B.make_linear_params(moduli, n, c_in, h, w, c_out, kh, kw, stride, pad)
