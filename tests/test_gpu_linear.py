@@ -97,6 +97,44 @@ def _random_linear(count: int, seed: int):
 RANDOM_LINEAR = _random_linear(16, 4242)
 
 
+def _random_linear_wide(count: int, seed: int):
+    """Seeded random layers over wider shapes: any accepted modulus up to 251,
+    dense layers of up to 300 inputs and 40 rows, convolutions of up to 199
+    channels (several channel chunks), up to 139 outputs (several groups of
+    64), kernels up to 7x7 (at most 64 taps), strides 1 to 4; sized so that
+    the oracle's plain convolution stays small."""
+    rng = np.random.default_rng(seed)
+    pool = [2, 3, 4, 5, 7, 8, 11, 13, 16, 17, 19, 23, 29, 31, 32, 37, 41, 64, 97, 127, 128, 251]
+    out = []
+    while len(out) < count:
+        k = int(rng.integers(1, 7))
+        base = sorted(int(m) for m in rng.choice(pool, size=k, replace=False))
+        if sum(1 for m in base if m % 2 == 0) > 1:
+            continue
+        if rng.random() < 0.25:
+            shape, kh, kw, stride, pad = (int(rng.integers(1, 40)), int(rng.integers(1, 300)), 1, 1), 1, 1, 1, 0
+        else:
+            kh, kw = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+            if kh * kw > 64:
+                continue
+            shape = (int(rng.integers(1, 3)), int(rng.integers(1, 200)), int(rng.integers(kh, 11)),
+                     int(rng.integers(kw, 11)))
+            stride, pad = int(rng.integers(1, 5)), int(rng.integers(0, min(kh, kw)))
+        c_out = int(rng.integers(1, 140))
+        n, c_in, h, w = shape
+        ho, wo = (h + 2 * pad - kh) // stride + 1, (w + 2 * pad - kw) // stride + 1
+        if n * ho * wo * c_out * c_in * kh * kw * sum(OL.label_lambda(m) for m in base) > 3e8:
+            continue
+        lp = B.make_linear_params(tuple(base), *shape, c_out, kh, kw, stride, pad)
+        if B.linear_plan_rc(lp) != 0:
+            continue
+        out.append((f"wide{len(out)}-{'-'.join(map(str, base))}", tuple(base), shape, c_out, kh, kw, stride, pad))
+    return out
+
+
+RANDOM_LINEAR += _random_linear_wide(32, 777)
+
+
 @pytest.mark.parametrize("case", SMALL + RANDOM_LINEAR, ids=[c[0] for c in SMALL + RANDOM_LINEAR])
 def test_linear_matches_oracle(case):
     name, moduli, shape, c_out, kh, kw, stride, pad = case
