@@ -236,7 +236,7 @@ def test_garble_matches_oracle(case):
     assert np.array_equal(H.to_u32(buf.tables)[: len(tab)], tab)
 
 
-@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("case", SMALL + RANDOM_BASES, ids=[c[0] for c in SMALL + RANDOM_BASES])
 def test_garble_on_given_zero_labels_matches_oracle(case):
     """redash_garble_scale_given on arbitrary valid zero-labels (as a free
     operation would leave them) against the oracle, word for word; the
@@ -274,7 +274,7 @@ def test_eval_on_oracle_tables_matches_oracle(case):
     assert bad.sum() == 0 and np.array_equal(y, _scaled(x, moduli, S))
 
 
-@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("case", SMALL + RANDOM_BASES, ids=[c[0] for c in SMALL + RANDOM_BASES])
 def test_encode_and_decode_match_oracle(case):
     name, moduli, S, n, seed, a0 = case
     bp, op = _params_pair(moduli, S, n, seed, a0)
