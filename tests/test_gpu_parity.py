@@ -570,6 +570,27 @@ def test_one_gadget_per_lane_on_random_bases(name, moduli, S):
     _check_full(w, 2048, 2048, 2048, 8)
 
 
+# Seeded random bases (up to 6 moduli) at one size in each launch regime of
+# the evaluator, as multiples of the CU count: the 12-wave split, the 4-wave
+# split, a full 4-wave round and its rest, the 2-wave split, a full 2-wave
+# round and its rest, and whole one-gadget-per-lane rounds with a rest.
+REGIME_SIZES = [("split12", 0, 60, 7), ("split4", 0, 250, 11), ("split4-round-rest", 2 * 192, 40, 3),
+                ("split2", 0, 600, 13), ("split2-round-rest", 2 * 384, 20, 5), ("lane-rounds-rest", 2 * 768, 100, 9)]
+REGIME_BASES = [b for b in _random_bases(60, 3131) if len(b[1]) <= 6][: len(REGIME_SIZES)]
+
+
+@pytest.mark.parametrize("regime,base", list(zip(REGIME_SIZES, REGIME_BASES)), ids=[r[0] for r in REGIME_SIZES])
+def test_launch_regimes_on_random_bases(regime, base):
+    name, rounds_per_cu, per_cu, extra = regime
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = cus * (rounds_per_cu + per_cu) + extra
+    _, moduli, S = base[:3]
+    P = rns.cardinality(moduli)
+    w = WL.Workload(f"regime-{name}-{base[0]}", tuple(moduli), tuple(S), n, 90 + len(moduli), "uniform", -(P // 2),
+                    P - P // 2)
+    _check_full(w, 2048, 2048, 2048, 8)
+
+
 @pytest.mark.parametrize("layer", WL.RESNET18, ids=[w.name for w in WL.RESNET18])
 def test_full_size_resnet18_layer(layer):
     if layer.n >= 400_000:  # the stem, run like the benchmark workload
