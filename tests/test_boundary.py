@@ -154,6 +154,43 @@ def test_bad_params_rejected_like_the_oracle(moduli, S):
         assert O.check_params(O.make_params(moduli, S, 1, 0)) == -1
 
 
+def test_random_params_accepted_and_sized_like_the_oracle():
+    """600 seeded random parameter sets, valid and not (any integer 0..300 as a
+    modulus, unsorted or repeated moduli, several even moduli, scaling indices
+    out of range, repeated or unsorted, t = 0 or k, k up to 16): the library
+    accepts exactly those the oracle accepts, and sizes those the same way."""
+    import numpy as np
+
+    rng = np.random.default_rng(515)
+    accepted = 0
+    for _ in range(600):
+        k = int(rng.integers(1, 17))
+        if rng.random() < 0.5:
+            pool = [m for m in range(2, 256) if rns.is_prime(m) or (m & (m - 1)) == 0]
+            moduli = sorted(int(m) for m in rng.choice(pool, size=k, replace=False))
+        else:
+            moduli = [int(m) for m in rng.integers(0, 301, size=k)]
+        t = int(rng.integers(0, k + 1))
+        if rng.random() < 0.7:
+            S = sorted(int(i) for i in rng.choice(k, size=t, replace=False))
+        else:
+            S = [int(i) for i in rng.integers(0, k + 2, size=t)]
+        n = int(rng.integers(0, 5000))
+        ok_lib = B.plan_rc(B.make_params(moduli, S, n, 0)) == 0
+        if k > 15:  # the oracle's struct holds at most 16; the library takes at most 15
+            assert not ok_lib
+            continue
+        ok_orc = O.check_params(O.make_params(moduli, S, n, 0)) == 0
+        assert ok_lib == ok_orc, (moduli, S)
+        if ok_lib:
+            accepted += 1
+            sz = B.redash_plan(B.make_params(moduli, S, n, 0))
+            osz = O.sizes(O.make_params(list(moduli), list(S), n, 0), n)
+            assert (sz["label_words"], sz["table_words"], sz["gates"]) == (
+                osz["label_words"], osz["table_words"], osz["gates"])
+    assert accepted > 50  # 71 with this seed
+
+
 def test_null_params():
     L = B.lib()
     s = B.Sizes()
