@@ -58,7 +58,14 @@ HASH_PAIRS = [(2, 3), (3, 2), (37, 2), (2, 37), (11, 13), (5, 3), (37, 31), (17,
               (41, 197), (241, 59), (61, 47), (53, 211)]
 
 
-@pytest.mark.parametrize("q,m", HASH_PAIRS)
+# every modulus the library accepts as the hash's output modulus (its pad's
+# digit extraction), each with a seeded random input modulus
+_ACCEPTED = [m for m in range(2, 256) if rns.is_prime(m) or (m & (m - 1)) == 0]
+HASH_EVERY_M = [(int(q), m) for q, m in zip(np.random.default_rng(99).choice(_ACCEPTED, size=len(_ACCEPTED)),
+                                             _ACCEPTED)]
+
+
+@pytest.mark.parametrize("q,m", HASH_PAIRS + HASH_EVERY_M)
 def test_hash_matches_oracle(q, m):
     count = 300
     rng = np.random.default_rng(q * 1000 + m)
