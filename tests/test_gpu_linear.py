@@ -289,6 +289,34 @@ CHAIN = [
 ]
 
 
+def _random_chain(count: int, seed: int):
+    """Seeded random layer-then-gadget cases: bases of 2 to 8 moduli with
+    P > 2^26 (the layer's outputs, at most 9 * 7 * 7 * 8 * 20 + 100 in size,
+    stay inside the signed range), a random scaling set, a random square
+    kernel, stride and padding."""
+    from oracle import rns
+
+    rng = np.random.default_rng(seed)
+    pool = [m for m in range(2, 256) if rns.is_prime(m) or (m & (m - 1)) == 0]
+    out = []
+    while len(out) < count:
+        k = int(rng.integers(2, 9))
+        base = sorted(int(m) for m in rng.choice(pool, size=k, replace=False))
+        P = rns.cardinality(base)
+        if sum(1 for m in base if m % 2 == 0) > 1 or not (1 << 26) < P < (1 << 63):
+            continue
+        t = int(rng.integers(1, k))
+        S = tuple(sorted(int(i) for i in rng.choice(k, size=t, replace=False)))
+        ks = int(rng.integers(1, 4))
+        shape = (int(rng.integers(1, 3)), int(rng.integers(1, 10)), int(rng.integers(ks, 8)), int(rng.integers(ks, 8)))
+        out.append((f"rand{len(out)}-k{k}-t{t}", tuple(base), S, shape, int(rng.integers(1, 7)), ks,
+                    int(rng.integers(1, 3)), int(rng.integers(0, ks))))
+    return out
+
+
+CHAIN += _random_chain(4, 5150)
+
+
 @pytest.mark.parametrize("case", CHAIN, ids=[c[0] for c in CHAIN])
 def test_layer_feeds_gadget_matches_oracle(case):
     from oracle import oracle as O
