@@ -449,21 +449,25 @@ k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__re
         const uint32_t src = gate_src(P.gate[g]);
         uint32_t r = 1;
         while (g + r < P.G && gate_src(P.gate[g + r]) == src) ++r;
+        const ModConst mq = P.mod[src];
+        const uint32_t q = mq.m;
+        // Every gate of the run hashes the same digit label: the wave reads,
+        // folds and colours it once per run.
+        uint32_t x[4] = {0, 0, 0, 0}, colour = 0;
+        if (live && part < r) {
+            const uint32_t *dig = LB.base(gate_dsrc(P.gate[g + part]), mq);
+            const uint32_t w0 = LB.get(dig, 0);
+            x[0] = w0;
+            static_for<kMaxW - 1>([&](auto w1) {
+                constexpr int w = decltype(w1)::value + 1;
+                if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
+            });
+            colour = w0 & mq.mask;
+            if (colour >= q) colour = 0;
+        }
         for (uint32_t i = 0; i < r; ++i) {
             const uint32_t d = P.gate[g + i];
-            const ModConst mq = P.mod[src];
-            const uint32_t q = mq.m;
             if (i % split == part && live) {
-                // the digit label: fold and colour (see k_eval)
-                const uint32_t *dig = LB.base(gate_dsrc(d), mq);
-                const uint32_t w0 = LB.get(dig, 0);
-                uint32_t x[4] = {w0, 0, 0, 0};
-                static_for<kMaxW - 1>([&](auto w1) {
-                    constexpr int w = decltype(w1)::value + 1;
-                    if (w < static_cast<int>(mq.W)) x[w & 3] ^= LB.get(dig, w);
-                });
-                uint32_t colour = w0 & mq.mask;
-                if (colour >= q) colour = 0;
                 const ModConst mm = P.mod[gate_dst(d)];
                 const uint32_t Wd = mm.W;
                 // the row (right-aligned, as the register labels)
