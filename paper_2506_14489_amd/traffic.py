@@ -36,7 +36,7 @@ MEASURED = {
         # taken on an earlier source; the device code built from these sources is the same,
         # instruction for instruction (since then: the split evaluator, unused helpers, and
         # host-side launch and plan-cache code)
-        "sources_sha256": "75fa89e7f0868298cf7053065752b7274f8a8c2bae6aca9c419a1335f59a3e66",
+        "sources_sha256": "e6d1a6279b70e9d1e1a73c72b80385963d4abc5d5bd31cfa73994043a2f59999",
     },
 }
 
