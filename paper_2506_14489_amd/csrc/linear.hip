@@ -915,6 +915,9 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                 };
                 v4i fa0[4], fb0[NCB], fa1[4], fb1[NCB];
                 frag(0, fa0, fb0);
+                // the wave's priority is raised while it issues its
+                // matrix-core steps and lowered for the staging and epilogue
+                __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int kk = 0; kk < 9; ++kk) {
                     // (scheduling barriers keep the loads of step kk + 1
@@ -930,6 +933,7 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
+                __builtin_amdgcn_s_setprio(0);
             } else {
 #pragma unroll
                 for (int ob = 0; ob < 4; ++ob)
