@@ -168,8 +168,14 @@ __device__ __forceinline__ PermTE02 perm_te02() {
 
 // NB independent blocks encrypted round by round, so that the table reads of
 // all blocks are in flight together.
+//
+// The wave's priority is raised for the rounds and lowered after them: when
+// several waves of a SIMD have an instruction ready, one in its AES rounds
+// (which keep the LDS pipe busy with table reads) issues before one in other
+// work (mostly VALU), so the two pipes stay busy together.
 template <int NB, typename Tab, typename Key>
 __device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB][4], const Key &K) {
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -195,6 +201,7 @@ __device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB]
         s[b][2] = T.last_column(s2, s3, s0, s1, K, 42);
         s[b][3] = T.last_column(s3, s0, s1, s2, K, 43);
     }
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // One block held as four little-endian column words, on the four tables.

@@ -30,13 +30,10 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 13309405.2,  # mean of four dispatches: 13,306,211 .. 13,311,067
-        "write_kib": 2271030.5,  # mean of four dispatches: 2,270,958 .. 2,271,093
-        "valu_insts": 4412700000,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
-        # taken on an earlier source; the device code built from these sources is the same,
-        # instruction for instruction (since then: the split evaluator, unused helpers, and
-        # host-side launch and plan-cache code)
-        "sources_sha256": "e6d1a6279b70e9d1e1a73c72b80385963d4abc5d5bd31cfa73994043a2f59999",
+        "fetch_kib": 13336422.0,  # mean of four dispatches: 13,332,968 .. 13,338,124
+        "write_kib": 2272711.75,  # mean of four dispatches: 2,272,655 .. 2,272,790
+        "valu_insts": 4412696442,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
+        "sources_sha256": "2514338403f38a37ff37afd87ccf301745f45c40ad89694e2ade87581546fb51",
     },
 }
 
