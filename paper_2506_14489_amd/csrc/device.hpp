@@ -173,7 +173,7 @@ __device__ __forceinline__ PermTE02 perm_te02() {
 // several waves of a SIMD have an instruction ready, one in its AES rounds
 // (which keep the LDS pipe busy with table reads) issues before one in other
 // work (mostly VALU), so the two pipes stay busy together.
-template <int NB, typename Tab, typename Key>
+template <int NB, bool PAIRED = false, typename Tab, typename Key>
 __device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB][4], const Key &K) {
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
@@ -181,25 +181,53 @@ __device__ __forceinline__ void aes128_encrypt_n(const Tab &T, uint32_t (&s)[NB]
 #pragma unroll
         for (int c = 0; c < 4; ++c) s[b][c] ^= K(c);
     // Rounds 1..9 stay a loop (the round keys are uniform loads): the
-    // instruction cache holds the whole gate loop that way.
-#pragma unroll 1
-    for (int r = 1; r < 10; ++r) {
+    // instruction cache holds the whole gate loop that way.  A round's new
+    // state needs registers of its own while the old one is read, so a loop
+    // of one round per pass copies the state back at the end of every pass.
+    // PAIRED takes two rounds per pass, the state going to t and back to s,
+    // without the copies; it holds more values live, which pays only where
+    // the kernel has registers to spare.
+    auto round_to = [&](const uint32_t(&in)[NB][4], uint32_t(&o)[NB][4], int r) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-            s[b][0] = T.column(s0, s1, s2, s3, K, 4 * r);
-            s[b][1] = T.column(s1, s2, s3, s0, K, 4 * r + 1);
-            s[b][2] = T.column(s2, s3, s0, s1, K, 4 * r + 2);
-            s[b][3] = T.column(s3, s0, s1, s2, K, 4 * r + 3);
+            o[b][0] = T.column(in[b][0], in[b][1], in[b][2], in[b][3], K, 4 * r);
+            o[b][1] = T.column(in[b][1], in[b][2], in[b][3], in[b][0], K, 4 * r + 1);
+            o[b][2] = T.column(in[b][2], in[b][3], in[b][0], in[b][1], K, 4 * r + 2);
+            o[b][3] = T.column(in[b][3], in[b][0], in[b][1], in[b][2], K, 4 * r + 3);
         }
-    }
+    };
+    auto last_round = [&](const uint32_t(&in)[NB][4]) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-        const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
-        s[b][0] = T.last_column(s0, s1, s2, s3, K, 40);
-        s[b][1] = T.last_column(s1, s2, s3, s0, K, 41);
-        s[b][2] = T.last_column(s2, s3, s0, s1, K, 42);
-        s[b][3] = T.last_column(s3, s0, s1, s2, K, 43);
+        for (int b = 0; b < NB; ++b) {
+            const uint32_t s0 = in[b][0], s1 = in[b][1], s2 = in[b][2], s3 = in[b][3];
+            s[b][0] = T.last_column(s0, s1, s2, s3, K, 40);
+            s[b][1] = T.last_column(s1, s2, s3, s0, K, 41);
+            s[b][2] = T.last_column(s2, s3, s0, s1, K, 42);
+            s[b][3] = T.last_column(s3, s0, s1, s2, K, 43);
+        }
+    };
+    if constexpr (PAIRED) {
+        uint32_t t[NB][4];
+#pragma unroll 1
+        for (int r = 1; r < 9; r += 2) {
+            round_to(s, t, r);
+            round_to(t, s, r + 1);
+        }
+        round_to(s, t, 9);
+        last_round(t);
+    } else {
+#pragma unroll 1
+        for (int r = 1; r < 10; ++r) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const uint32_t s0 = s[b][0], s1 = s[b][1], s2 = s[b][2], s3 = s[b][3];
+                s[b][0] = T.column(s0, s1, s2, s3, K, 4 * r);
+                s[b][1] = T.column(s1, s2, s3, s0, K, 4 * r + 1);
+                s[b][2] = T.column(s2, s3, s0, s1, K, 4 * r + 2);
+                s[b][3] = T.column(s3, s0, s1, s2, K, 4 * r + 3);
+            }
+        }
+        last_round(s);
     }
     __builtin_amdgcn_s_setprio(0);
 }
@@ -641,7 +669,7 @@ __device__ __forceinline__ void hash_fraction(const uint32_t *T, uint32_t x0, ui
 // The hash fractions of NG gates that share one input label (folded into
 // x0..x3): gate j uses tweak tau + j and two blocks (a gate whose output
 // modulus is 2 only reads V[j][0..3]).
-template <int NG, typename Tab, typename Key>
+template <int NG, bool PAIRED = false, typename Tab, typename Key>
 __device__ __forceinline__ void hash_fraction_n(const Tab &T, const Key &rk, uint32_t x0, uint32_t x1, uint32_t x2,
                                                 uint32_t x3, uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
     const uint32_t u0 = x2, u1 = x3, u2 = x2 ^ x0, u3 = x3 ^ x1;
@@ -660,7 +688,7 @@ __device__ __forceinline__ void hash_fraction_n(const Tab &T, const Key &rk, uin
             s[2 * j + h][3] = u3 ^ gid;
         }
     }
-    aes128_encrypt_n<2 * NG>(T, s, rk);
+    aes128_encrypt_n<2 * NG, PAIRED>(T, s, rk);
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
 #pragma unroll

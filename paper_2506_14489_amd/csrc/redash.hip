@@ -483,7 +483,7 @@ k_eval_split(const Plan P, const uint32_t *__restrict__ in, const uint32_t *__re
                 uint32_t T[kMaxW];
                 load_label(T, LB, gate_tsrc(d), mm, gate_tsrc(d) != kLocZero);
                 uint32_t Vn[1][8];
-                hash_fraction_n<1>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g + i, P.gid, Vn);
+                hash_fraction_n<1, true>(TT, LdsKey{K}, x[0], x[1], x[2], x[3], tau0 + g + i, P.gid, Vn);
                 const uint32_t e = gate_dst(d) | (gate_kind(d) << 4) | (gate_tab(d) << 5) | (gate_coeff(d) << 6);
                 reg_update(g + i, e, mm, Vn[0], row, T);
                 store_label(T, LB, gate_tdst(d), mm);
