@@ -674,30 +674,34 @@ __device__ __forceinline__ void hash_fraction_n(const Tab &T, const Key &rk, uin
                                                 uint32_t x3, uint64_t tau, uint32_t gid, uint32_t (&V)[NG][8]) {
     const uint32_t u0 = x2, u1 = x3, u2 = x2 ^ x0, u3 = x3 ^ x1;
     uint32_t s[2 * NG][4];
-    uint32_t k0[2 * NG], k1[2 * NG];
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const uint64_t tw = (tau + static_cast<uint64_t>(j)) * 4u + static_cast<uint64_t>(h);
-            k0[2 * j + h] = static_cast<uint32_t>(tw);
-            k1[2 * j + h] = static_cast<uint32_t>(tw >> 32);
-            s[2 * j + h][0] = u0 ^ k0[2 * j + h];
-            s[2 * j + h][1] = u1 ^ k1[2 * j + h];
+            s[2 * j + h][0] = u0 ^ static_cast<uint32_t>(tw);
+            s[2 * j + h][1] = u1 ^ static_cast<uint32_t>(tw >> 32);
             s[2 * j + h][2] = u2;
             s[2 * j + h][3] = u3 ^ gid;
         }
     }
     aes128_encrypt_n<2 * NG, PAIRED>(T, s, rk);
+    // Matyas-Meyer-Oseas feed-forward of the block input u ^ T.  The inputs
+    // are formed again from x and tau rather than kept through the rounds
+    // (opaque keeps the compiler from reusing the earlier values): six
+    // registers live across the AES instead of up to twelve.
+    const uint32_t y0 = opaque(x0), y1 = opaque(x1), y2 = opaque(x2), y3 = opaque(x3);
+    const uint64_t tau2 = (static_cast<uint64_t>(opaque(static_cast<uint32_t>(tau >> 32))) << 32) |
+                          opaque(static_cast<uint32_t>(tau));
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            // Matyas-Meyer-Oseas feed-forward of the block input u ^ T
-            V[j][4 * h + 0] = s[2 * j + h][0] ^ u0 ^ k0[2 * j + h];
-            V[j][4 * h + 1] = s[2 * j + h][1] ^ u1 ^ k1[2 * j + h];
-            V[j][4 * h + 2] = s[2 * j + h][2] ^ u2;
-            V[j][4 * h + 3] = s[2 * j + h][3] ^ u3 ^ gid;
+            const uint64_t tw = (tau2 + static_cast<uint64_t>(j)) * 4u + static_cast<uint64_t>(h);
+            V[j][4 * h + 0] = s[2 * j + h][0] ^ y2 ^ static_cast<uint32_t>(tw);
+            V[j][4 * h + 1] = s[2 * j + h][1] ^ y3 ^ static_cast<uint32_t>(tw >> 32);
+            V[j][4 * h + 2] = s[2 * j + h][2] ^ y2 ^ y0;
+            V[j][4 * h + 3] = s[2 * j + h][3] ^ y3 ^ y1 ^ gid;
         }
     }
 }

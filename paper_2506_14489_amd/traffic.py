@@ -30,12 +30,10 @@ WRITE_FACTOR = 1048576 / 1048576
 MEASURED = {
     "batched": {
         "kernel": "k_eval",
-        "fetch_kib": 13336422.0,  # mean of four dispatches: 13,332,968 .. 13,338,124
-        "write_kib": 2272711.75,  # mean of four dispatches: 2,272,655 .. 2,272,790
-        "valu_insts": 4412696442,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
-        # taken on an earlier source; k_eval built from these sources is the same, instruction
-        # for instruction (since then: the split evaluator's AES rounds two per loop pass)
-        "sources_sha256": "d29bc00a57831fdbc861ce2af063e1f38a33aad32e4f49c557b799c7d8449385",
+        "fetch_kib": 12965419.0,  # mean of four dispatches: 12,964,332 .. 12,966,117
+        "write_kib": 1404928.0,  # four dispatches, equal
+        "valu_insts": 4382490490,  # SQ_INSTS_VALU per dispatch (wave instructions; two dispatches, equal)
+        "sources_sha256": "b3f36e4997a0ab6a67ffa26bf5807a1bb3cc0c5851e32c83f009608848f52bd3",
     },
 }
 
