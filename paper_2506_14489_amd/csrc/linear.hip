@@ -219,6 +219,9 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     while (L->xt > 16 && L->xt / 2 >= L->cols) L->xt /= 2;
     auto pieces = [&](uint32_t xt) { return L->kh * ((xt - 1) * p->stride + p->kw) * (ck / 16); };
     if (L->xt == 32 && pieces(32) > 2 * kLinBlock) L->xt = 16;
+    // a 3x3 kernel over several 64-channel chunks keeps the next chunk's
+    // weights in registers, which only the 16-position tile has room for
+    if (L->ncc > 1 && ck == 64 && p->kh == 3 && p->kw == 3) L->xt = 16;
     if (pieces(L->xt) > 2 * kLinBlock) return REDASH_E_PARAM;
     L->xw = (L->xt - 1) * p->stride + p->kw;
     L->halo = L->kh * L->xw * L->xstride;
@@ -227,7 +230,8 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     // the merged output words overlay the staged inputs (used at the end of
     // a packed word, after every wave has read its fragments)
     L->lds_o = kLinOTile * L->ostride * 4;
-    L->lds_bytes = L->lds_a + (L->lds_b > L->lds_o ? L->lds_b : L->lds_o);
+    // then the accumulator seeds of the 64 output channels (base, -b mod m)
+    L->lds_bytes = L->lds_a + (L->lds_b > L->lds_o ? L->lds_b : L->lds_o) + 2 * kLinOTile * 4;
     if (L->lds_bytes > kLinMaxLds) return REDASH_E_PARAM;
     L->xtiles = (L->cols + L->xt - 1) / L->xt;
     L->plane_bytes = static_cast<uint64_t>(L->nimg) * L->hp * L->wp * L->cp;
@@ -513,26 +517,27 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     // output channel of element r of row block ob for this lane
     auto o_local = [&](int ob, int r) -> uint32_t { return ob * 16 + 4 * (lane / 16) + r; };
 
-    // The accumulators start at base[ob][r] = 128 rowsum (m > 128) + off
-    // (+ (-b mod m) R_j for the garbler) and end at u = sum w v + off (+ ...)
-    // in [0, 2^31) with u / m < 2^23.
-    const bool shifted = M.m > 128;
-    uint32_t base[4][4], negb[4][4];
-#pragma unroll
-    for (int ob = 0; ob < 4; ++ob)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            base[ob][r] = (shifted ? static_cast<uint32_t>(128 * rowsum[o_local(ob, r)]) : 0u) + M.off;
-            negb[ob][r] = 0;
-            if constexpr (GARBLE) {
-                const uint32_t o = og * kLinOTile + o_local(ob, r);
-                if (bias && o < L.c_out) {
-                    int64_t bm = bias[o] % static_cast<int64_t>(M.m);
-                    if (bm < 0) bm += M.m;
-                    negb[ob][r] = (M.m - static_cast<uint32_t>(bm)) % M.m;
-                }
+    // The accumulators start at base = 128 rowsum (m > 128) + off (+ (-b mod
+    // m) R_j for the garbler) and end at u = sum w v + off (+ ...) in
+    // [0, 2^31) with u / m < 2^23.  The 64 output channels' base and -b mod m
+    // sit in LDS after the staging area (read at each residue's first chunk).
+    uint32_t *sbase = reinterpret_cast<uint32_t *>(lds + L.lds_bytes - 2 * kLinOTile * 4);
+    uint32_t *snegb = sbase + kLinOTile;
+    if (tid < kLinOTile) {
+        const bool shifted = M.m > 128;
+        sbase[tid] = (shifted ? static_cast<uint32_t>(128 * rowsum[tid]) : 0u) + M.off;
+        uint32_t nb = 0;
+        if constexpr (GARBLE) {
+            const uint32_t o = og * kLinOTile + tid;
+            if (bias && o < L.c_out) {
+                int64_t bm = bias[o] % static_cast<int64_t>(M.m);
+                if (bm < 0) bm += M.m;
+                nb = (M.m - static_cast<uint32_t>(bm)) % M.m;
             }
         }
+        snegb[tid] = nb;
+    }
+    __syncthreads();
 
     // This thread's (at most two) staged pieces: piece e = tid + 256 t of a
     // residue's halo is (row dy, column xin, 16 channels c16); its plane
@@ -599,6 +604,21 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     v4i pfA[2][4];
     load_stage(pfA, ahead);
     advance(ahead);
+    // 3x3 kernels on 64-channel chunks (kc = 576: 64 rows of 36 16-byte
+    // pieces, 9 per thread): the next chunk's weights are loaded into
+    // registers while the current stage computes, as the input pieces are
+    constexpr bool kWpf = K33 > 0 && NCB == 1;  // with 32-position tiles the registers do not suffice
+    constexpr int kWq = kWpf ? 9 : 1;
+    v4i wf[kWq];
+    auto load_weights = [&](uint32_t cc) {
+        const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad + og * kLinOTile) * L.kc;
+#pragma unroll
+        for (int q = 0; q < kWq; ++q) {
+            const uint32_t e = tid + kLinBlock * q, rr = e / 36, p = e % 36;
+            wf[q] = *reinterpret_cast<const v4i *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * p);
+        }
+    };
+    if constexpr (kWpf) load_weights(0);
 
     // One stage with the pieces in pf; returns false after the last stage.
     auto stage = [&](v4i (&pf)[2][4]) -> bool {
@@ -620,20 +640,31 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
             for (int ob = 0; ob < 4; ++ob)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int32_t b0 = static_cast<int32_t>(base[ob][r] + negb[ob][r] * Rj);
+                    const int32_t b0 = static_cast<int32_t>(sbase[o_local(ob, r)] + snegb[o_local(ob, r)] * Rj);
 #pragma unroll
                     for (int cb = 0; cb < NCB; ++cb) acc[ob][cb][r] = b0;
                 }
         }
         __syncthreads();  // the previous stage's fragments have been read
         if (L.ncc > 1 || !a_staged) {
-            // weights of chunk cc: 64 rows of kc bytes, 16 bytes per load
-            const uint8_t *ap = prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad + og * kLinOTile) * L.kc;
-            const uint32_t per_row = L.kc / 16;
-            for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
-                const uint32_t rr = e / per_row, q = e % per_row;
-                *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
-                    *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
+            if constexpr (kWpf) {
+                // weights of chunk cc from the registers, then the next chunk's
+#pragma unroll
+                for (int q = 0; q < kWq; ++q) {
+                    const uint32_t e = tid + kLinBlock * q, rr = e / 36, p = e % 36;
+                    *reinterpret_cast<v4i *>(Al + rr * L.astride + 16 * p) = wf[q];
+                }
+                if (L.ncc > 1) load_weights(cc + 1 < L.ncc ? cc + 1 : 0u);
+            } else {
+                // weights of chunk cc: 64 rows of kc bytes, 16 bytes per load
+                const uint8_t *ap =
+                    prep + ((static_cast<uint64_t>(i) * L.ncc + cc) * L.o_pad + og * kLinOTile) * L.kc;
+                const uint32_t per_row = L.kc / 16;
+                for (uint32_t e = tid; e < kLinOTile * per_row; e += kLinBlock) {
+                    const uint32_t rr = e / per_row, q = e % per_row;
+                    *reinterpret_cast<uint4 *>(Al + rr * L.astride + 16 * q) =
+                        *reinterpret_cast<const uint4 *>(ap + static_cast<uint64_t>(rr) * L.kc + 16 * q);
+                }
             }
             a_staged = true;
         }

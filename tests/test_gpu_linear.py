@@ -63,6 +63,10 @@ SMALL = [
     ("conv-5x1-two-chunks", (3, 4, 5, 13), (2, 119, 9, 6), 5, 5, 1, 1, 0),
     ("conv-2x1-stride3-two-chunks", (3, 4, 5, 13), (2, 119, 9, 6), 5, 2, 1, 3, 0),
     ("conv-1x3", (2, 3, 5, 7, 11), (1, 33, 5, 12), 9, 1, 3, 1, 0),
+    # several 64-channel chunks, 3x3, rows of at most 16 outputs: the next
+    # chunk's weights are loaded into registers while a stage computes
+    ("conv3x3-three-chunks-7x7", (2, 3, 5, 7, 37), (1, 192, 7, 7), 64, 3, 3, 1, 1),
+    ("conv3x3-two-chunks-stride2", (3, 5, 7, 31), (1, 128, 14, 14), 70, 3, 3, 2, 1),
 ]
 
 
