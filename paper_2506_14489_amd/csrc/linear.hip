@@ -88,6 +88,7 @@ struct LinPlan {
     uint32_t halo;                // LDS bytes of one residue's staged input (kh xw xstride)
     uint32_t lds_a, lds_b, lds_o, lds_bytes;
     uint32_t npairs;
+    uint32_t word_split;          // k_linear_gemm: one workgroup per packed word (else per modulus)
     uint64_t n_in, n_out;         // activations
     uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
@@ -280,6 +281,13 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         }
     }
     L->npairs = np;
+    // Several channel chunks: a workgroup per packed word rather than per
+    // modulus when the per-modulus grid is small: the small moduli, with the
+    // most residues (128 for m = 2, 25 for 37 at 128-bit labels), would
+    // otherwise set the launch's length; measured slower on large grids,
+    // where the chip is full either way.
+    const uint64_t grid_mod = static_cast<uint64_t>(L->nimg) * L->rows * L->xtiles * L->k * L->ogroups;
+    L->word_split = (L->ncc > 1 && grid_mod < 2048) ? 1u : 0u;
     L->total_planes = pl_off;
     L->rowsum_off = static_cast<uint64_t>(L->k) * L->ncc * L->o_pad * L->kc;
     return REDASH_OK;
@@ -502,11 +510,14 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     // one XCD, whose L2 then serves the shared plane rows
     const uint32_t nb = gridDim.x, full = nb / kXcds * kXcds;
     const uint32_t tile = blockIdx.x < full ? (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds : blockIdx.x;
-    const uint32_t i = blockIdx.y, og = blockIdx.z;
+    // one packed word (pair table entry blockIdx.y) or every word of modulus blockIdx.y
+    const uint32_t i = L.word_split ? L.pair_mod[blockIdx.y] : blockIdx.y, og = blockIdx.z;
     const uint32_t xtile = tile % L.xtiles;
     const uint32_t row = (tile / L.xtiles) % L.rows;
     const uint32_t img = tile / (L.xtiles * L.rows);
     const LinMod M = L.mod[i];
+    const uint32_t w_lo = L.word_split ? L.pair_word[blockIdx.y] : 0u;
+    const uint32_t w_hi = L.word_split ? w_lo + 1 : M.W;
     constexpr uint32_t XT = 16 * NCB;
     const uint32_t x0 = xtile * XT;
     const int32_t *rowsum = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
@@ -600,7 +611,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     uint32_t part[4][NCB][4];
     v4i acc[4][NCB];
     bool a_staged = false;
-    Stage cur{0, 0, 0}, ahead{0, 0, 0};
+    Stage cur{w_lo, 0, 0}, ahead{w_lo, 0, 0};
     v4i pfA[2][4];
     load_stage(pfA, ahead);
     advance(ahead);
@@ -676,7 +687,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
                     if (pval[t]) *reinterpret_cast<v4i *>(Bl + q * L.halo + loff[t]) = plane_field(pf[t][q], M, j0 + q);
             }
         // pf is free: the next stage
-        if (ahead.w < M.W) load_stage(pf, ahead);
+        if (ahead.w < w_hi) load_stage(pf, ahead);
         advance(ahead);
         __syncthreads();
         if (j < g) {
@@ -772,7 +783,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
                     dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
             }
         }
-        return cur.w < M.W;
+        return cur.w < w_hi;
     };
     while (stage(pfA)) {
     }
@@ -1075,7 +1086,8 @@ int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, co
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE, K33>), dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
+    hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE, K33>),
+                       dim3(static_cast<uint32_t>(tiles), L.word_split ? L.npairs : L.k, L.ogroups),
                        dim3(kLinBlock), L.lds_bytes, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
 }

@@ -269,6 +269,14 @@ def test_full_size_resnet18_layer(layer):
     _check_full_layer(layer, 24)
 
 
+def test_full_size_several_chunks_one_workgroup_per_modulus():
+    """Two images of ResNet-18's 128-channel 28x28 layer: a grid large enough
+    (2,688 workgroups) that the several-chunk contraction gives each modulus
+    one workgroup; the batch-1 layers above give each packed word one."""
+    w = WL._conv("l2.b-batch2", WL.PRIMES_12, (11,), 31, (2, 128, 28, 28), 128, 3, 1, 1)
+    _check_full_layer(w, 24)
+
+
 # ---------------------------------------------------------------------------
 # a layer feeding the scaling gadget: the gadget is garbled on the layer's
 # output zero-labels (redash_garble_scale_given), evaluated on its output
