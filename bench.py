@@ -99,7 +99,20 @@ def expected_values(w, x):
 MFMA_I8_PEAK_TOPS = 5000.0  # dense int8 matrix-core peak of the MI355X, TOP/s
 
 
-def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
+_VALUES = {}
+
+
+def layer_values(w):
+    """WL.make_inputs(w), computed once per workload (the exact conv outputs of
+    a ResNet-18 layer serve both its linear layer's check and its gadget)."""
+    from paper_2506_14489_amd import workloads as WL
+
+    if w not in _VALUES:
+        _VALUES[w] = WL.make_inputs(w)
+    return _VALUES[w]
+
+
+def time_linear_layer(w, params, buf, steps: int, warmup: int, dev, garble: bool = True):
     """The garbled conv layer that produces workload w's activations (Y = sum w X
     on the labels of its int8 inputs), on the gadget's garbled input labels:
     prepare the weights, garble the output zero-labels, time the evaluator,
@@ -111,9 +124,15 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     from paper_2506_14489_amd import workloads as WL
 
     a, wt = WL.layer_operands(w)
-    n, c_in, h, wd = w.in_shape
-    c_out, _, kh, kw = w.w_shape
-    lp = B.make_linear_params(w.moduli, n, c_in, h, wd, c_out, kh, kw, w.stride, w.pad)
+    if w.kind == "fc":  # a dense layer: 1x1 kernel over `batch` positions of one row
+        (n, c_in), (c_out, _) = w.in_shape, w.w_shape
+        h, wd, kh, kw, stride, pad = 1, 1, 1, 1, 1, 0
+        lp = B.make_linear_params(w.moduli, n, c_in, 1, 1, c_out)
+    else:
+        n, c_in, h, wd = w.in_shape
+        c_out, _, kh, kw = w.w_shape
+        stride, pad = w.stride, w.pad
+        lp = B.make_linear_params(w.moduli, n, c_in, h, wd, c_out, kh, kw, stride, pad)
     sz = B.redash_linear_plan(lp)
     stream = torch.cuda.current_stream()
     n_in = n * c_in * h * wd
@@ -147,9 +166,10 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     torch.cuda.synchronize()
     g0 = torch.cuda.Event(enable_timing=True)
     g1 = torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
-    g1.record(stream)
+    if garble:
+        g0.record(stream)
+        B.redash_linear_garble(lp, buf.in_zero, prep, None, buf.offsets, work, Z, stream)
+        g1.record(stream)
     n_out = w.n
     dp = B.make_params(w.moduli, w.scale_idx, n_out, w.seed)
     y = torch.empty(n_out, dtype=torch.int64, device=dev)
@@ -157,26 +177,65 @@ def time_linear_layer(w, params, buf, steps: int, warmup: int, dev):
     B.redash_decode(dp, Y, Z, buf.offsets, y, bad, stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / steps
-    ok = int(bad.item()) == 0 and np.array_equal(y.cpu().numpy(), WL.make_inputs(w))
+    ok = int(bad.item()) == 0 and np.array_equal(y.cpu().numpy(), layer_values(w))
     if not ok:
-        log("linear layer: decode check FAILED")
+        log(f"linear layer {w.name}: decode check FAILED")
         sys.exit(1)
     ops = cost.linear_ops_per_output(w.moduli, c_in, kh, kw) * n_out
     tops = ops / (ms / 1e3) / 1e12
     gbs = cost.linear_bytes(w.moduli, n_in, n_out) / (ms / 1e3) / 1e9
-    log(f"linear layer: eval {ms:.3f} ms per call, {tops:.0f} TOP/s")
-    return {
-        "layer": f"conv {kh}x{kw} stride {w.stride} pad {w.pad}, {c_in}->{c_out} channels, input {list(w.in_shape)}, "
-                 f"{len(w.moduli)} moduli",
+    log(f"linear layer {w.name}: eval {ms:.3f} ms per call, {tops:.0f} TOP/s")
+    r = {
+        "layer": (f"dense {c_in}->{c_out}, batch {n}" if w.kind == "fc" else
+                  f"conv {kh}x{kw} stride {stride} pad {pad}, {c_in}->{c_out} channels, input {list(w.in_shape)}")
+                 + f", {len(w.moduli)} moduli",
         "ms_per_call": round(ms, 4),
         "outputs_per_s": round(n_out / (ms / 1e3), 1),
         "roofline": {"bound": "mfma", "achieved": round(tops, 1), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOP/s",
                      "frac": round(tops / MFMA_I8_PEAK_TOPS, 4), "dtype": "i8",
                      "ops_per_output": cost.linear_ops_per_output(w.moduli, c_in, kh, kw), "kernel": "k_linear"},
         "hbm": {"achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)},
-        "garble_ms": round(g0.elapsed_time(g1), 4),
         "check": "decode(eval labels, garbler zero-labels) = exact integer convolution, all outputs",
         "steps": steps,
+    }
+    if garble:
+        r["garble_ms"] = round(g0.elapsed_time(g1), 4)
+    return r
+
+
+def time_resnet18_linear(steps: int, warmup: int, dev):
+    """The 21 garbled linear layers of ResNet-18 at batch 1 (20 convolutions and
+    the dense layer), each on input labels garbled for its own input size:
+    sum of the per-layer evaluation times, every output decoded and checked."""
+    import torch
+
+    from paper_2506_14489_amd import binding as B
+    from paper_2506_14489_amd import cost
+    from paper_2506_14489_amd import workloads as WL
+
+    layers, ms_tot, ops_tot = [], 0.0, 0
+    for w in WL.RESNET18:
+        n_in = int(np.prod(w.in_shape))
+        params = B.make_params(w.moduli, w.scale_idx, n_in, w.seed)
+        buf = B.Buffers(params, dev)
+        B.redash_garble_scale(params, buf.offsets, buf.in_zero, buf.out_zero, buf.tables, buf.work,
+                              torch.cuda.current_stream())
+        r = time_linear_layer(w, params, buf, steps, warmup, dev, garble=False)
+        c_in = w.in_shape[1]
+        kh, kw = (1, 1) if w.kind == "fc" else w.w_shape[2:]
+        ops_tot += cost.linear_ops_per_output(w.moduli, c_in, kh, kw) * w.n
+        ms_tot += r["ms_per_call"]
+        layers.append({"layer": w.name, "shape": r["layer"], "ms_per_call": r["ms_per_call"],
+                       "int8_frac": r["roofline"]["frac"]})
+        del buf
+        torch.cuda.empty_cache()
+    tops = ops_tot / (ms_tot / 1e3) / 1e12
+    log(f"resnet18 linear layers: {ms_tot:.3f} ms over {len(layers)} layers")
+    return {
+        "ms_total": round(ms_tot, 4),
+        "int8_frac": round(tops / MFMA_I8_PEAK_TOPS, 4),
+        "check": "every layer: decode(eval labels, garbler zero-labels) = exact integer layer output",
+        "layers": layers,
     }
 
 
@@ -191,7 +250,7 @@ def time_workload(w, steps: int, warmup: int, dev, values: str = "values uniform
     from paper_2506_14489_amd import workloads as WL
 
     n = w.n
-    x = WL.make_inputs(w)
+    x = layer_values(w) if w.kind in ("conv", "fc") else WL.make_inputs(w)
     params = B.make_params(w.moduli, w.scale_idx, n, w.seed)
     buf = B.Buffers(params, dev)
     stream = torch.cuda.current_stream()
@@ -333,7 +392,8 @@ def main():
     ap.add_argument("--garble-steps", type=int, default=3,
                     help="timed garbler calls (offline phase, reported beside the evaluator; 0 skips)")
     ap.add_argument("--no-linear", action="store_true",
-                    help="skip timing the garbled conv layer that produces the workload's activations")
+                    help="skip timing the garbled conv layer that produces the workload's activations "
+                         "(and the ResNet-18 linear layers)")
     ap.add_argument("--no-resnet18", action="store_true",
                     help="skip timing the 21 ResNet-18 layers (sum of gadgets over sum of per-layer times)")
     ap.add_argument("--no-short-bases", action="store_true",
@@ -373,7 +433,7 @@ def main():
     n = w.n
     log(f"workload {w.name}: {n} gadgets, moduli {w.moduli}, s = {w.s}, seed {w.seed}")
     t0 = time.time()
-    x = WL.make_inputs(w)
+    x = layer_values(w) if w.kind in ("conv", "fc") else WL.make_inputs(w)
     log(f"inputs ready in {time.time() - t0:.1f} s")
 
     dev = torch.device("cuda:0")
@@ -546,6 +606,8 @@ def main():
                                                args.warmup, dev) for sw in WL.SHORT_BASES]
     if not args.no_resnet18:
         result["resnet18"] = time_resnet18(max(args.steps // 2, 1), args.warmup, dev)
+    if not args.no_linear and not args.no_resnet18:
+        result["resnet18_linear"] = time_resnet18_linear(max(args.steps // 2, 1), args.warmup, dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, x, min(args.cpu_sample, n), args.cpu_seconds,
                                               slices=not args.no_cpu_slices)
