@@ -89,6 +89,7 @@ struct LinPlan {
     uint32_t lds_a, lds_b, lds_o, lds_bytes;
     uint32_t npairs;
     uint32_t word_split;          // k_linear_gemm: one workgroup per packed word (else per modulus)
+    uint32_t fold_c;              // column fold (see the plan): the layer's own c_in, else 0
     uint64_t n_in, n_out;         // activations
     uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
@@ -175,22 +176,40 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         L->oX = 1;
     }
     L->taps = static_cast<uint32_t>(taps);
+    // Column fold: with few input channels the kw columns of a kernel row
+    // become kw c_in channels of a kh x 1 kernel (plane byte (y, x, dx c_in +
+    // c) holds input (y, x + dx, c)), so that a K slice carries kw c_in
+    // weights instead of c_in and up to 16 - c_in zeros (the 7x7 stride-2
+    // stem over 3 channels: 4 K steps of 64 instead of 13), where the staged
+    // halo of a 16-position tile still fits (kh (15 stride + 1) 16-byte
+    // pieces per channel chunk of 16, 32 or 64).  From here on c_in, kw and
+    // taps are those of the folded layer.
+    L->fold_c = 0;
+    const uint32_t cf = p->kw * p->c_in, ckf = cf <= 16 ? 16u : cf <= 32 ? 32u : 64u;
+    if (!dense && p->kw > 1 && p->c_in < 16 && cf <= 64 &&
+        p->kh * (15 * p->stride + 1) * (ckf / 16) <= 2 * kLinBlock) {
+        L->fold_c = p->c_in;
+        L->c_in = p->kw * p->c_in;
+        L->kw = 1;
+        L->taps = p->kh;
+    }
     // channel chunk: 64, or fewer when the channels are few or the taps many
-    const uint32_t cin16 = round_up(p->c_in, 16);
+    const uint32_t cin16 = round_up(L->c_in, 16);
     uint32_t ck = 64;
     while (ck > 16 && (ck / 2 >= cin16 || round_up(L->taps * ck, 64) > 1024)) ck /= 2;
     L->ck = ck;
     L->lg_ck = ck == 64 ? 6 : ck == 32 ? 5 : 4;
     L->kc = round_up(L->taps * ck, 64);
-    L->ncc = (p->c_in + ck - 1) / ck;
+    L->ncc = (L->c_in + ck - 1) / ck;
     L->cp = L->ncc * ck;
     L->hp = L->in_rows + 2 * p->pad;
-    L->wp = L->in_cols + 2 * p->pad;
+    // folded: plane column x serves output column x / stride
+    L->wp = L->fold_c ? (L->cols - 1) * p->stride + 1 : L->in_cols + 2 * p->pad;
     // M = ceil(2^16 / kw) <= 2^16: with e = M kw - 2^16 < kw, (t M) >> 16 =
     // floor(t/kw + t e / (kw 2^16)), and t e / 2^16 < 64 kw / 2^16 < 1 keeps
     // the error below 1/kw for every tap t < 64 and kw <= 64 (t M < 2^22: a
     // 24-bit multiply).  (2^32 / kw would not fit 32 bits for kw = 1.)
-    L->kw_magic = ((1u << 16) + p->kw - 1) / p->kw;
+    L->kw_magic = ((1u << 16) + L->kw - 1) / L->kw;
     L->o_pad = round_up(p->c_out, kLinOTile);
     L->ogroups = L->o_pad / kLinOTile;
     // 16-byte LDS reads of 16 rows (or columns) at a stride of S bytes, four
@@ -218,13 +237,13 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     // 16-byte pieces per residue (two per thread)
     L->xt = 32;
     while (L->xt > 16 && L->xt / 2 >= L->cols) L->xt /= 2;
-    auto pieces = [&](uint32_t xt) { return L->kh * ((xt - 1) * p->stride + p->kw) * (ck / 16); };
+    auto pieces = [&](uint32_t xt) { return L->kh * ((xt - 1) * p->stride + L->kw) * (ck / 16); };
     if (L->xt == 32 && pieces(32) > 2 * kLinBlock) L->xt = 16;
     // a 3x3 kernel over several 64-channel chunks keeps the next chunk's
     // weights in registers, which only the 16-position tile has room for
     if (L->ncc > 1 && ck == 64 && p->kh == 3 && p->kw == 3) L->xt = 16;
     if (pieces(L->xt) > 2 * kLinBlock) return REDASH_E_PARAM;
-    L->xw = (L->xt - 1) * p->stride + p->kw;
+    L->xw = (L->xt - 1) * p->stride + L->kw;
     L->halo = L->kh * L->xw * L->xstride;
     L->ostride = L->xt + 4;  // the four lane groups of an atomic OR fall 16 banks apart
     L->lds_b = 4 * L->halo;
@@ -260,7 +279,7 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         // |sum w v| <= K floor(m/2) (m - 1) =: B (signed weights, residues v < m);
         // u = sum w v + off (+ (-b mod m) R_j, below m^2) lies in [0, 2B + m^2),
         // below 2^31 for K <= 16384, and u / m < 2^23 (a signed 24-bit product)
-        const uint64_t K = static_cast<uint64_t>(L->taps) * p->c_in;
+        const uint64_t K = static_cast<uint64_t>(L->taps) * L->c_in;
         const uint64_t B = K * (mc.m / 2) * (mc.m - 1);
         lm.off = static_cast<uint32_t>((B + mc.m - 1) / mc.m * mc.m);
         const uint64_t u_max = lm.off + B + static_cast<uint64_t>(mc.m) * mc.m;
@@ -331,8 +350,15 @@ __global__ void __launch_bounds__(256) k_linear_prepare(const LinPlan L, const i
         const uint32_t i = static_cast<uint32_t>(r / L.ncc);
         const uint32_t tap = kb / L.ck, c = cc * L.ck + kb % L.ck;
         int32_t v = 0;
-        if (o < L.c_out && c < L.c_in && tap < L.taps)
-            v = signed_residue(wts[(static_cast<uint64_t>(o) * L.c_in + c) * L.taps + tap], L.mod[i].m);
+        if (o < L.c_out && c < L.c_in && tap < L.taps) {
+            // folded: channel c = dx c_in' + c' of kernel row tap is weight
+            // (o, c', tap, dx) of the layer's kh x kw kernel (kw = c_in / c_in')
+            const uint32_t kw0 = L.fold_c ? L.c_in / L.fold_c : 1u;
+            const uint64_t at = L.fold_c ? (static_cast<uint64_t>(o) * L.fold_c + c % L.fold_c) * (L.taps * kw0) +
+                                               static_cast<uint64_t>(tap) * kw0 + c / L.fold_c
+                                         : (static_cast<uint64_t>(o) * L.c_in + c) * L.taps + tap;
+            v = signed_residue(wts[at], L.mod[i].m);
+        }
         prep[e] = static_cast<uint8_t>(static_cast<int8_t>(v));
     }
 }
@@ -413,7 +439,36 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
         inside = y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 && x < static_cast<int32_t>(L.in_cols);
         return inside ? (img * L.sN + static_cast<uint32_t>(y) * L.sY + static_cast<uint32_t>(x) * L.sX) * 4u : 0u;
     };
-    {
+    if (L.fold_c) {
+        // folded layer: channel c = dx c_in' + c' of plane column xp is input
+        // channel c' at padded column xp + dx; outside the input the word is
+        // 0, whose fields are the residues of the padding value 0
+        const uint32_t p = tid % 64, c16 = tid / 64, pp = pp0 + p;
+        if (pp < npos && c16 < ngrp) {
+            const uint32_t xp = pp % L.wp, t = pp / L.wp;
+            const int32_t y = static_cast<int32_t>(t % L.hp) - static_cast<int32_t>(L.pad);
+            const uint32_t img = t / L.hp;
+            const uint32_t *src = in + (static_cast<uint64_t>(M.woff) + w) * L.n_in;
+            v4i q4[4];
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t ch = cbase + 16 * c16 + static_cast<uint32_t>(4 * d + k);
+                    const uint32_t dx = ch / L.fold_c, c = ch - dx * L.fold_c;
+                    const int32_t x = static_cast<int32_t>(xp + dx) - static_cast<int32_t>(L.pad);
+                    const bool ok = ch < L.c_in && y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
+                                    x < static_cast<int32_t>(L.in_cols);
+                    const uint32_t a =
+                        ok ? (img * L.sN + static_cast<uint32_t>(y) * L.sY + static_cast<uint32_t>(x) * L.sX + c * L.sC) * 4u
+                           : 0u;
+                    const uint32_t v = load_word(src, a);
+                    q4[d][k] = static_cast<int32_t>(ok ? v : 0u);
+                }
+#pragma unroll
+            for (int d = 0; d < 4; ++d) *reinterpret_cast<v4i *>(&T[p * 68 + 16 * c16 + 4 * d]) = q4[d];
+        }
+    } else {
         const uint32_t p = tid % 64, c16 = tid / 64, pp = pp0 + p;
         if (pp < npos && c16 < ngrp) {
             bool inside = false;
@@ -442,6 +497,7 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
     if (pp >= npos || c16 >= ngrp) return;  // no barrier follows
     bool inside = false;
     (void)at(pp, inside);
+    inside = inside || L.fold_c;  // folded: padding was read as 0 words
     const uint32_t c0 = cbase + 16 * c16;
     uint32_t wd[16];
 #pragma unroll

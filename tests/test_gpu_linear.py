@@ -67,6 +67,12 @@ SMALL = [
     # chunk's weights are loaded into registers while a stage computes
     ("conv3x3-three-chunks-7x7", (2, 3, 5, 7, 37), (1, 192, 7, 7), 64, 3, 3, 1, 1),
     ("conv3x3-two-chunks-stride2", (3, 5, 7, 31), (1, 128, 14, 14), 70, 3, 3, 2, 1),
+    # column fold (fewer than 16 channels, kw c_in <= 64: kh x 1 over kw c_in channels)
+    ("fold-63-channels-m251", (2, 251), (1, 9, 11, 13), 5, 7, 7, 1, 3),
+    ("no-fold-63-channels-stride2-halo", (2, 251), (1, 9, 11, 13), 5, 7, 7, 2, 3),
+    ("fold-one-channel-5x5", (3, 5, 7, 11), (2, 1, 9, 23), 4, 5, 5, 1, 2),
+    ("fold-1x4-stride3", (2, 3, 5, 7), (1, 2, 4, 17), 6, 1, 4, 3, 0),
+    ("no-fold-65-channels", (5, 7), (1, 13, 6, 8), 3, 5, 5, 1, 2),
 ]
 
 
