@@ -90,6 +90,7 @@ struct LinPlan {
     uint32_t npairs;
     uint32_t word_split;          // k_linear_gemm: one workgroup per packed word (else per modulus)
     uint32_t fold_c;              // column fold (see the plan): the layer's own c_in, else 0
+    uint32_t fold_magic;          // floor(c / fold_c) = (c fold_magic) >> 16 for every c < 64
     uint64_t n_in, n_out;         // activations
     uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
@@ -185,10 +186,13 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     // pieces per channel chunk of 16, 32 or 64).  From here on c_in, kw and
     // taps are those of the folded layer.
     L->fold_c = 0;
+    L->fold_magic = 0;
     const uint32_t cf = p->kw * p->c_in, ckf = cf <= 16 ? 16u : cf <= 32 ? 32u : 64u;
     if (!dense && p->kw > 1 && p->c_in < 16 && cf <= 64 &&
         p->kh * (15 * p->stride + 1) * (ckf / 16) <= 2 * kLinBlock) {
         L->fold_c = p->c_in;
+        // ceil(2^16 / c_in): as for the taps below, exact for every c < 64
+        L->fold_magic = ((1u << 16) + p->c_in - 1) / p->c_in;
         L->c_in = p->kw * p->c_in;
         L->kw = 1;
         L->taps = p->kh;
@@ -455,7 +459,7 @@ __global__ void __launch_bounds__(256) k_linear_unpack(const LinPlan L, const ui
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const uint32_t ch = cbase + 16 * c16 + static_cast<uint32_t>(4 * d + k);
-                    const uint32_t dx = ch / L.fold_c, c = ch - dx * L.fold_c;
+                    const uint32_t dx = __umul24(ch, L.fold_magic) >> 16, c = ch - dx * L.fold_c;
                     const int32_t x = static_cast<int32_t>(xp + dx) - static_cast<int32_t>(L.pad);
                     const bool ok = ch < L.c_in && y >= 0 && y < static_cast<int32_t>(L.in_rows) && x >= 0 &&
                                     x < static_cast<int32_t>(L.in_cols);
