@@ -570,13 +570,16 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     // one XCD, whose L2 then serves the shared plane rows
     const uint32_t nb = gridDim.x, full = nb / kXcds * kXcds;
     const uint32_t tile = blockIdx.x < full ? (blockIdx.x % kXcds) * (nb / kXcds) + blockIdx.x / kXcds : blockIdx.x;
-    // one packed word (pair table entry blockIdx.y) or every word of modulus blockIdx.y
-    const uint32_t i = L.word_split ? L.pair_mod[blockIdx.y] : blockIdx.y, og = blockIdx.z;
+    // one packed word (pair table entry blockIdx.z, the output channel group
+    // blockIdx.y: the words of the small moduli, with the most residues, are
+    // dispatched first for every group) or every word of modulus blockIdx.y
+    const uint32_t i = L.word_split ? L.pair_mod[blockIdx.z] : blockIdx.y;
+    const uint32_t og = L.word_split ? blockIdx.y : blockIdx.z;
     const uint32_t xtile = tile % L.xtiles;
     const uint32_t row = (tile / L.xtiles) % L.rows;
     const uint32_t img = tile / (L.xtiles * L.rows);
     const LinMod M = L.mod[i];
-    const uint32_t w_lo = L.word_split ? L.pair_word[blockIdx.y] : 0u;
+    const uint32_t w_lo = L.word_split ? L.pair_word[blockIdx.z] : 0u;
     const uint32_t w_hi = L.word_split ? w_lo + 1 : M.W;
     constexpr uint32_t XT = 16 * NCB;
     const uint32_t x0 = xtile * XT;
@@ -1147,7 +1150,8 @@ int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, co
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
     hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE, K33>),
-                       dim3(static_cast<uint32_t>(tiles), L.word_split ? L.npairs : L.k, L.ogroups),
+                       L.word_split ? dim3(static_cast<uint32_t>(tiles), L.ogroups, L.npairs)
+                                    : dim3(static_cast<uint32_t>(tiles), L.k, L.ogroups),
                        dim3(kLinBlock), L.lds_bytes, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
 }
