@@ -304,13 +304,14 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
         }
     }
     L->npairs = np;
-    // Several channel chunks: a workgroup per packed word rather than per
-    // modulus when the per-modulus grid is small: the small moduli, with the
+    // A workgroup per packed word rather than per modulus (both contraction
+    // kernels) when the per-modulus grid is small: the small moduli, with the
     // most residues (128 for m = 2, 25 for 37 at 128-bit labels), would
     // otherwise set the launch's length; measured slower on large grids,
     // where the chip is full either way.
-    const uint64_t grid_mod = static_cast<uint64_t>(L->nimg) * L->rows * L->xtiles * L->k * L->ogroups;
-    L->word_split = (L->ncc > 1 && grid_mod < 2048) ? 1u : 0u;
+    const uint64_t tiles = static_cast<uint64_t>(L->nimg) * L->rows * L->xtiles;
+    const uint64_t grid_mod = (L->ncc > 1 ? tiles : (tiles + 3) / 4) * L->k * L->ogroups;  // 4 tiles per workgroup
+    L->word_split = grid_mod < 2048 ? 1u : 0u;
     L->total_planes = pl_off;
     L->rowsum_off = static_cast<uint64_t>(L->k) * L->ncc * L->o_pad * L->kc;
     return REDASH_OK;
@@ -879,8 +880,13 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
     // for the garbler (-b mod m), to be multiplied by R_j
     int32_t *seed = reinterpret_cast<int32_t *>(lds + L.lds_a + 4 * L.halo);
     int32_t *negb = seed + kLinOTile;
-    const uint32_t i = blockIdx.y, og = blockIdx.z;
+    // one packed word (pair table entry blockIdx.z, output channel group
+    // blockIdx.y) or every word of modulus blockIdx.y, as in k_linear_gemm
+    const uint32_t i = L.word_split ? L.pair_mod[blockIdx.z] : blockIdx.y;
+    const uint32_t og = L.word_split ? blockIdx.y : blockIdx.z;
     const LinMod M = L.mod[i];
+    const uint32_t w_lo = L.word_split ? L.pair_word[blockIdx.z] : 0u;
+    const uint32_t w_hi = L.word_split ? w_lo + 1 : M.W;
     if (tid < kLinOTile) {
         const int32_t *rs = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
         seed[tid] = static_cast<int32_t>((M.m > 128 ? static_cast<uint32_t>(128 * rs[tid]) : 0u) + M.off);
@@ -968,12 +974,12 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
         for (int s = 0; s < PL; ++s)
             if (lane + 64 * s < pieces) *reinterpret_cast<v4i *>(Bw + loff(s)) = plane_field(pf[s], M, j);
     };
-    load(0);
+    load(pn(w_lo, 0));
     stage(0);
     // (nw, nj): the next residue to stage; its plane is in pf once staged
-    uint32_t nw = 0, nj = 1;
-    if (nj == g_of(0)) nw = 1, nj = 0;
-    if (nw < M.W && pn(nw, nj) != 0) load(pn(nw, nj));
+    uint32_t nw = w_lo, nj = 1;
+    if (nj == g_of(w_lo)) nw = w_lo + 1, nj = 0;
+    if (nw < w_hi && pn(nw, nj) != pn(w_lo, 0)) load(pn(nw, nj));
 
     uint32_t part[4][NCB][4];
     v4i acc[4][NCB];
@@ -984,7 +990,7 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
 #pragma unroll
             for (int r = 0; r < 4; ++r) part[ob][cb][r] = 0;
 
-    for (uint32_t w = 0; w < M.W; ++w) {
+    for (uint32_t w = w_lo; w < w_hi; ++w) {
         const uint32_t g = g_of(w);
         uint32_t Rw = 0;
         if constexpr (GARBLE) Rw = offsets[M.woff + w];
@@ -1067,11 +1073,11 @@ k_linear_gemm_w(const LinPlan L, const uint8_t *__restrict__ planes, const uint8
             // the next residue's halo over this one (after this wave's reads,
             // in LDS order), then the plane of the one after into the
             // registers if it is a new plane
-            if (nw < M.W) {
+            if (nw < w_hi) {
                 stage(nj);
                 uint32_t mw = nw, mj = nj + 1;
                 if (mj == g_of(mw)) mw += 1, mj = 0;
-                if (mw < M.W && pn(mw, mj) != pn(nw, nj)) load(pn(mw, mj));
+                if (mw < w_hi && pn(mw, mj) != pn(nw, nj)) load(pn(mw, mj));
                 nw = mw;
                 nj = mj;
             }
@@ -1166,7 +1172,9 @@ int launch_gemm_w(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, 
     if (rc) return rc;
     const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
-    hipLaunchKernelGGL((k_linear_gemm_w<NCB, GARBLE, K33, PL>), dim3(static_cast<uint32_t>((tiles + 3) / 4), L.k, L.ogroups),
+    const uint32_t nb = static_cast<uint32_t>((tiles + 3) / 4);
+    hipLaunchKernelGGL((k_linear_gemm_w<NCB, GARBLE, K33, PL>),
+                       L.word_split ? dim3(nb, L.ogroups, L.npairs) : dim3(nb, L.k, L.ogroups),
                        dim3(kLinBlock), lds, stream, L, planes, prep, bias, offsets, out);
     return lin_launched();
 }
