@@ -91,6 +91,7 @@ struct LinPlan {
     uint32_t word_split;          // k_linear_gemm: one workgroup per packed word (else per modulus)
     uint32_t fold_c;              // column fold (see the plan): the layer's own c_in, else 0
     uint32_t fold_magic;          // floor(c / fold_c) = (c fold_magic) >> 16 for every c < 64
+    uint32_t flat, tile_rows;     // k_linear_gemm over the flattened plane (see the plan); rows of tiles
     uint64_t n_in, n_out;         // activations
     uint64_t plane_bytes;         // nimg hp wp cp
     uint64_t rowsum_off;          // byte offset of the row sums in the prepared buffer
@@ -249,6 +250,22 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     if (pieces(L->xt) > 2 * kLinBlock) return REDASH_E_PARAM;
     L->xw = (L->xt - 1) * p->stride + L->kw;
     L->halo = L->kh * L->xw * L->xstride;
+    L->tile_rows = L->rows;
+    // Flattened tiles for narrow rows (3x3, stride 1, several chunks, at
+    // most 8 output columns): output q = y wp + x of the padded plane reads
+    // q + dy wp + dx, so a tile of 16 consecutive q stages one run of
+    // 16 + 2 wp + 2 plane positions and reads tap (dy, dx) at offset
+    // dy wp + dx; outputs with x >= cols are dropped at the store.  A
+    // 16-position tile over a 7-position row otherwise leaves 9 of 16
+    // matrix columns idle.
+    L->flat = 0;
+    if (p->stride == 1 && L->kh == 3 && L->kw == 3 && ck == 64 && L->ncc > 1 && L->cols <= 8 && L->xt == 16) {
+        L->flat = 1;
+        L->xw = 16 + 2 * L->wp + 2;
+        L->halo = L->xw * L->xstride;
+        L->tile_rows = 1;
+        if (L->xw * (ck / 16) > 2 * kLinBlock) return REDASH_E_PARAM;  // not reached: wp <= 10
+    }
     L->ostride = L->xt + 4;  // the four lane groups of an atomic OR fall 16 banks apart
     L->lds_b = 4 * L->halo;
     // the merged output words overlay the staged inputs (used at the end of
@@ -257,7 +274,7 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     // then the accumulator seeds of the 64 output channels (base, -b mod m)
     L->lds_bytes = L->lds_a + (L->lds_b > L->lds_o ? L->lds_b : L->lds_o) + 2 * kLinOTile * 4;
     if (L->lds_bytes > kLinMaxLds) return REDASH_E_PARAM;
-    L->xtiles = (L->cols + L->xt - 1) / L->xt;
+    L->xtiles = L->flat ? (L->rows * L->wp + 15) / 16 : (L->cols + L->xt - 1) / L->xt;
     L->plane_bytes = static_cast<uint64_t>(L->nimg) * L->hp * L->wp * L->cp;
     if (L->plane_bytes >= (1ull << 32)) return REDASH_E_PARAM;  // 32-bit offsets within a plane
 
@@ -309,7 +326,7 @@ int build_lin_plan(const redash_linear_params *p, LinPlan *L) {
     // most residues (128 for m = 2, 25 for 37 at 128-bit labels), would
     // otherwise set the launch's length; measured slower on large grids,
     // where the chip is full either way.
-    const uint64_t tiles = static_cast<uint64_t>(L->nimg) * L->rows * L->xtiles;
+    const uint64_t tiles = static_cast<uint64_t>(L->nimg) * L->tile_rows * L->xtiles;
     const uint64_t grid_mod = (L->ncc > 1 ? tiles : (tiles + 3) / 4) * L->k * L->ogroups;  // 4 tiles per workgroup
     L->word_split = grid_mod < 2048 ? 1u : 0u;
     L->total_planes = pl_off;
@@ -577,8 +594,8 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     const uint32_t i = L.word_split ? L.pair_mod[blockIdx.z] : blockIdx.y;
     const uint32_t og = L.word_split ? blockIdx.y : blockIdx.z;
     const uint32_t xtile = tile % L.xtiles;
-    const uint32_t row = (tile / L.xtiles) % L.rows;
-    const uint32_t img = tile / (L.xtiles * L.rows);
+    const uint32_t row = (tile / L.xtiles) % L.tile_rows;
+    const uint32_t img = tile / (L.xtiles * L.tile_rows);
     const LinMod M = L.mod[i];
     const uint32_t w_lo = L.word_split ? L.pair_word[blockIdx.z] : 0u;
     const uint32_t w_hi = L.word_split ? w_lo + 1 : M.W;
@@ -587,7 +604,8 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     const int32_t *rowsum = reinterpret_cast<const int32_t *>(prep + L.rowsum_off) + i * L.o_pad + og * kLinOTile;
     const uint32_t ksteps = L.kc / 64;
     const uint32_t kg = 16 * (lane / 16);
-    const uint32_t rowb = L.xw * L.xstride;
+    // staged bytes between kernel rows: a row of the halo, or wp positions of the flattened run
+    const uint32_t rowb = (L.flat ? L.wp : L.xw) * L.xstride;
 
     // output channel of element r of row block ob for this lane
     auto o_local = [&](int ob, int r) -> uint32_t { return ob * 16 + 4 * (lane / 16) + r; };
@@ -619,7 +637,7 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
     // offset (the column clamped into the padded row: the columns past the
     // row feed outputs that are dropped) and its LDS offset.
     const uint32_t c16n = L.ck / 16;
-    const uint32_t pieces = L.kh * L.xw * c16n;
+    const uint32_t pieces = (L.flat ? 1u : L.kh) * L.xw * c16n;
     uint32_t poff[2], loff[2];
     bool pval[2];
 #pragma unroll
@@ -634,7 +652,8 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
         const uint32_t grp = 2 * L.wpair, gb = xin - xin % grp;
         if (gb + grp <= L.xw) xin = gb + (xin - gb) / 2 + ((xin - gb) % 2) * L.wpair;
         uint32_t xp = x0 * L.stride + xin;
-        xp = xp < L.wp ? xp : L.wp - 1;
+        const uint32_t xlim = L.flat ? L.hp * L.wp : L.wp;  // flattened: the image's last position
+        xp = xp < xlim ? xp : xlim - 1;
         poff[t] = ((img * L.hp + row * L.stride + dy) * L.wp + xp) * L.cp + 16 * c16;
         loff[t] = dy * rowb + xin * L.xstride + 16 * c16;
     }
@@ -842,9 +861,14 @@ k_linear_gemm(const LinPlan L, const uint8_t *__restrict__ planes, const uint8_t
             uint32_t *dstp = out + (static_cast<uint64_t>(M.woff) + w) * L.n_out;
             for (uint32_t e = tid; e < kLinOTile * XT; e += kLinBlock) {
                 const uint32_t ol = e / XT, xl = e % XT;
-                const uint32_t o = og * kLinOTile + ol, x = x0 + xl;
-                if (o < L.c_out && x < L.cols)
-                    dstp[img * L.oN + o * L.oO + row * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
+                const uint32_t o = og * kLinOTile + ol;
+                uint32_t y = row, x = x0 + xl;
+                if (L.flat) {
+                    y = x / L.wp;
+                    x -= y * L.wp;
+                }
+                if (o < L.c_out && x < L.cols && y < L.rows)
+                    dstp[img * L.oN + o * L.oO + y * L.oY + x * L.oX] = Ol[ol * L.ostride + xl];
             }
         }
         return cur.w < w_hi;
@@ -1153,7 +1177,7 @@ int launch_gemm(const LinPlan &L, const uint8_t *planes, const uint8_t *prep, co
                 const uint32_t *offsets, uint32_t *out, hipStream_t stream) {
     int rc = lin_allow_lds(reinterpret_cast<const void *>(&k_linear_gemm<NCB, GARBLE, K33>), L.lds_bytes);
     if (rc) return rc;
-    const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.rows * L.xtiles;
+    const uint64_t tiles = static_cast<uint64_t>(L.nimg) * L.tile_rows * L.xtiles;
     if (tiles >= (1ull << 31)) return REDASH_E_PARAM;
     hipLaunchKernelGGL((k_linear_gemm<NCB, GARBLE, K33>),
                        L.word_split ? dim3(static_cast<uint32_t>(tiles), L.ogroups, L.npairs)

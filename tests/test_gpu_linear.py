@@ -67,6 +67,9 @@ SMALL = [
     # chunk's weights are loaded into registers while a stage computes
     ("conv3x3-three-chunks-7x7", (2, 3, 5, 7, 37), (1, 192, 7, 7), 64, 3, 3, 1, 1),
     ("conv3x3-two-chunks-stride2", (3, 5, 7, 31), (1, 128, 14, 14), 70, 3, 3, 2, 1),
+    # flattened tiles (3x3 stride 1 over several chunks, rows of at most 8 outputs)
+    ("flat-narrow-batch2-ragged", (2, 3, 5, 7, 37), (2, 128, 5, 6), 70, 3, 3, 1, 1),
+    ("flat-narrow-nopad-m251", (3, 5, 251), (1, 130, 9, 10), 9, 3, 3, 1, 0),
     # column fold (fewer than 16 channels, kw c_in <= 64: kh x 1 over kw c_in channels)
     ("fold-63-channels-m251", (2, 251), (1, 9, 11, 13), 5, 7, 7, 1, 3),
     ("no-fold-63-channels-stride2-halo", (2, 251), (1, 9, 11, 13), 5, 7, 7, 2, 3),
